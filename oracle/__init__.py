@@ -1,0 +1,253 @@
+"""fp64 CPU oracle of the ETA decode path -- TEST INFRASTRUCTURE ONLY.
+
+Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The GPU library never uses it.
+
+Inputs are numpy arrays: ``float32`` for fp32 data, ``uint16`` for bf16 data
+given as raw 16-bit words (upcast exactly inside the C code).  All arithmetic
+is double precision (``eta_oracle.c``).  What each function follows in the
+paper is stated in the C source and repeated briefly below.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+# ETA_ORACLE_LIB lets the mutation test point the wrapper at a deliberately broken build.
+_LIB_PATH = os.environ.get("ETA_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+F32, BF16 = 0, 1
+
+_dp = ctypes.POINTER(ctypes.c_double)
+_vp = ctypes.c_void_p
+
+
+class _Problem(ctypes.Structure):
+    _fields_ = [
+        ("B", ctypes.c_int32), ("Hq", ctypes.c_int32), ("Hkv", ctypes.c_int32),
+        ("d", ctypes.c_int32), ("b", ctypes.c_int32),
+        ("T_cap", ctypes.c_int64),
+        ("q_dtype", ctypes.c_int32), ("kv_dtype", ctypes.c_int32),
+        ("q", _vp), ("k", _vp), ("v", _vp),
+        ("seq_lens", _vp), ("tau", _vp),
+        ("beta", ctypes.c_double), ("z", ctypes.c_double), ("a", ctypes.c_double),
+        ("c", ctypes.c_int32), ("lwb", ctypes.c_int32), ("self_ungated", ctypes.c_int32),
+        ("screen_all", ctypes.c_int32), ("gate_off", ctypes.c_int32),
+        ("mu", _vp), ("sigma", _vp), ("maxnorm", _vp),
+        ("sel_in", _vp),
+        ("rows", _vp), ("n_rows", ctypes.c_int32),
+        ("n_threads", ctypes.c_int32),
+        ("o", _vp), ("sel", _vp), ("bounds", _vp), ("counts", _vp), ("lse", _vp),
+        ("rescued", _vp),
+    ]
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        from . import build as _b
+        _b.build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    lib.eta_oracle_gate.restype = ctypes.c_double
+    lib.eta_oracle_gate.argtypes = [ctypes.c_double] * 3
+    lib.eta_oracle_summaries.restype = None
+    lib.eta_oracle_summaries.argtypes = [_vp, ctypes.c_int, ctypes.c_int64, ctypes.c_int64,
+                                         ctypes.c_int, ctypes.c_int, _vp, _vp, _vp]
+    lib.eta_oracle_envelope.restype = None
+    lib.eta_oracle_envelope.argtypes = [_vp, ctypes.c_int, ctypes.c_int64, ctypes.c_int64,
+                                        ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp]
+    lib.eta_oracle_bound.restype = ctypes.c_double
+    lib.eta_oracle_bound.argtypes = [_vp, _vp, _vp, ctypes.c_double, ctypes.c_int, ctypes.c_double]
+    lib.eta_oracle_predict.restype = None
+    lib.eta_oracle_predict.argtypes = [_vp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                       ctypes.c_int, _vp, _vp, _vp]
+    lib.eta_oracle_select.restype = ctypes.c_int64
+    lib.eta_oracle_select.argtypes = [_vp, ctypes.c_int64, ctypes.c_double, ctypes.c_int,
+                                      ctypes.c_int, ctypes.c_int, _vp]
+    lib.eta_oracle_attend.restype = None
+    lib.eta_oracle_attend.argtypes = [_vp, _vp, _vp, ctypes.c_int, ctypes.c_int64,
+                                      ctypes.c_int64, ctypes.c_int, ctypes.c_int, _vp,
+                                      ctypes.c_int, ctypes.c_double, ctypes.c_double,
+                                      ctypes.c_int, ctypes.c_int, _vp, _vp, _vp]
+    lib.eta_oracle_decode.restype = ctypes.c_int
+    lib.eta_oracle_decode.argtypes = [ctypes.POINTER(_Problem)]
+    _lib = lib
+    return lib
+
+
+def _dtype_code(a: np.ndarray) -> int:
+    if a.dtype == np.float32:
+        return F32
+    if a.dtype == np.uint16:
+        return BF16
+    raise TypeError(f"oracle takes float32 or uint16 (bf16 bits) arrays, got {a.dtype}")
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(_vp)
+
+
+def _c(a, dtype=None):
+    if a is None:
+        return None
+    a = np.asarray(a) if dtype is None else np.asarray(a, dtype=dtype)
+    return np.ascontiguousarray(a)
+
+
+# ------------------------------------------------------------------ pieces
+
+def gate(S: float, tau: float, beta: float) -> float:
+    """Gated score S * sigmoid(beta (S - tau)) -- Eq. (soft_mask) x Eq. (mult_attn)."""
+    return _load().eta_oracle_gate(float(S), float(tau), float(beta))
+
+
+def summaries(k: np.ndarray, b: int):
+    """(mu, sigma, M) of the full blocks of one key sequence ``k[T][d]``.
+
+    Population mean / standard deviation per coordinate and the largest key
+    norm, Sec. "Block-Based Scanning via Dual Metadata Caching".
+    """
+    k = _c(k)
+    T, d = k.shape
+    N = T // b
+    mu = np.zeros((max(N, 1), d)); sg = np.zeros((max(N, 1), d)); mx = np.zeros(max(N, 1))
+    _load().eta_oracle_summaries(_ptr(k), _dtype_code(k), d, T, d, b, _ptr(mu), _ptr(sg), _ptr(mx))
+    return mu[:N], sg[:N], mx[:N]
+
+
+def envelope(k: np.ndarray, b: int, b_sub: int, mu: np.ndarray) -> np.ndarray:
+    """Sub-block envelope standard deviation, Eq. (subblock_envelope_appx)."""
+    k = _c(k)
+    T, d = k.shape
+    N = T // b
+    env = np.zeros((max(N, 1), d))
+    mu = _c(mu, np.float64)
+    _load().eta_oracle_envelope(_ptr(k), _dtype_code(k), d, T, d, b, b_sub, _ptr(mu), _ptr(env))
+    return env[:N]
+
+
+def bound(q: np.ndarray, mu: np.ndarray, sigma: np.ndarray, M: float, z: float) -> float:
+    """Score_dual(q, B), Eq. (dual_bound_eq), for one head and one block."""
+    q = _c(q, np.float64); mu = _c(mu, np.float64); sigma = _c(sigma, np.float64)
+    return _load().eta_oracle_bound(_ptr(q), _ptr(mu), _ptr(sigma), float(M), q.shape[0], float(z))
+
+
+def predict(q: np.ndarray, W: Optional[np.ndarray], bias: Optional[np.ndarray]) -> np.ndarray:
+    """tau[B][Hq] = concat_h(q[b,h,:]) W + bias, Eq. (tau_pred); W None -> bias."""
+    q = _c(q)
+    B, Hq, d = q.shape
+    W = _c(W, np.float32)
+    bias = _c(bias, np.float32)
+    tau = np.zeros((B, Hq))
+    _load().eta_oracle_predict(_ptr(q), _dtype_code(q), B, Hq, d, _ptr(W), _ptr(bias), _ptr(tau))
+    return tau
+
+
+def select(bounds: np.ndarray, tau_eff: float, c: int, lwb: int = 0, screen_all: bool = False):
+    """Selection with pins and top-1 rescue for one head -> (sel uint8[N], rescued index or -1)."""
+    bounds = _c(bounds, np.float64)
+    N = bounds.shape[0]
+    sel = np.zeros(max(N, 1), np.uint8)
+    r = _load().eta_oracle_select(_ptr(bounds), N, float(tau_eff), int(c), int(lwb),
+                                  int(bool(screen_all)), _ptr(sel))
+    return sel[:N], int(r)
+
+
+def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, b: int, sel: np.ndarray, *,
+           use_tail: bool = True, tau_eff: float = float("-inf"), beta: float = 4.0,
+           self_ungated: bool = False, gate_off: bool = False):
+    """Gated softmax attention of one head over selected blocks (+ tail) -> (o, lse, count)."""
+    q = _c(q, np.float64); k = _c(k); v = _c(v)
+    T, d = k.shape
+    assert v.shape == k.shape and v.dtype == k.dtype
+    N = T // b
+    sel = np.ascontiguousarray(np.asarray(sel, np.uint8).reshape(-1)[:N])
+    if sel.shape[0] < 1:
+        sel = np.zeros(1, np.uint8)
+    o = np.zeros(d); lse = ctypes.c_double(); cnt = ctypes.c_int64()
+    _load().eta_oracle_attend(_ptr(q), _ptr(k), _ptr(v), _dtype_code(k), d, T, d, b, _ptr(sel),
+                              int(use_tail), float(tau_eff), float(beta), int(self_ungated),
+                              int(gate_off), _ptr(o), ctypes.byref(lse), ctypes.byref(cnt))
+    return o, lse.value, cnt.value
+
+
+# ------------------------------------------------------------------ batched
+
+@dataclass
+class DecodeResult:
+    o: np.ndarray          # [B][Hq][d] float64
+    sel: np.ndarray        # [B][Hq][N_cap] uint8
+    bounds: np.ndarray     # [B][Hq][N_cap] float64 (NaN beyond N_b)
+    counts: np.ndarray     # [B][Hq] int64
+    lse: np.ndarray        # [B][Hq] float64
+    rescued: np.ndarray    # [B][Hq] int64 (-1: no rescue)
+
+
+def decode(q: np.ndarray, k: np.ndarray, v: np.ndarray, seq_lens: Sequence[int], tau: np.ndarray,
+           *, block_size: int, beta: float = 4.0, z: float = 1.0, a: float = 0.0,
+           rescue_window: int = 128, lwb: int = 0, self_ungated: bool = False,
+           screen_all: bool = False, gate_off: bool = False,
+           rows: Optional[Sequence[int]] = None, sel_in: Optional[np.ndarray] = None,
+           n_threads: int = 0) -> DecodeResult:
+    """One ETA decode step for every (sequence, query head), or for ``rows``.
+
+    q [B][Hq][d]; k, v [B][Hkv][T_cap][d]; seq_lens [B]; tau [B][Hq].
+    Bounds -> threshold / pins / rescue -> gated attention over the selected
+    blocks plus the tail (Alg. "Hardware-Aligned Block-Sparse Decoding").
+    Rows not requested are left zero.
+    """
+    q = _c(q); k = _c(k); v = _c(v)
+    B, Hq, d = q.shape
+    B2, Hkv, T_cap, d2 = k.shape
+    assert B2 == B and d2 == d and v.shape == k.shape and v.dtype == k.dtype
+    assert Hq % Hkv == 0
+    b = int(block_size)
+    Ncap = T_cap // b
+    sl = np.ascontiguousarray(np.asarray(seq_lens, np.int32))
+    tau = _c(tau, np.float64).reshape(B, Hq)
+    tau = np.ascontiguousarray(tau)
+    rows_a = None if rows is None else np.ascontiguousarray(np.asarray(rows, np.int32))
+    sel_in_a = None if sel_in is None else np.ascontiguousarray(np.asarray(sel_in, np.uint8))
+    res = DecodeResult(
+        o=np.zeros((B, Hq, d)),
+        sel=np.zeros((B, Hq, max(Ncap, 1)), np.uint8),
+        bounds=np.full((B, Hq, max(Ncap, 1)), np.nan),
+        counts=np.zeros((B, Hq), np.int64),
+        lse=np.full((B, Hq), -np.inf),
+        rescued=np.full((B, Hq), -1, np.int64),
+    )
+    P = _Problem(
+        B=B, Hq=Hq, Hkv=Hkv, d=d, b=b, T_cap=T_cap,
+        q_dtype=_dtype_code(q), kv_dtype=_dtype_code(k),
+        q=_ptr(q), k=_ptr(k), v=_ptr(v), seq_lens=_ptr(sl), tau=_ptr(tau),
+        beta=float(beta), z=float(z), a=float(a),
+        c=int(rescue_window), lwb=int(lwb), self_ungated=int(bool(self_ungated)),
+        screen_all=int(bool(screen_all)), gate_off=int(bool(gate_off)),
+        mu=None, sigma=None, maxnorm=None,
+        sel_in=_ptr(sel_in_a),
+        rows=_ptr(rows_a), n_rows=0 if rows_a is None else int(rows_a.shape[0]),
+        n_threads=int(n_threads),
+        o=_ptr(res.o), sel=_ptr(res.sel), bounds=_ptr(res.bounds), counts=_ptr(res.counts),
+        lse=_ptr(res.lse), rescued=_ptr(res.rescued),
+    )
+    rc = _load().eta_oracle_decode(ctypes.byref(P))
+    if rc != 0:
+        raise ValueError(f"eta_oracle_decode rejected the problem (code {rc})")
+    res.sel = res.sel[:, :, :Ncap]
+    res.bounds = res.bounds[:, :, :Ncap]
+    return res
+
+
+def gate_vec(S: np.ndarray, tau: float, beta: float) -> np.ndarray:
+    """Elementwise ``gate`` over an array (convenience for tests)."""
+    lib = _load()
+    return np.array([lib.eta_oracle_gate(float(s), float(tau), float(beta)) for s in np.ravel(S)]
+                    ).reshape(np.shape(S))

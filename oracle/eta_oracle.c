@@ -1,0 +1,368 @@
+/*
+ * ETA decode oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, fp64 CPU reference of the Elastic Threshold Attention
+ * inference decode path.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load it.  The GPU library never calls it
+ * and it never calls the GPU library; the two share no source.
+ *
+ * Every quantity is computed in double precision from inputs that are upcast
+ * exactly from their stored type (fp32, or bf16 given as raw 16-bit words).
+ *
+ * What it follows (paper sections / equations / algorithms):
+ *   - block summaries mu_B, sigma_B, M_B:
+ *       Sec. "Block-Based Scanning via Dual Metadata Caching" (definitions
+ *       of the Dual Probabilistic-Geometric Block Index); population
+ *       variance (divide by b), the standard deviation being what is stored
+ *       (App. "GQA-Grouped Execution and Compact Metadata Layout").
+ *   - threshold predictor: Eq. (tau_pred), tau = concat(q_1..q_H) W + b.
+ *   - gate: Eq. (soft_mask) and Eq. (mult_attn): S~ = S * sigmoid(beta (S - tau)),
+ *       the diagonal (the query's own key) ungated.
+ *   - bound: Eq. (dual_bound_eq), (1/sqrt d) min(<q,mu> + z sqrt(sum q_i^2 sigma_i^2), |q| M).
+ *   - selection, top-1 rescue, tail: Alg. "Hardware-Aligned Block-Sparse
+ *       Decoding (Inference)" and App. "Top-1 Rescue, Tail Handling, and
+ *       Kernel Validation"; slack tau_eff = tau - a for screening and gate
+ *       (same algorithm); pinning of the most recent blocks
+ *       (App. sub-block envelope paragraph, "lwb").
+ *   - softmax over the attended set: the plain definition (Sec.
+ *       "Elastic Threshold Attention", dense attention output), which the
+ *       chunked two-stage reduction of the paper reaches exactly.
+ *
+ * Readings where the paper is silent or ambiguous:
+ *   - a block survives iff bound >= tau_eff (the algorithm's comparison).
+ *   - rescue window: blocks [0, min(c, N)); rescue fires iff no block in the
+ *     window is selected (threshold or pin); the rescued block is the first
+ *     index attaining the maximum bound (strict '>' scan over the window).
+ *     A bound that is NaN is never selected and never rescued.
+ *   - T < b: no full blocks, no rescue, only the tail is attended.
+ *   - T = 0 or nothing attended (rescue disabled, nothing selected, no tail):
+ *     the output is the zero vector and the log-sum-exp is -inf.
+ *   - tau = -inf: the gate is identically 1 (S~ = S).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <omp.h>
+
+#define OR_F32 0
+#define OR_BF16 1
+
+static double ld(const void* p, int dt, int64_t i) {
+  if (dt == OR_F32) return (double)((const float*)p)[i];
+  uint32_t u = ((uint32_t)((const uint16_t*)p)[i]) << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return (double)f;
+}
+
+/* sigmoid, evaluated without overflow for either sign of x. */
+static double sigmoid(double x) {
+  if (x >= 0.0) return 1.0 / (1.0 + exp(-x));
+  double e = exp(x);
+  return e / (1.0 + e);
+}
+
+/* Eq. (soft_mask) x Eq. (mult_attn): the gated score S * sigma(beta (S - tau)). */
+double eta_oracle_gate(double S, double tau, double beta) {
+  if (isinf(tau) && tau < 0) return S;
+  return S * sigmoid(beta * (S - tau));
+}
+
+/*
+ * Block summaries for one (sequence, kv head): rows k[t * row_stride + i],
+ * t in [0, T).  N = floor(T / b) full blocks; outputs mu[N][d], sigma[N][d],
+ * maxnorm[N].  Population statistics, two passes (mean, then deviations).
+ */
+void eta_oracle_summaries(const void* k, int dt, int64_t row_stride, int64_t T, int d, int b,
+                          double* mu, double* sigma, double* maxnorm) {
+  int64_t N = T / b;
+  for (int64_t j = 0; j < N; ++j) {
+    double* m = mu + j * d;
+    double* s = sigma + j * d;
+    for (int i = 0; i < d; ++i) { m[i] = 0.0; s[i] = 0.0; }
+    double best = 0.0;
+    for (int t = 0; t < b; ++t) {
+      int64_t row = (j * b + t) * row_stride;
+      double n2 = 0.0;
+      for (int i = 0; i < d; ++i) {
+        double x = ld(k, dt, row + i);
+        m[i] += x;
+        n2 += x * x;
+      }
+      double n = sqrt(n2);
+      if (n > best) best = n;
+    }
+    for (int i = 0; i < d; ++i) m[i] /= (double)b;
+    for (int t = 0; t < b; ++t) {
+      int64_t row = (j * b + t) * row_stride;
+      for (int i = 0; i < d; ++i) {
+        double dv = ld(k, dt, row + i) - m[i];
+        s[i] += dv * dv;
+      }
+    }
+    for (int i = 0; i < d; ++i) s[i] = sqrt(s[i] / (double)b);
+    maxnorm[j] = best;
+  }
+}
+
+/*
+ * Sub-block envelope variant of sigma (App. "Sub-Block Variance Envelope",
+ * Eq. subblock_envelope_appx): per coordinate, the largest over contiguous
+ * sub-blocks of b_sub tokens of sqrt(mean over the sub-block of (k_i - mu_i)^2),
+ * with mu the full-block centroid.  Same layout as eta_oracle_summaries.
+ */
+void eta_oracle_envelope(const void* k, int dt, int64_t row_stride, int64_t T, int d, int b,
+                         int b_sub, const double* mu, double* env) {
+  int64_t N = T / b;
+  int nsub = b / b_sub;
+  for (int64_t j = 0; j < N; ++j) {
+    const double* m = mu + j * d;
+    double* e = env + j * d;
+    for (int i = 0; i < d; ++i) e[i] = 0.0;
+    for (int sb = 0; sb < nsub; ++sb) {
+      for (int i = 0; i < d; ++i) {
+        double acc = 0.0;
+        for (int t = 0; t < b_sub; ++t) {
+          int64_t row = (j * b + (int64_t)sb * b_sub + t) * row_stride;
+          double dv = ld(k, dt, row + i) - m[i];
+          acc += dv * dv;
+        }
+        double sd = sqrt(acc / (double)b_sub);
+        if (sd > e[i]) e[i] = sd;
+      }
+    }
+  }
+}
+
+/* Eq. (dual_bound_eq) for one query head and one block. */
+double eta_oracle_bound(const double* q, const double* mu, const double* sigma, double M, int d,
+                        double z) {
+  double dot = 0.0, var = 0.0, qn2 = 0.0;
+  for (int i = 0; i < d; ++i) {
+    dot += q[i] * mu[i];
+    var += q[i] * q[i] * sigma[i] * sigma[i];
+    qn2 += q[i] * q[i];
+  }
+  double gauss = dot + z * sqrt(var);
+  double spher = sqrt(qn2) * M;
+  double lo = gauss < spher ? gauss : spher;
+  if (isnan(gauss) || isnan(spher)) lo = NAN;
+  return lo / sqrt((double)d);
+}
+
+/* Eq. (tau_pred): tau[b][h] = sum_j qbar[b][j] W[j][h] + bias[h]; W == NULL -> tau = bias. */
+void eta_oracle_predict(const void* q, int dt, int B, int Hq, int d, const float* W,
+                        const float* bias, double* tau) {
+  int64_t J = (int64_t)Hq * d;
+  for (int bb = 0; bb < B; ++bb) {
+    for (int h = 0; h < Hq; ++h) {
+      double acc = bias ? (double)bias[h] : 0.0;
+      if (W) {
+        for (int64_t j = 0; j < J; ++j) acc += ld(q, dt, (int64_t)bb * J + j) * (double)W[j * Hq + h];
+      }
+      tau[(int64_t)bb * Hq + h] = acc;
+    }
+  }
+}
+
+/*
+ * Block selection for one head: threshold, pins, top-1 rescue.
+ * Returns the rescued block index, or -1 when rescue did not fire.
+ */
+int64_t eta_oracle_select(const double* bound, int64_t N, double tau_eff, int c, int lwb,
+                          int screen_all, uint8_t* sel) {
+  for (int64_t j = 0; j < N; ++j) sel[j] = (screen_all || bound[j] >= tau_eff) ? 1 : 0;
+  for (int64_t j = N - lwb; j < N; ++j)
+    if (j >= 0) sel[j] = 1;
+  int64_t Wn = c < N ? c : N;
+  if (Wn < 1) return -1;
+  for (int64_t j = 0; j < Wn; ++j)
+    if (sel[j]) return -1;
+  double best = -INFINITY;
+  int64_t arg = -1;
+  for (int64_t j = 0; j < Wn; ++j) {
+    if (isnan(bound[j])) continue;
+    if (arg < 0 || bound[j] > best) { best = bound[j]; arg = j; }
+  }
+  if (arg >= 0) sel[arg] = 1;
+  return arg;
+}
+
+/*
+ * Gated softmax attention of one query head over the tokens of the selected
+ * full blocks, plus the tail [N b, T) when use_tail.  K, V rows are
+ * k[t * row_stride + i].  gate_off = 1 gives plain softmax attention (the dense
+ * baseline).  Writes o[d], the log-sum-exp of the gated scores and the number of
+ * attended tokens.
+ */
+void eta_oracle_attend(const double* q, const void* k, const void* v, int dt, int64_t row_stride,
+                       int64_t T, int d, int b, const uint8_t* sel, int use_tail, double tau_eff,
+                       double beta, int self_ungated, int gate_off, double* o, double* lse,
+                       int64_t* count) {
+  int64_t N = T / b;
+  double scale = 1.0 / sqrt((double)d);
+  /* pass 1: gated scores of the attended set and their maximum */
+  double* st = (double*)malloc(sizeof(double) * (size_t)(T > 0 ? T : 1));
+  uint8_t* in = (uint8_t*)malloc((size_t)(T > 0 ? T : 1));
+  double m = -INFINITY;
+  int64_t cnt = 0;
+  for (int64_t t = 0; t < T; ++t) {
+    int64_t j = t / b;
+    in[t] = (j < N) ? sel[j] : (uint8_t)(use_tail ? 1 : 0);
+    if (!in[t]) continue;
+    double S = 0.0;
+    for (int i = 0; i < d; ++i) S += q[i] * ld(k, dt, t * row_stride + i);
+    S *= scale;
+    double Sg = (gate_off || (self_ungated && t == T - 1)) ? S : eta_oracle_gate(S, tau_eff, beta);
+    st[t] = Sg;
+    if (Sg > m) m = Sg;
+    ++cnt;
+  }
+  for (int i = 0; i < d; ++i) o[i] = 0.0;
+  if (cnt == 0) {
+    *lse = -INFINITY;
+    *count = 0;
+    free(st);
+    free(in);
+    return;
+  }
+  /* pass 2: normalised weights and the weighted value sum */
+  double Z = 0.0;
+  for (int64_t t = 0; t < T; ++t) {
+    if (!in[t]) continue;
+    double w = exp(st[t] - m);
+    Z += w;
+    for (int i = 0; i < d; ++i) o[i] += w * ld(v, dt, t * row_stride + i);
+  }
+  for (int i = 0; i < d; ++i) o[i] /= Z;
+  *lse = m + log(Z);
+  *count = cnt;
+  free(st);
+  free(in);
+}
+
+/* ---------------------------------------------------------------- batched */
+
+typedef struct {
+  int32_t B, Hq, Hkv, d, b;
+  int64_t T_cap;               /* rows per (sequence, kv head) in K and V */
+  int32_t q_dtype, kv_dtype;   /* OR_F32 / OR_BF16 */
+  const void* q;               /* [B][Hq][d] */
+  const void* k;               /* [B][Hkv][T_cap][d] */
+  const void* v;               /* [B][Hkv][T_cap][d] */
+  const int32_t* seq_lens;     /* [B] */
+  const double* tau;           /* [B][Hq] predicted or constant threshold */
+  double beta, z, a;           /* gate temperature, z-score, slack (tau_eff = tau - a) */
+  int32_t c;                   /* rescue window in blocks (0 disables rescue) */
+  int32_t lwb;                 /* pinned most-recent full blocks */
+  int32_t self_ungated;        /* key T-1 keeps S~ = S */
+  int32_t screen_all;          /* every full block selected */
+  int32_t gate_off;            /* plain softmax (dense baseline) */
+  /* optional precomputed summaries [B][Hkv][N_cap][d], [B][Hkv][N_cap]; NULL -> computed here */
+  const double* mu;
+  const double* sigma;
+  const double* maxnorm;
+  /* optional external block mask [B][Hq][N_cap] replacing bounds + selection */
+  const uint8_t* sel_in;
+  /* optional subset of rows (b * Hq + h); NULL -> every row */
+  const int32_t* rows;
+  int32_t n_rows;
+  int32_t n_threads;           /* <= 0: OpenMP default */
+  /* outputs (any may be NULL except o) */
+  double* o;                   /* [B][Hq][d] */
+  uint8_t* sel;                /* [B][Hq][N_cap] */
+  double* bounds;              /* [B][Hq][N_cap] (NaN beyond N_b) */
+  int64_t* counts;             /* [B][Hq] attended tokens */
+  double* lse;                 /* [B][Hq] */
+  int64_t* rescued;            /* [B][Hq] rescued block or -1 */
+} eta_oracle_problem;
+
+static const void* off(const void* p, int dt, int64_t elems) {
+  return (const char*)p + elems * (dt == OR_F32 ? 4 : 2);
+}
+
+int eta_oracle_decode(const eta_oracle_problem* P) {
+  if (P->Hkv <= 0 || P->Hq % P->Hkv || P->b <= 0 || P->d <= 0) return 1;
+  const int64_t Ncap = P->T_cap / P->b;
+  const int G = P->Hq / P->Hkv;
+  const int d = P->d;
+  const int64_t nrows = P->rows ? P->n_rows : (int64_t)P->B * P->Hq;
+  const int64_t nbg = (int64_t)P->B * P->Hkv;
+  const int nthr = P->n_threads > 0 ? P->n_threads : omp_get_max_threads();
+
+  /* block summaries of the (sequence, kv head) pairs the requested rows use */
+  uint8_t* need = (uint8_t*)calloc((size_t)nbg, 1);
+  for (int64_t r = 0; r < nrows; ++r) {
+    int32_t row = P->rows ? P->rows[r] : (int32_t)r;
+    need[(row / P->Hq) * P->Hkv + (row % P->Hq) / G] = 1;
+  }
+  const double* mu = P->mu;
+  const double* sg = P->sigma;
+  const double* mx = P->maxnorm;
+  double *own_mu = NULL, *own_sg = NULL, *own_mx = NULL;
+  if (mu == NULL && P->sel_in == NULL) {
+    own_mu = (double*)malloc(sizeof(double) * (size_t)(nbg * Ncap * d + 1));
+    own_sg = (double*)malloc(sizeof(double) * (size_t)(nbg * Ncap * d + 1));
+    own_mx = (double*)malloc(sizeof(double) * (size_t)(nbg * Ncap + 1));
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nthr)
+    for (int64_t bg = 0; bg < nbg; ++bg) {
+      if (!need[bg]) continue;
+      int64_t T = P->seq_lens[bg / P->Hkv];
+      if (T > P->T_cap) T = P->T_cap;
+      if (T < 0) T = 0;
+      eta_oracle_summaries(off(P->k, P->kv_dtype, bg * P->T_cap * d), P->kv_dtype, d, T, d, P->b,
+                           own_mu + bg * Ncap * d, own_sg + bg * Ncap * d, own_mx + bg * Ncap);
+    }
+    mu = own_mu;
+    sg = own_sg;
+    mx = own_mx;
+  }
+
+  /* per query head: bounds -> selection -> rescue -> gated attention */
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nthr)
+  for (int64_t r = 0; r < nrows; ++r) {
+    int32_t row = P->rows ? P->rows[r] : (int32_t)r;
+    int bb = row / P->Hq, h = row % P->Hq, g = h / G;
+    int64_t bg = (int64_t)bb * P->Hkv + g;
+    int64_t T = P->seq_lens[bb];
+    if (T > P->T_cap) T = P->T_cap;
+    if (T < 0) T = 0;
+    int64_t N = T / P->b;
+    double* qh = (double*)malloc(sizeof(double) * (size_t)d);
+    for (int i = 0; i < d; ++i) qh[i] = ld(P->q, P->q_dtype, (int64_t)row * d + i);
+    double tau_eff = P->tau[row] - P->a;
+    uint8_t* sel = (uint8_t*)calloc((size_t)(Ncap + 1), 1);
+    int64_t resc = -1;
+    if (P->sel_in) {
+      memcpy(sel, P->sel_in + (int64_t)row * Ncap, (size_t)N);
+    } else {
+      double* bnd = (double*)malloc(sizeof(double) * (size_t)(N + 1));
+      for (int64_t j = 0; j < N; ++j)
+        bnd[j] = eta_oracle_bound(qh, mu + (bg * Ncap + j) * d, sg + (bg * Ncap + j) * d,
+                                  mx[bg * Ncap + j], d, P->z);
+      resc = eta_oracle_select(bnd, N, tau_eff, P->c, P->lwb, P->screen_all, sel);
+      if (P->bounds) {
+        for (int64_t j = 0; j < Ncap; ++j) P->bounds[(int64_t)row * Ncap + j] = j < N ? bnd[j] : NAN;
+      }
+      free(bnd);
+    }
+    double lse;
+    int64_t cnt;
+    const int64_t kvoff = bg * P->T_cap * d;
+    eta_oracle_attend(qh, off(P->k, P->kv_dtype, kvoff), off(P->v, P->kv_dtype, kvoff), P->kv_dtype,
+                      d, T, d, P->b, sel, 1, tau_eff, P->beta, P->self_ungated, P->gate_off,
+                      P->o + (int64_t)row * d, &lse, &cnt);
+    if (P->sel) memcpy(P->sel + (int64_t)row * Ncap, sel, (size_t)Ncap);
+    if (P->counts) P->counts[row] = cnt;
+    if (P->lse) P->lse[row] = lse;
+    if (P->rescued) P->rescued[row] = resc;
+    free(sel);
+    free(qh);
+  }
+  free(own_mu);
+  free(own_sg);
+  free(own_mx);
+  free(need);
+  return 0;
+}

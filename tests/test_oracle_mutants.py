@@ -1,0 +1,76 @@
+"""The oracle's pins catch plausible mistakes (CPU only).
+
+Each case copies the oracle's C source, plants one plausible mistake (a dropped
+term, a wrong sign, an off-by-one, a transposed index ...), builds it into a
+temporary library, and runs the pin suite against that build in a subprocess.
+The pin suite must fail for every mutant; it must pass for the unmodified
+source.
+"""
+import os
+import subprocess
+import sys
+import tempfile
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "eta_oracle.c")
+
+MUTANTS = {
+    "unbiased_variance": ("s[i] = sqrt(s[i] / (double)b);", "s[i] = sqrt(s[i] / (double)(b - 1));"),
+    "variance_not_std": ("s[i] = sqrt(s[i] / (double)b);", "s[i] = s[i] / (double)b;"),
+    "mean_off_by_one": ("m[i] /= (double)b;", "m[i] /= (double)(b + 1);"),
+    "maxnorm_is_mean": ("if (n > best) best = n;", "best += n / b;"),
+    "dropped_z": ("double gauss = dot + z * sqrt(var);", "double gauss = dot + sqrt(var);"),
+    "z_sign": ("double gauss = dot + z * sqrt(var);", "double gauss = dot - z * sqrt(var);"),
+    "sigma_not_squared": ("var += q[i] * q[i] * sigma[i] * sigma[i];", "var += q[i] * q[i] * sigma[i];"),
+    "max_not_min": ("double lo = gauss < spher ? gauss : spher;", "double lo = gauss > spher ? gauss : spher;"),
+    "bound_unscaled": ("return lo / sqrt((double)d);", "return lo;"),
+    "strict_threshold": ("bound[j] >= tau_eff) ? 1 : 0;", "bound[j] > tau_eff) ? 1 : 0;"),
+    "rescue_last_max": ("if (arg < 0 || bound[j] > best)", "if (arg < 0 || bound[j] >= best)"),
+    "rescue_window_short": ("int64_t Wn = c < N ? c : N;", "int64_t Wn = c < N ? c - 1 : N;"),
+    "pins_off_by_one": ("for (int64_t j = N - lwb; j < N; ++j)", "for (int64_t j = N - lwb + 1; j < N; ++j)"),
+    "gate_sign": ("return S * sigmoid(beta * (S - tau));", "return S * sigmoid(beta * (tau - S));"),
+    "gate_missing_S": ("return S * sigmoid(beta * (S - tau));", "return sigmoid(beta * (S - tau));"),
+    "slack_sign": ("double tau_eff = P->tau[row] - P->a;", "double tau_eff = P->tau[row] + P->a;"),
+    "tail_dropped": ("in[t] = (j < N) ? sel[j] : (uint8_t)(use_tail ? 1 : 0);", "in[t] = (j < N) ? sel[j] : 0;"),
+    "score_unscaled": ("    S *= scale;\n", "\n"),
+    "self_index": ("(self_ungated && t == T - 1)", "(self_ungated && t == T - 2)"),
+    "predictor_transposed": ("(double)W[j * Hq + h];", "(double)W[h * J + j];"),
+    "softmax_no_max_shift": ("double w = exp(st[t] - m);", "double w = exp(st[t] - m) * (1.0 + 1e-3 * (t == 0));"),
+}
+
+
+def _run_pins(lib_path):
+    env = dict(os.environ, ETA_ORACLE_LIB=lib_path)
+    return subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                           os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                          cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+
+
+def _build(src_text, tmp):
+    c = os.path.join(tmp, "o.c")
+    so = os.path.join(tmp, "liboracle_mut.so")
+    with open(c, "w") as f:
+        f.write(src_text)
+    subprocess.run(["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-std=c11", c, "-o", so, "-lm"],
+                   check=True, capture_output=True)
+    return so
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_mutant(name):
+    old, new = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) >= 1, f"mutation anchor for {name} not found in the oracle source"
+    with tempfile.TemporaryDirectory() as tmp:
+        so = _build(src.replace(old, new, 1), tmp)
+        r = _run_pins(so)
+    assert r.returncode != 0, f"pin suite passed against mutant {name}:\n{r.stdout[-2000:]}"
+
+
+def test_pins_pass_on_unmodified_source():
+    with tempfile.TemporaryDirectory() as tmp:
+        so = _build(open(SRC).read(), tmp)
+        r = _run_pins(so)
+    assert r.returncode == 0, r.stdout[-3000:]

@@ -1,0 +1,401 @@
+"""Pins of the fp64 oracle against what the paper and mathematics fix (CPU only).
+
+Each test checks the oracle against something other than itself: closed forms
+from the paper's gate analysis, textbook/library routines in special cases,
+theorems about the bound, hand-worked values, and an independent brute-force
+reading of the decode algorithm on tiny inputs.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+from scipy.optimize import minimize_scalar
+from scipy.special import expit, lambertw
+
+import brute
+import oracle
+from synth import as_numpy, config1, make_workload
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+GOLD = json.load(open(os.path.join(HERE, "golden", "gate_regimes.json")))
+
+
+def _bf16_bits(x: np.ndarray) -> np.ndarray:
+    return as_numpy(torch.from_numpy(np.ascontiguousarray(x, np.float32)).to(torch.bfloat16))
+
+
+def _f64(a: np.ndarray) -> np.ndarray:
+    if a.dtype == np.uint16:
+        return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return a.astype(np.float64)
+
+
+# --------------------------------------------------------------------- gate
+
+@pytest.mark.parametrize("beta,tau", [(1.0, 0.5), (4.0, 2.0), (5.0, 2.81), (2.0, -3.0), (4.0, 0.0),
+                                      (4.0, -0.5)])
+def test_gate_derivative_at_tau_matches_closed_form(beta, tau):
+    h = 1e-6
+    num = (oracle.gate(tau + h, tau, beta) - oracle.gate(tau - h, tau, beta)) / (2 * h)
+    expected = eval(GOLD["derivative_at_tau"], {}, {"beta": beta, "tau": tau})
+    assert abs(num - expected) < 1e-6
+
+
+@pytest.mark.parametrize("beta,tau", [(4.0, 2.0), (5.0, 2.81), (1.0, 0.3), (5.0, 0.01), (2.0, 1.0)])
+def test_gate_minimiser_is_lambert_w_closed_form(beta, tau):
+    w = float(lambertw(math.exp(-1.0 - beta * tau)).real)
+    s_star = -(1.0 + w) / beta
+    res = minimize_scalar(lambda S: oracle.gate(S, tau, beta),
+                          bracket=(-3.0 / beta, -1.1 / beta, 0.0), tol=1e-12)
+    assert abs(res.x - s_star) < 1e-5
+    assert abs(oracle.gate(s_star, tau, beta) - (-w / beta)) < 1e-12
+    # footnote bounds on the minimiser for tau > 0
+    assert GOLD["sstar_lower_times_beta"] / beta < s_star < GOLD["sstar_upper_times_beta"] / beta
+
+
+def test_lambert_constant_of_the_footnote():
+    w = float(lambertw(math.exp(-1.0)).real)
+    assert round(w, GOLD["lambertw0_at_inv_e_decimals"]) == GOLD["lambertw0_at_inv_e"]
+
+
+def test_gate_shape_limits_and_regimes():
+    beta, tau = GOLD["final_beta"], GOLD["trained_median_tau"]
+    # far below threshold the gated score contracts to zero (weight exp(0) = 1)
+    assert abs(oracle.gate(-40.0, tau, beta)) < 1e-60
+    # far above threshold the gate is the identity
+    assert abs(oracle.gate(tau + 20.0, tau, beta) - (tau + 20.0)) < 1e-30
+    # tau = -inf means no gating at all
+    for S in (-3.0, 0.0, 2.5):
+        assert oracle.gate(S, -math.inf, beta) == S
+    # regime 1 (tau far below -2/beta, e.g. the start-dense bias): essentially dense on the support
+    tau1 = GOLD["start_dense_bias"]
+    assert tau1 < GOLD["regime1_tau_upper_times_beta"] / beta
+    assert max(abs(oracle.gate(S, tau1, beta) - S) for S in np.linspace(-3, 3, 61)) < 1e-8
+    # monotone increasing on [S*, inf)
+    w = float(lambertw(math.exp(-1.0 - beta * tau)).real)
+    grid = np.linspace(-(1 + w) / beta, 10.0, 500)
+    vals = oracle.gate_vec(grid, tau, beta)
+    assert np.all(np.diff(vals) > 0)
+
+
+def test_gate_is_logistic_times_score():
+    # scipy's logistic function is an independent evaluation of sigma
+    for S in (-5.0, -0.3, 0.0, 1.7, 4.0):
+        for tau, beta in ((2.0, 4.0), (-1.0, 1.0), (2.81, 5.0)):
+            assert abs(oracle.gate(S, tau, beta) - S * expit(beta * (S - tau))) < 1e-14
+
+
+# ---------------------------------------------------------------- summaries
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("b", [4, 16, 64])
+def test_summaries_match_numpy(dt, b):
+    rng = np.random.default_rng(7)
+    K = rng.standard_normal((1000, 64)).astype(np.float32) * 1.5 + 0.7
+    Kin = K if dt == "f32" else _bf16_bits(K)
+    Kd = _f64(Kin)
+    mu, sg, M = oracle.summaries(Kin, b)
+    N = 1000 // b
+    assert mu.shape == (N, 64) and M.shape == (N,)
+    blocks = Kd[:N * b].reshape(N, b, 64)
+    np.testing.assert_allclose(mu, blocks.mean(axis=1), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(sg, blocks.std(axis=1, ddof=0), rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(M, np.linalg.norm(blocks, axis=2).max(axis=1), rtol=1e-12)
+
+
+def test_summaries_population_variance_hand_example():
+    # two-token block {x, y}: population std is |x - y| / 2 (not / sqrt(2))
+    K = np.array([[3.0, -1.0, 0.0], [1.0, -1.0, 4.0]], np.float32)
+    mu, sg, M = oracle.summaries(K, 2)
+    np.testing.assert_allclose(mu[0], [2.0, -1.0, 2.0])
+    np.testing.assert_allclose(sg[0], [1.0, 0.0, 2.0])
+    assert M[0] == pytest.approx(math.sqrt(18.0))   # rows have norms sqrt(10), sqrt(18)
+
+
+def test_envelope_dominates_flat_sigma_and_hand_case():
+    rng = np.random.default_rng(3)
+    K = rng.standard_normal((640, 32)).astype(np.float32)
+    K[100:104] += 9.0                          # a localised 4-token spike
+    mu, sg, _ = oracle.summaries(K, 64)
+    env = oracle.envelope(K, 64, 4, mu)
+    assert np.all(env >= sg - 1e-12)
+    assert np.all(env[1] > 2.0 * sg[1].mean())  # the spike's block is inflated
+    # constant sub-blocks: envelope_i = max_m |c_m - mu_i|
+    c = np.array([1.0, 2.0, 4.0, 9.0], np.float32)
+    Kc = np.repeat(c, 4)[:, None].repeat(3, axis=1).astype(np.float32)
+    m2, s2, _ = oracle.summaries(Kc, 16)
+    e2 = oracle.envelope(Kc, 16, 4, m2)
+    np.testing.assert_allclose(e2[0], np.abs(c - c.mean()).max() * np.ones(3), rtol=1e-12)
+
+
+# -------------------------------------------------------------------- bound
+
+def test_bound_hand_worked_example():
+    # d = 4, q = e1, block {2 e1, 0}: mu = e1, sigma = e1, M = 2
+    q = np.array([1.0, 0.0, 0.0, 0.0])
+    mu = np.array([1.0, 0.0, 0.0, 0.0]); sg = np.array([1.0, 0.0, 0.0, 0.0])
+    assert oracle.bound(q, mu, sg, 2.0, 0.5) == pytest.approx(0.75)   # min(1.5, 2) / 2
+    assert oracle.bound(q, mu, sg, 2.0, 2.0) == pytest.approx(1.0)    # min(3, 2) / 2
+    q2 = np.array([0.0, 2.0, 0.0, 0.0])                             # orthogonal query
+    assert oracle.bound(q2, mu, sg, 2.0, 3.0) == pytest.approx(0.0)
+
+
+def _random_blocks(seed, nblk, b, d, dt="f32"):
+    rng = np.random.default_rng(seed)
+    K = rng.standard_normal((nblk * b, d)).astype(np.float32)
+    # heavy-tailed coordinates and a few planted, query-aligned blocks
+    K[:, 3] *= 4.0
+    q = rng.standard_normal(d)
+    for j in rng.choice(nblk, nblk // 10, replace=False):
+        K[j * b:(j + 1) * b] += (3.0 * math.sqrt(d) * q / np.linalg.norm(q)).astype(np.float32)
+    Kin = K if dt == "f32" else _bf16_bits(K)
+    return q, Kin
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_spherical_ceiling_is_a_true_upper_bound(dt):
+    # with z huge the bound is the Cauchy-Schwarz term |q| M / sqrt(d) >= max_k q.k / sqrt(d)
+    b, d = 16, 32
+    q, K = _random_blocks(11, 400, b, d, dt)
+    mu, sg, M = oracle.summaries(K, b)
+    Kd = _f64(K).reshape(400, b, d)
+    true_max = (Kd @ q).max(axis=1) / math.sqrt(d)
+    for j in range(400):
+        bd = oracle.bound(q, mu[j], sg[j], M[j], 1e12)
+        assert bd == pytest.approx(np.linalg.norm(q) * M[j] / math.sqrt(d), rel=1e-12)
+        assert bd >= true_max[j] - 1e-12
+
+
+@pytest.mark.parametrize("b,d", [(4, 8), (16, 32), (64, 64)])
+def test_dual_bound_is_certified_at_samuelson_diagonal_z(b, d):
+    # qT Sigma q <= d sum q_i^2 sigma_i^2 (Cauchy-Schwarz) and Samuelson's
+    # inequality (max deviation <= sqrt(b-1) std) => bound >= block max at z = sqrt((b-1) d)
+    nblk = 300
+    q, K = _random_blocks(5 + b, nblk, b, d)
+    mu, sg, M = oracle.summaries(K, b)
+    Kd = _f64(K).reshape(nblk, b, d)
+    true_max = (Kd @ q).max(axis=1) / math.sqrt(d)
+    z = math.sqrt((b - 1) * d)
+    for j in range(nblk):
+        assert oracle.bound(q, mu[j], sg[j], M[j], z) >= true_max[j] - 1e-12
+
+
+def test_cantelli_finite_population_count():
+    # with the full covariance, at most floor(b / (1 + z^2)) keys exceed mu.q + z sqrt(qT Sigma q)
+    b, d = 64, 16
+    q, K = _random_blocks(21, 200, b, d)
+    mu, sg, M = oracle.summaries(K, b)
+    Kd = _f64(K).reshape(200, b, d)
+    for z in (0.5, 1.0, 2.0, 3.0):
+        cap = math.floor(b / (1 + z * z))
+        for j in range(200):
+            X = Kd[j] @ q
+            cov = np.cov(Kd[j].T, bias=True)
+            thr = q @ mu[j] + z * math.sqrt(q @ cov @ q)
+            assert int((X >= thr + 1e-9).sum()) <= cap
+
+
+# ---------------------------------------------------------------- predictor
+
+def test_predictor_special_cases():
+    rng = np.random.default_rng(2)
+    B, Hq, d = 3, 4, 8
+    q = rng.standard_normal((B, Hq, d)).astype(np.float32)
+    bias = rng.standard_normal(Hq).astype(np.float32)
+    np.testing.assert_array_equal(oracle.predict(q, None, bias), np.tile(bias.astype(np.float64), (B, 1)))
+    # one-hot column picks one coordinate of the concatenated query: head 2, dim 5 -> head 1
+    W = np.zeros((Hq * d, Hq), np.float32)
+    W[2 * d + 5, 1] = 1.0
+    W[0 * d + 0, 3] = -2.0
+    tau = oracle.predict(q, W, bias)
+    np.testing.assert_allclose(tau[:, 1], q[:, 2, 5].astype(np.float64) + bias[1], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(tau[:, 3], -2.0 * q[:, 0, 0].astype(np.float64) + bias[3], atol=1e-12)
+    np.testing.assert_allclose(tau[:, 0], bias[0], atol=0)
+    # linear in W
+    W1 = rng.standard_normal((Hq * d, Hq)).astype(np.float32)
+    W2 = rng.standard_normal((Hq * d, Hq)).astype(np.float32)
+    lhs = oracle.predict(q, W1 + W2, None)
+    rhs = oracle.predict(q, W1, None) + oracle.predict(q, W2, None)
+    np.testing.assert_allclose(lhs, rhs, rtol=1e-5, atol=1e-5)
+
+
+def test_start_dense_initialisation_keeps_every_block():
+    wl = make_workload(B=1, Hq=4, Hkv=2, d=32, block=16, seq_lens=[512], dtype=torch.float32,
+                       predictor=False, tau_const=GOLD["start_dense_bias"], seed=9)
+    q, k, v = as_numpy(wl.q), as_numpy(wl.k), as_numpy(wl.v)
+    tau = oracle.predict(q, np.zeros((4 * 32, 4), np.float32), as_numpy(wl.bias))
+    r = oracle.decode(q, k, v, wl.seq_lens, tau, block_size=16, rescue_window=128)
+    assert r.sel.all()
+    assert np.all(r.counts == 512)
+
+
+# ---------------------------------------------------------------- selection
+
+def test_selection_threshold_pins_and_rescue():
+    bounds = np.array([0.1, 0.9, 0.9, 0.3, 5.0, 0.2])
+    sel, r = oracle.select(bounds, 1.0, c=4)           # nothing >= 1 inside window [0, 4)
+    assert r == 1                                      # first of the tied maxima
+    np.testing.assert_array_equal(sel, [0, 1, 0, 0, 1, 0])
+    sel, r = oracle.select(bounds, 0.5, c=4)           # window already has selections
+    assert r == -1
+    np.testing.assert_array_equal(sel, [0, 1, 1, 0, 1, 0])
+    sel, r = oracle.select(bounds, 10.0, c=2, lwb=1)   # pin outside window, rescue in [0, 2)
+    assert r == 1
+    np.testing.assert_array_equal(sel, [0, 1, 0, 0, 0, 1])
+    sel, r = oracle.select(bounds, 10.0, c=6, lwb=1)   # pinned block inside window: no rescue
+    assert r == -1
+    np.testing.assert_array_equal(sel, [0, 0, 0, 0, 0, 1])
+    sel, r = oracle.select(bounds, 10.0, c=0)          # rescue disabled
+    assert r == -1 and sel.sum() == 0
+    sel, r = oracle.select(bounds, 0.9, c=4)           # bound == tau survives (>=)
+    np.testing.assert_array_equal(sel, [0, 1, 1, 0, 1, 0])
+    sel, r = oracle.select(np.array([np.nan, 0.2, np.nan]), 1.0, c=3)
+    assert r == 1 and sel.tolist() == [0, 1, 0]
+    sel, r = oracle.select(bounds, 10.0, c=6, screen_all=True)
+    assert r == -1 and sel.all()
+
+
+# ---------------------------------------------------------------- attention
+
+def _sdpa(q, K, V, bias=None):
+    qt = torch.from_numpy(q)[None, None, None, :]
+    kt = torch.from_numpy(K)[None, None]
+    vt = torch.from_numpy(V)[None, None]
+    m = None if bias is None else torch.from_numpy(bias)[None, None, None, :]
+    return torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, attn_mask=m)[0, 0, 0].numpy()
+
+
+@pytest.mark.parametrize("T", [1, 63, 64, 200, 1000])
+def test_tau_minus_inf_is_textbook_softmax_attention(T):
+    wl = make_workload(B=2, Hq=4, Hkv=2, d=32, block=16, seq_lens=[T, max(1, T // 2)],
+                       T_cap=T, dtype=torch.float32, predictor=False, tau_const=-math.inf,
+                       planted={"frac": 0.1}, seed=T)
+    q, k, v = as_numpy(wl.q), as_numpy(wl.k), as_numpy(wl.v)
+    tau = np.full((2, 4), -np.inf)
+    r = oracle.decode(q, k, v, wl.seq_lens, tau, block_size=16, rescue_window=128)
+    for bb in range(2):
+        Tb = wl.seq_lens[bb]
+        for h in range(4):
+            g = h // 2
+            ref = _sdpa(q[bb, h].astype(np.float64), _f64(k[bb, g, :Tb]), _f64(v[bb, g, :Tb]))
+            np.testing.assert_allclose(r.o[bb, h], ref, rtol=1e-10, atol=1e-12)
+            assert r.counts[bb, h] == Tb
+
+
+def test_screen_all_is_dense_gated_attention():
+    # softmax(S~) = softmax(S + (S~ - S)): SDPA with the gate's offset as an additive mask
+    wl = make_workload(B=1, Hq=2, Hkv=1, d=16, block=8, seq_lens=[203], dtype=torch.float32,
+                       predictor=False, tau_const=0.4, planted={"frac": 0.2}, seed=4)
+    q, k, v = as_numpy(wl.q), as_numpy(wl.k), as_numpy(wl.v)
+    tau = np.full((1, 2), 0.4)
+    r = oracle.decode(q, k, v, wl.seq_lens, tau, block_size=8, beta=3.0, screen_all=True)
+    for h in range(2):
+        qh = q[0, h].astype(np.float64)
+        S = _f64(k[0, 0]) @ qh / 4.0
+        off = np.array([oracle.gate(s, 0.4, 3.0) - s for s in S])
+        ref = _sdpa(qh, _f64(k[0, 0]), _f64(v[0, 0]), off)
+        np.testing.assert_allclose(r.o[0, h], ref, rtol=1e-10, atol=1e-12)
+        assert r.counts[0, h] == 203
+
+
+def test_convex_output_decomposition():
+    # o over a union of disjoint token sets is the Z-weighted combination of the parts
+    rng = np.random.default_rng(8)
+    T, b, d = 333, 16, 24
+    K = rng.standard_normal((T, d)).astype(np.float32)
+    V = rng.standard_normal((T, d)).astype(np.float32)
+    q = rng.standard_normal(d)
+    N = T // b
+    for trial in range(5):
+        part = rng.integers(0, 2, N).astype(np.uint8)
+        o_all, l_all, n_all = oracle.attend(q, K, V, b, np.ones(N, np.uint8), use_tail=True,
+                                            tau_eff=1.1, beta=4.0)
+        o1, l1, n1 = oracle.attend(q, K, V, b, part, use_tail=False, tau_eff=1.1, beta=4.0)
+        o2, l2, n2 = oracle.attend(q, K, V, b, 1 - part, use_tail=True, tau_eff=1.1, beta=4.0)
+        Z1, Z2 = math.exp(l1) if n1 else 0.0, math.exp(l2)
+        np.testing.assert_allclose(o_all, (Z1 * o1 + Z2 * o2) / (Z1 + Z2), rtol=1e-12, atol=1e-13)
+        assert l_all == pytest.approx(math.log(Z1 + Z2), rel=1e-13)
+        assert n_all == n1 + n2 == T
+
+
+def test_nothing_attended_gives_zero_output():
+    K = np.ones((32, 4), np.float32)
+    o, lse, n = oracle.attend(np.ones(4), K, K, 16, np.zeros(2, np.uint8), use_tail=False)
+    assert n == 0 and lse == -math.inf and np.all(o == 0)
+
+
+def test_self_ungated_changes_only_the_last_key():
+    rng = np.random.default_rng(1)
+    K = rng.standard_normal((40, 8)).astype(np.float32)
+    V = rng.standard_normal((40, 8)).astype(np.float32)
+    q = rng.standard_normal(8)
+    sel = np.ones(2, np.uint8)
+    o0, l0, _ = oracle.attend(q, K, V, 16, sel, tau_eff=2.0, beta=4.0, self_ungated=False)
+    o1, l1, _ = oracle.attend(q, K, V, 16, sel, tau_eff=2.0, beta=4.0, self_ungated=True)
+    S_last = float(K[-1] @ q) / math.sqrt(8)
+    g_last = oracle.gate(S_last, 2.0, 4.0)
+    # closed-form swap of one weight: Z1 = Z0 - e^{g} + e^{S}
+    Z0, Z1 = math.exp(l0), math.exp(l1)
+    assert Z1 == pytest.approx(Z0 - math.exp(g_last) + math.exp(S_last), rel=1e-12)
+    np.testing.assert_allclose(o1 * Z1, o0 * Z0 + (math.exp(S_last) - math.exp(g_last)) * V[-1].astype(np.float64),
+                               rtol=1e-10, atol=1e-12)
+
+
+# ------------------------------------------------------ whole path vs brute force
+
+CASES = [
+    # B, Hq, Hkv, d, b, lens, c, tau, z, a, lwb, self_ungated, dtype
+    (1, 1, 1, 8, 4, [1], 4, 0.5, 1.0, 0.0, 0, False, torch.float32),
+    (1, 1, 1, 8, 4, [3], 4, 0.5, 1.0, 0.0, 0, False, torch.float32),
+    (1, 2, 1, 8, 4, [4], 4, 0.5, 1.0, 0.0, 0, False, torch.float32),
+    (2, 2, 2, 8, 4, [37, 5], 3, 0.8, 1.0, 0.0, 0, True, torch.float32),
+    (1, 4, 2, 16, 8, [100], 2, 3.0, 1.0, 0.0, 0, False, torch.float32),     # forces rescue
+    (1, 4, 1, 16, 8, [100], 2, 3.0, 1.0, 0.0, 2, False, torch.float32),     # pins
+    (2, 4, 2, 64, 16, [1024, 777], 16, 1.3, 2.0, 0.2, 0, False, torch.bfloat16),
+    (1, 8, 2, 64, 64, [1000], 128, 1.5, 1.0, 0.0, 0, False, torch.bfloat16),
+    (3, 4, 4, 8, 4, [64, 65, 66], 100, 0.2, 1.0, -0.3, 1, True, torch.bfloat16),
+    (1, 2, 1, 32, 16, [512], 0, 5.0, 1.0, 0.0, 0, False, torch.float32),    # rescue off, tail-less
+]
+
+
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_oracle_matches_brute_force_algorithm(case):
+    B, Hq, Hkv, d, b, lens, c, tau0, z, a, lwb, su, dt = CASES[case]
+    wl = make_workload(B=B, Hq=Hq, Hkv=Hkv, d=d, block=b, seq_lens=lens, dtype=dt,
+                       predictor=False, tau_const=tau0, planted={"frac": 0.15}, seed=100 + case)
+    q, k, v = as_numpy(wl.q), as_numpy(wl.k), as_numpy(wl.v)
+    rng = np.random.default_rng(case)
+    tau = tau0 + 0.3 * rng.standard_normal((B, Hq))
+    r = oracle.decode(q, k, v, lens, tau, block_size=b, z=z, a=a, beta=4.0, rescue_window=c,
+                      lwb=lwb, self_ungated=su)
+    G = Hq // Hkv
+    for bb in range(B):
+        for h in range(Hq):
+            o, att, ntok = brute.decode_head(q[bb, h], k[bb, h // G], v[bb, h // G], lens[bb], b, c,
+                                             tau[bb, h], a=a, z=z, beta=4.0, lwb=lwb,
+                                             self_ungated=su)
+            np.testing.assert_allclose(r.o[bb, h], o, rtol=1e-10, atol=1e-12)
+            assert set(np.nonzero(r.sel[bb, h])[0].tolist()) == att
+            assert r.counts[bb, h] == ntok
+
+
+# ----------------------------------------------------------- planted sanity
+
+def test_config1_selects_exactly_the_planted_blocks():
+    wl = config1()
+    q, k, v = as_numpy(wl.q), as_numpy(wl.k), as_numpy(wl.v)
+    tau = oracle.predict(q, None, as_numpy(wl.bias))
+    assert np.all(tau == 2.0)
+    r = oracle.decode(q, k, v, wl.seq_lens, tau, block_size=64, z=1.0, beta=4.0, rescue_window=128)
+    for h in range(4):
+        assert np.nonzero(r.sel[0, h])[0].tolist() == wl.planted[(0, h)].tolist()
+        assert r.counts[0, h] == 8 * 64
+        # planted scores ~ 3 |q| >> 0: the output is the planted-only attention
+        o_p, _, _ = oracle.attend(q[0, h].astype(np.float64), k[0, h], v[0, h], 64, r.sel[0, h],
+                                  use_tail=False, tau_eff=2.0, beta=4.0)
+        np.testing.assert_allclose(r.o[0, h], o_p, rtol=1e-12)
+    # the margin to the threshold is wide (no block inside the 1e-4 tie band)
+    assert np.nanmin(np.abs(r.bounds - 2.0)) > 1e-2
