@@ -1,0 +1,317 @@
+#!/usr/bin/env python3
+"""Benchmark of the ETA decode step on one MI355X.
+
+Workload: one decode step at 512K context -- batch 1, 16 query / 4 KV heads
+(GQA 4), head_dim 128, KV blocks of 128 tokens, bf16 K/V ~N(0,1) with 1% of the
+blocks planted query-aligned, thresholds from the linear predictor with the
+bias placed for a given fraction of surviving blocks per head (synthetic data,
+see the design doc).  A timed step is eta_predict_threshold + eta_decode (screen,
+gated split decode over the surviving blocks, combine, mask); the KV cache and
+its block summaries are resident in HBM before timing starts.  The summary
+build (once per prefill) is timed on its own.
+
+One JSON line on stdout:
+  value           microseconds per decode step at 20% head survival
+  roofline        achieved HBM bandwidth of the split-decode kernel (the
+                  dominant one) on its algorithmic bytes, from HIP events
+                  recorded around each of its launches in the timed region
+  cpu_baseline    the fp64 oracle timed on this host's cores on the same step
+  sweep           the same step at 1% / 5% / 20% / 100% survival, with the
+                  dense decode baseline at the same shape
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+PRIMARY_SURVIVAL = 0.20
+SWEEP = (0.01, 0.05, 0.20, 1.00)
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_20888_amd", "csrc", "eta_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "split_decode_512k_traffic.json")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_src_sha() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="approximate CPU time budget of the oracle baseline")
+    ap.add_argument("--only-primary", action="store_true",
+                    help="time only the 20%% survival point (profiling runs)")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="also run a plain device copy of this size (counter calibration)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the ETA decode path here is single-GPU; see DESIGN.md for how it would shard)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2609_20888_amd import eta
+    from synth import config4, place_bias
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a ROCm GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    eta.load_library()
+
+    log("[bench] generating the 512K workload on the GPU")
+    wl = config4(device=dev, survival=PRIMARY_SURVIVAL)
+    B, Hq, Hkv, d, bs = wl.B, wl.Hq, wl.Hkv, wl.d, wl.block
+    sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
+    q, k, v, W = wl.q, wl.k, wl.v, wl.W
+    e = 2  # bf16 bytes
+    Ncap = wl.n_blk_cap
+    torch.cuda.synchronize()
+
+    # ---- summary build (prefill-time), timed on its own
+    summ = eta.build_block_summaries(k, sl, bs, num_q_heads=Hq)
+    torch.cuda.synchronize()
+    s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 5
+    s0.record()
+    for _ in range(reps):
+        eta.build_block_summaries(k, sl, bs, num_q_heads=Hq, out=summ)
+    s1.record()
+    torch.cuda.synchronize()
+    sum_ms = s0.elapsed_time(s1) / reps
+    sum_bytes = B * Hkv * wl.seq_lens[0] * d * e + B * Hkv * (wl.seq_lens[0] // bs) * (2 * d * 4 + 4)
+    log(f"[bench] summary build {sum_ms * 1e3:.1f} us ({sum_bytes / sum_ms / 1e6:.0f} GB/s)")
+
+    # ---- thresholds: place the predictor bias from the GPU's own bounds
+    bounds = eta.block_bounds(q, sl, summ, k, block_size=bs, z=wl.z).cpu().numpy()
+    qW = eta.predict_threshold(q, W, torch.zeros(Hq, device=dev)).cpu().numpy().astype(np.float64)
+    nblk = [t // bs for t in wl.seq_lens]
+    biases = {s: torch.as_tensor(place_bias(bounds, nblk, qW, s, wl.a), device=dev) for s in SWEEP}
+
+    params = eta.decode_params(beta=wl.beta, z=wl.z, offset_a=wl.a, rescue_window=wl.rescue_window)
+    desc = eta.kv_desc(k, Hq, bs)
+    ws = eta.alloc_workspace(eta.decode_workspace_size(desc, params), dev)
+    out = torch.empty_like(q)
+    mask = torch.empty(B, Hq, Ncap, dtype=torch.uint8, device=dev)
+    counts = torch.empty(B, Hq, dtype=torch.int32, device=dev)
+    tau = torch.empty(B, Hq, dtype=torch.float32, device=dev)
+
+    def step(bias):
+        eta.predict_threshold(q, W, bias, out=tau)
+        eta.decode(q, k, v, sl, summ, tau, block_size=bs, params=params, out=out, mask=mask,
+                   counts=counts, workspace=ws)
+
+    def algorithmic(mask_np):
+        """Bytes the step must move (mask -> union of the group's heads)."""
+        G = Hq // Hkv
+        mk = mask_np.reshape(B, Hkv, G, Ncap)
+        union_blocks = int(mk.any(axis=2).sum())
+        tail = sum(t - (t // bs) * bs for t in wl.seq_lens) * Hkv
+        kv = union_blocks * bs * d * e * 2 + tail * d * e * 2
+        summaries = sum(nblk) * Hkv * (2 * d * 4 + 4)
+        small = (B * Hq * d * e * 2            # q in, out
+                 + B * Hq * Ncap               # mask
+                 + Hq * d * Hq * 4 + Hq * 4    # predictor W, bias
+                 + B * Hq * 4 * 2)             # tau out and in
+        d_head = float(mask_np[:, :, :nblk[0]].mean())
+        d_union = union_blocks / float(B * Hkv * nblk[0])
+        return kv, kv + summaries + small, union_blocks, d_head, d_union
+
+    def time_point(bias, steps, warmup, profile):
+        for _ in range(warmup):
+            step(bias)
+        torch.cuda.synchronize()
+        if profile:
+            eta.profile_begin()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ev0.record()
+        for _ in range(steps):
+            step(bias)
+        ev1.record()
+        torch.cuda.synchronize()
+        wall_ms = (time.perf_counter() - t0) * 1e3
+        kt = eta.profile_end() if profile else None
+        return wall_ms / steps, ev0.elapsed_time(ev1) / steps, kt
+
+    def cold_point(bias, steps):
+        """Per-step GPU time with the 256 MB last-level cache flushed before each step."""
+        flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+        times = []
+        for _ in range(steps):
+            flush.fill_(1)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            step(bias)
+            b.record()
+            torch.cuda.synchronize()
+            times.append(a.elapsed_time(b))
+        del flush
+        return float(np.median(times))
+
+    def dense_point(steps, warmup):
+        dws = eta.alloc_workspace(eta.dense_workspace_size(desc), dev)
+        dout = torch.empty_like(q)
+        for _ in range(warmup):
+            eta.dense_decode(q, k, v, sl, block_size=bs, out=dout, workspace=dws)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(steps):
+            eta.dense_decode(q, k, v, sl, block_size=bs, out=dout, workspace=dws)
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / steps
+
+    dense_ms = dense_point(max(10, args.steps // 4), 3)
+    dense_bytes = B * Hkv * wl.seq_lens[0] * d * e * 2
+    log(f"[bench] dense decode {dense_ms * 1e3:.1f} us ({dense_bytes / dense_ms / 1e6:.0f} GB/s)")
+
+    sweep = {}
+    primary = None
+    for s in (SWEEP if not args.only_primary else (PRIMARY_SURVIVAL,)):
+        is_primary = abs(s - PRIMARY_SURVIVAL) < 1e-9
+        steps = args.steps if is_primary else max(20, args.steps // 4)
+        warm = args.warmup if is_primary else 5
+        ms, gpu_ms, kt = time_point(biases[s], steps, warm, profile=is_primary)
+        kv_b, step_b, ub, dh, du = algorithmic(mask.cpu().numpy())
+        cold_ms = cold_point(biases[s], 20)
+        entry = {"survival_target": s, "us_per_step": round(ms * 1e3, 2),
+                 "gpu_us_per_step": round(gpu_ms * 1e3, 2), "cold_us_per_step": round(cold_ms * 1e3, 2),
+                 "d_head": round(dh, 4), "d_union": round(du, 4), "union_blocks": ub,
+                 "step_bytes": step_b, "effective_GBps": round(step_b / ms / 1e6, 1),
+                 "effective_GBps_cold": round(step_b / cold_ms / 1e6, 1),
+                 "speedup_vs_dense": round(dense_ms / gpu_ms, 3)}
+        log(f"[bench] survival {s:.2f}: {entry}")
+        sweep[f"{int(round(s * 100))}%"] = entry
+        if is_primary:
+            primary = (ms, gpu_ms, kt, kv_b, step_b, ub, dh, du, steps, warm, cold_ms)
+
+    ms, gpu_ms, kt, kv_b, step_b, ub, dh, du, steps, warm, cold_ms = primary
+    split_ms, split_n = kt["split_decode"]
+    split_avg_ms = split_ms / max(split_n, 1)
+    achieved = kv_b / split_avg_ms / 1e6
+    kernels = {name: {"avg_us": round(t / max(n, 1) * 1e3, 2), "launches": n}
+               for name, (t, n) in kt.items() if n}
+
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        try:
+            tr = json.load(open(TRAFFIC_FILE))
+            if tr.get("kernel_src_sha") == kernel_src_sha():
+                traffic = tr.get("hbm_bytes_per_launch")
+        except (ValueError, OSError):
+            traffic = None
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl, biases[PRIMARY_SURVIVAL], args.cpu_seconds)
+
+    if args.copy_probe_mib > 0:
+        src = torch.empty(args.copy_probe_mib << 20, dtype=torch.uint8, device=dev).fill_(3)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] copy probe: {args.copy_probe_mib} MiB copied")
+
+    result = {
+        "metric": "decode attention us/step + effective HBM GB/s (frac of peak) at 128K/512K ctx",
+        "value": round(ms * 1e3, 2),
+        "unit": "us/step",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warm,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "eta_decode_512k_b1_gqa16x4_d128_blk128_bf16_survival20",
+                   "batch": B, "context": wl.seq_lens[0], "q_heads": Hq, "kv_heads": Hkv,
+                   "head_dim": d, "block": bs, "survival_target": PRIMARY_SURVIVAL,
+                   "beta": wl.beta, "z": wl.z, "rescue_window": wl.rescue_window,
+                   "parallelism": "single_gpu"},
+        "effective_GBps": round(step_b / ms / 1e6, 1),
+        "effective_frac_of_peak": round(step_b / ms / 1e6 / HBM_PEAK_GBS, 4),
+        "cold_us_per_step": round(cold_ms * 1e3, 2),
+        "d_head": round(dh, 4), "d_union": round(du, 4),
+        "dense_us_per_step": round(dense_ms * 1e3, 2),
+        "speedup_vs_dense": round(dense_ms / gpu_ms, 3),
+        "summary_build_us": round(sum_ms * 1e3, 1),
+        "summary_build_GBps": round(sum_bytes / sum_ms / 1e6, 1),
+        "roofline": {"bound": "hbm", "kernel": "split_decode", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "algorithmic_bytes_per_launch": kv_b,
+                     "avg_launch_us": round(split_avg_ms * 1e3, 2), "union_blocks": ub},
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+        "sweep": sweep,
+        "paper_context": "up to 2.15x end-to-end decode speedup over FlashAttention-2 "
+                         "(H100 SXM 80GB, fp16, 22-layer 1.45B model, B=64, 256K, 16% union)",
+        "kernel_src_sha": kernel_src_sha(),
+    }
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(wl, bias, budget_s):
+    """The fp64 oracle (unchanged, OpenMP over heads) on this host, on the same step."""
+    import numpy as np
+
+    import oracle
+    from synth import as_numpy
+
+    log("[bench] cpu baseline: copying the workload to the host")
+    q, k, v = as_numpy(wl.q), as_numpy(wl.k), as_numpy(wl.v)
+    W = as_numpy(wl.W)
+    b = bias.detach().cpu().numpy()
+    t0 = time.perf_counter()
+    summ = oracle.block_index(k, wl.seq_lens, wl.block)
+    t_index = time.perf_counter() - t0
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
+    rows = list(range(wl.B * wl.Hq))
+    n, elapsed = 0, 0.0
+    while True:
+        t0 = time.perf_counter()
+        tau = oracle.predict(q, W, b)
+        oracle.decode(q, k, v, wl.seq_lens, tau, block_size=wl.block, beta=wl.beta, z=wl.z,
+                      a=wl.a, rescue_window=wl.rescue_window, summaries=summ, rows=rows)
+        elapsed += time.perf_counter() - t0
+        n += 1
+        if elapsed >= budget_s or n >= 50:
+            break
+    per_step_us = elapsed / n * 1e6
+    log(f"[bench] cpu baseline {per_step_us:.0f} us/step over {n} steps "
+        f"(block index {t_index:.1f} s, untimed)")
+    return {"value": round(per_step_us, 1), "unit": "us/step", "cores": min(threads, len(rows)),
+            "kind": "oracle",
+            "sample": f"the full 512K step (all {len(rows)} query heads), repeated {n}x; "
+                      f"block summaries precomputed by the oracle, untimed"}
+
+
+if __name__ == "__main__":
+    main()

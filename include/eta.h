@@ -1,0 +1,247 @@
+/*
+ * eta.h -- C ABI of the Elastic Threshold Attention (ETA) decode path on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * One decode step of ETA attention for a batch of sequences, each with one new
+ * query token per query head, over a KV cache split into contiguous blocks of
+ * b tokens:
+ *
+ *   1. block summaries (built once per cache, at prefill):   mu, sigma, M per full block
+ *   2. threshold prediction:                                  tau = concat_h(q_h) W + bias
+ *   3. screening of every full block by its score bound against tau_eff = tau - a,
+ *      per-head top-1 rescue, GQA union of the surviving blocks
+ *   4. shifted-SiLU-gated softmax attention over the surviving blocks plus the
+ *      partial tail, split over the union and merged by log-sum-exp.
+ *
+ * Paper references are to "Elastic Threshold Attention: Learned Contextual
+ * Sparsity for Long-Context Decoding" (section / equation / algorithm names).
+ *
+ * Conventions shared by every entry point
+ *   - All data pointers are DEVICE pointers owned by the caller.  The library
+ *     allocates no device memory in any entry point; scratch space is the
+ *     caller's `workspace`.
+ *   - Work is enqueued on the caller's HIP stream (`stream`, a hipStream_t;
+ *     NULL = the null stream) and returns without synchronising.  Outputs are
+ *     valid once the stream reaches that point.
+ *   - Arguments are validated on the host before anything is enqueued.  A
+ *     failed call enqueues nothing and returns a non-zero eta_status_t;
+ *     eta_last_error_string() names the argument.  Device-side values (the
+ *     contents of seq_lens, q, tau, K, V) cannot be checked without a
+ *     synchronisation and are not: seq_lens[b] is clamped to
+ *     [0, capacity_tokens] before use, so no access leaves the buffers; NaN
+ *     in q, tau, K or V propagates to the outputs.
+ *   - Supported shapes: head_dim in {64, 128}; block_size in {64, 128};
+ *     G = num_q_heads / num_kv_heads in {1, 2, 4, 8}; K/V dtype fp32 or
+ *     bf16; q / output dtype fp32 or bf16.  Anything else returns
+ *     ETA_ERR_UNSUPPORTED -- there is no fallback path.
+ *   - Every device pointer must be 16-byte aligned; K/V strides must keep
+ *     token rows 16-byte aligned; the workspace must be 256-byte aligned.
+ *   - Functions never throw across the ABI and are safe to call from several
+ *     host threads (the error string is per thread).  Calls that share a
+ *     workspace must be ordered on one stream.
+ */
+#ifndef ETA_H_
+#define ETA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ETA_OK = 0,
+  ETA_ERR_INVALID_ARG = 1,   /* null pointer, bad size, misalignment, inconsistent shapes */
+  ETA_ERR_UNSUPPORTED = 2,   /* valid but outside the supported shape / dtype set */
+  ETA_ERR_WORKSPACE = 3,     /* workspace missing, misaligned or too small */
+  ETA_ERR_HIP = 4            /* a HIP runtime call or kernel launch failed */
+} eta_status_t;
+
+typedef enum { ETA_DT_F32 = 0, ETA_DT_BF16 = 1 } eta_dtype_t;
+
+/*
+ * KV cache geometry.  K and V share it.  Element (b, h, t, i) of K lives at
+ * k[b*stride_b + h*stride_h + t*stride_t + i] (strides in elements, the head
+ * dimension contiguous); the contiguous layout is [batch][num_kv_heads]
+ * [capacity_tokens][head_dim].  Token t of sequence b is valid for
+ * t < seq_lens[b] <= capacity_tokens.  Block j covers tokens [j*b, (j+1)*b);
+ * it is "full" when (j+1)*b <= seq_lens[b] (Sec. "Block-Based Scanning via
+ * Dual Metadata Caching": the cache is cut into contiguous blocks of b tokens).
+ */
+typedef struct {
+  int32_t batch;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t block_size;
+  int32_t kv_dtype;            /* eta_dtype_t */
+  int64_t capacity_tokens;
+  int64_t stride_b, stride_h, stride_t;
+} eta_kv_desc_t;
+
+/*
+ * Block index (the "Dual Probabilistic-Geometric Block Index" of Sec.
+ * "Block-Based Scanning via Dual Metadata Caching"), fp32, dimension-major so
+ * that a wavefront reading coordinate i of 64 consecutive blocks issues one
+ * coalesced load:
+ *   mu[((b*num_kv_heads + h)*head_dim + i)*n_blk_cap + j]     centroid
+ *   sigma[((b*num_kv_heads + h)*head_dim + i)*n_blk_cap + j]  coordinate std (population)
+ *   max_norm[(b*num_kv_heads + h)*n_blk_cap + j]              largest key L2 norm
+ * The standard deviation (not the variance) is stored, as the paper does
+ * (App. "GQA-Grouped Execution and Compact Metadata Layout").
+ * n_blk_cap >= capacity_tokens / block_size.
+ */
+typedef struct {
+  float* mu;
+  float* sigma;
+  float* max_norm;
+  int64_t n_blk_cap;
+} eta_summary_t;
+
+/* Decode hyper-parameters (Alg. "Hardware-Aligned Block-Sparse Decoding (Inference)"). */
+typedef struct {
+  float beta;                   /* gate temperature, Eq. (soft_mask); finite, >= 0 */
+  float z;                      /* z-score of the bound, Eq. (dual_bound_eq); finite, >= 0 */
+  float offset_a;               /* slack: tau_eff = tau - offset_a, used by screen and gate */
+  int32_t rescue_window_blocks; /* c: top-1 rescue over blocks [0, min(c, N)); 0 disables; <= 256 */
+  int32_t pin_recent_blocks;    /* lwb: the last lwb full blocks are always selected; >= 0 */
+  int32_t self_ungated;         /* 1: key seq_len-1 uses S~ = S (Eq. (mult_attn), M_tt = 1) */
+  int32_t screen_all;           /* 1: every full block selected (dense gated attention) */
+  int32_t num_splits;           /* splits per (sequence, kv head); 0: library default; <= 1024 */
+} eta_decode_params_t;
+
+/*
+ * eta_build_block_summaries -- one pass over K that writes mu, sigma, M of
+ * every full block of every (sequence, kv head) (Sec. "Block-Based Scanning
+ * via Dual Metadata Caching"; the single O(L d) prefill pass of App.
+ * "End-to-End Systems Accounting").
+ *   kv        cache geometry (num_q_heads is not used but must be valid)
+ *   k         keys, kv->kv_dtype, layout of eta_kv_desc_t
+ *   seq_lens  device int32 [batch]
+ *   out       summary buffers; entries of blocks that are not full are not written
+ * Statistics are accumulated in fp32: mean first, then the mean squared
+ * deviation from it (two passes over an on-chip copy of the block).
+ */
+eta_status_t eta_build_block_summaries(const eta_kv_desc_t* kv, const void* k,
+                                       const int32_t* seq_lens, const eta_summary_t* out,
+                                       void* stream);
+
+/*
+ * eta_predict_threshold -- Eq. (tau_pred): tau[b][h] = sum_j qbar[b][j] W[j][h] + bias[h],
+ * qbar[b] the concatenation of the num_q_heads query heads of sequence b
+ * (post-RoPE queries).  W == NULL gives frozen per-head constants tau[b][h] =
+ * bias[h] (Sec. "Runtime Contextuality and Domain-Specific Offline
+ * Calibration").
+ *   q        [batch][num_q_heads][head_dim], q_dtype (eta_dtype_t)
+ *   W        fp32 [num_q_heads*head_dim][num_q_heads] row-major, or NULL
+ *   bias     fp32 [num_q_heads] (required)
+ *   tau_out  fp32 [batch][num_q_heads]
+ * fp32 accumulation.  head_dim here may be any value in [1, 1024].
+ */
+eta_status_t eta_predict_threshold(int32_t batch, int32_t num_q_heads, int32_t head_dim,
+                                   int32_t q_dtype, const void* q, const float* W,
+                                   const float* bias, float* tau_out, void* stream);
+
+/* Bytes of workspace eta_decode needs for this geometry and these params. */
+eta_status_t eta_decode_workspace_size(const eta_kv_desc_t* kv, const eta_decode_params_t* p,
+                                       size_t* bytes);
+
+/*
+ * eta_decode -- one ETA decode step (Alg. "Hardware-Aligned Block-Sparse
+ * Decoding (Inference)"; GQA-grouped execution of App. "GQA-Grouped Execution
+ * and Compact Metadata Layout").  For every sequence b and query head h
+ * (kv head g = h / G), with s = 1/sqrt(head_dim), N = floor(T_b / block_size):
+ *   bound_j  = s * min(<q,mu_j> + z*sqrt(sum_i q_i^2 sigma_ji^2), |q| M_j)  (Eq. dual_bound_eq)
+ *   sel_j    = bound_j >= tau_eff | j >= N - lwb | screen_all
+ *   rescue   if no block in [0, min(c, N)) is selected, the first block of that
+ *            window with the largest bound is selected (top-1 rescue)
+ *   attended = selected full blocks + the tail [N*block_size, T_b)
+ *   S_t      = s <q, k_t>,  S~_t = S_t * sigmoid(beta (S_t - tau_eff))     (Eq. mult_attn)
+ *   out      = sum_t softmax(S~)_t v_t over the attended tokens
+ * A kv block is read from HBM once per (sequence, kv head) if any of its G
+ * query heads selected it (GQA union); each head attends only the blocks it
+ * selected.  A head that attends nothing (possible only with rescue disabled,
+ * no selection and no tail, or T_b = 0) gets a zero output.
+ *   q                  [batch][num_q_heads][head_dim], q_dtype
+ *   k, v               kv->kv_dtype, layout of eta_kv_desc_t
+ *   seq_lens           device int32 [batch]
+ *   summ               block index built by eta_build_block_summaries
+ *   tau                fp32 [batch][num_q_heads] (eta_predict_threshold output)
+ *   out                [batch][num_q_heads][head_dim], q_dtype (bf16: round to nearest even)
+ *   block_mask         uint8 [batch][num_q_heads][summ->n_blk_cap]: 1 = block attended
+ *                      by that head (threshold, pin or rescue); 0 elsewhere, including
+ *                      every entry j >= N
+ *   head_token_counts  int32 [batch][num_q_heads] attended tokens per head, or NULL
+ *   workspace          >= eta_decode_workspace_size() bytes, 256-byte aligned
+ * Results are deterministic: the same inputs give bitwise-identical outputs.
+ */
+eta_status_t eta_decode(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q, const void* k,
+                        const void* v, const int32_t* seq_lens, const eta_summary_t* summ,
+                        const float* tau, const eta_decode_params_t* p, void* out,
+                        uint8_t* block_mask, int32_t* head_token_counts, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
+/*
+ * eta_block_bounds -- the screening bound of Eq. (dual_bound_eq) for every
+ * full block and query head, as eta_decode computes it, without selecting or
+ * attending.  For threshold calibration and diagnostics.
+ *   bounds  fp32 [batch][num_q_heads][summ->n_blk_cap]; NaN for j >= N
+ */
+eta_status_t eta_block_bounds(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q,
+                              const int32_t* seq_lens, const eta_summary_t* summ, float z,
+                              float* bounds, void* stream);
+
+/* Bytes of workspace eta_dense_decode needs. */
+eta_status_t eta_dense_workspace_size(const eta_kv_desc_t* kv, int32_t num_splits, size_t* bytes);
+
+/*
+ * eta_dense_decode -- plain softmax attention decode over all T_b tokens (the
+ * dense attention output of Sec. "Elastic Threshold Attention"), split over
+ * the context and merged by log-sum-exp: the dense baseline the ETA path is
+ * measured against (the paper compares with FlashAttention-2 decode).  Same
+ * layouts as eta_decode; num_splits 0 = library default.
+ */
+eta_status_t eta_dense_decode(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q,
+                              const void* k, const void* v, const int32_t* seq_lens, void* out,
+                              int32_t num_splits, void* workspace, size_t workspace_bytes,
+                              void* stream);
+
+/* Human-readable detail of the last failure on this host thread ("" if none). */
+const char* eta_last_error_string(void);
+
+/* ABI version of this header: 1. */
+int32_t eta_abi_version(void);
+
+/*
+ * Kernel timing.  Between eta_profile_begin() and eta_profile_end(), every
+ * kernel the library launches is bracketed by a pair of HIP events recorded
+ * on the launch stream (at most 65536 launches).  eta_profile_end waits for
+ * the events and writes, per kernel kind, the summed duration in milliseconds
+ * and the launch count.
+ */
+typedef enum {
+  ETA_KERNEL_SUMMARIES = 0,
+  ETA_KERNEL_PREDICT = 1,
+  ETA_KERNEL_SCREEN = 2,
+  ETA_KERNEL_SPLIT_DECODE = 3,
+  ETA_KERNEL_COMBINE = 4,
+  ETA_KERNEL_DENSE_SPLIT = 5,
+  ETA_KERNEL_DENSE_COMBINE = 6,
+  ETA_KERNEL_BOUNDS = 7,
+  ETA_KERNEL_KINDS = 8
+} eta_kernel_kind_t;
+
+typedef struct {
+  double ms_total;
+  int64_t launches;
+} eta_kernel_time_t;
+
+eta_status_t eta_profile_begin(void);
+eta_status_t eta_profile_end(eta_kernel_time_t* out /* [ETA_KERNEL_KINDS] */);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ETA_H_ */

@@ -39,6 +39,7 @@ class _Problem(ctypes.Structure):
         ("beta", ctypes.c_double), ("z", ctypes.c_double), ("a", ctypes.c_double),
         ("c", ctypes.c_int32), ("lwb", ctypes.c_int32), ("self_ungated", ctypes.c_int32),
         ("screen_all", ctypes.c_int32), ("gate_off", ctypes.c_int32),
+        ("bounds_only", ctypes.c_int32),
         ("mu", _vp), ("sigma", _vp), ("maxnorm", _vp),
         ("sel_in", _vp),
         ("rows", _vp), ("n_rows", ctypes.c_int32),
@@ -191,18 +192,47 @@ class DecodeResult:
     rescued: np.ndarray    # [B][Hq] int64 (-1: no rescue)
 
 
+def block_index(k: np.ndarray, seq_lens: Sequence[int], block_size: int, n_threads: int = 0):
+    """Summaries (mu, sigma, M) of every full block of every (sequence, kv head).
+
+    k [B][Hkv][T_cap][d] -> mu, sigma [B][Hkv][N_cap][d] and M [B][Hkv][N_cap] (float64),
+    zero for blocks that are not full.  Same arithmetic as ``summaries``.
+    """
+    import concurrent.futures as cf
+    k = _c(k)
+    B, Hkv, T_cap, d = k.shape
+    Ncap = T_cap // block_size
+    mu = np.zeros((B, Hkv, max(Ncap, 1), d)); sg = np.zeros_like(mu)
+    mx = np.zeros((B, Hkv, max(Ncap, 1)))
+    lib = _load()
+    code = _dtype_code(k)
+
+    def one(bg):
+        b, g = divmod(bg, Hkv)
+        T = max(0, min(int(seq_lens[b]), T_cap))
+        sub = k[b, g]
+        lib.eta_oracle_summaries(_ptr(sub), code, d, T, d, block_size,
+                                 mu[b, g].ctypes.data_as(_vp), sg[b, g].ctypes.data_as(_vp),
+                                 mx[b, g].ctypes.data_as(_vp))
+    workers = n_threads if n_threads > 0 else (os.cpu_count() or 1)
+    with cf.ThreadPoolExecutor(max_workers=workers) as ex:   # ctypes releases the GIL
+        list(ex.map(one, range(B * Hkv)))
+    return mu[:, :, :Ncap], sg[:, :, :Ncap], mx[:, :, :Ncap]
+
+
 def decode(q: np.ndarray, k: np.ndarray, v: np.ndarray, seq_lens: Sequence[int], tau: np.ndarray,
            *, block_size: int, beta: float = 4.0, z: float = 1.0, a: float = 0.0,
            rescue_window: int = 128, lwb: int = 0, self_ungated: bool = False,
-           screen_all: bool = False, gate_off: bool = False,
+           screen_all: bool = False, gate_off: bool = False, bounds_only: bool = False,
            rows: Optional[Sequence[int]] = None, sel_in: Optional[np.ndarray] = None,
-           n_threads: int = 0) -> DecodeResult:
+           summaries=None, n_threads: int = 0) -> DecodeResult:
     """One ETA decode step for every (sequence, query head), or for ``rows``.
 
     q [B][Hq][d]; k, v [B][Hkv][T_cap][d]; seq_lens [B]; tau [B][Hq].
     Bounds -> threshold / pins / rescue -> gated attention over the selected
     blocks plus the tail (Alg. "Hardware-Aligned Block-Sparse Decoding").
-    Rows not requested are left zero.
+    Rows not requested are left zero.  ``bounds_only`` stops after the bounds.
+    ``summaries`` = (mu, sigma, M) from ``block_index`` skips recomputing them.
     """
     q = _c(q); k = _c(k); v = _c(v)
     B, Hq, d = q.shape
@@ -212,7 +242,7 @@ def decode(q: np.ndarray, k: np.ndarray, v: np.ndarray, seq_lens: Sequence[int],
     b = int(block_size)
     Ncap = T_cap // b
     sl = np.ascontiguousarray(np.asarray(seq_lens, np.int32))
-    tau = _c(tau, np.float64).reshape(B, Hq)
+    tau = np.zeros((B, Hq)) if tau is None else _c(tau, np.float64).reshape(B, Hq)
     tau = np.ascontiguousarray(tau)
     rows_a = None if rows is None else np.ascontiguousarray(np.asarray(rows, np.int32))
     sel_in_a = None if sel_in is None else np.ascontiguousarray(np.asarray(sel_in, np.uint8))
@@ -224,6 +254,12 @@ def decode(q: np.ndarray, k: np.ndarray, v: np.ndarray, seq_lens: Sequence[int],
         lse=np.full((B, Hq), -np.inf),
         rescued=np.full((B, Hq), -1, np.int64),
     )
+    smu = ssg = smx = None
+    if summaries is not None:
+        smu = np.ascontiguousarray(summaries[0], np.float64)
+        ssg = np.ascontiguousarray(summaries[1], np.float64)
+        smx = np.ascontiguousarray(summaries[2], np.float64)
+        assert smu.shape == (B, Hkv, Ncap, d) and smx.shape == (B, Hkv, Ncap)
     P = _Problem(
         B=B, Hq=Hq, Hkv=Hkv, d=d, b=b, T_cap=T_cap,
         q_dtype=_dtype_code(q), kv_dtype=_dtype_code(k),
@@ -231,7 +267,8 @@ def decode(q: np.ndarray, k: np.ndarray, v: np.ndarray, seq_lens: Sequence[int],
         beta=float(beta), z=float(z), a=float(a),
         c=int(rescue_window), lwb=int(lwb), self_ungated=int(bool(self_ungated)),
         screen_all=int(bool(screen_all)), gate_off=int(bool(gate_off)),
-        mu=None, sigma=None, maxnorm=None,
+        bounds_only=int(bool(bounds_only)),
+        mu=_ptr(smu), sigma=_ptr(ssg), maxnorm=_ptr(smx),
         sel_in=_ptr(sel_in_a),
         rows=_ptr(rows_a), n_rows=0 if rows_a is None else int(rows_a.shape[0]),
         n_threads=int(n_threads),

@@ -259,6 +259,7 @@ typedef struct {
   int32_t self_ungated;        /* key T-1 keeps S~ = S */
   int32_t screen_all;          /* every full block selected */
   int32_t gate_off;            /* plain softmax (dense baseline) */
+  int32_t bounds_only;         /* stop after the bounds (no selection, no attention) */
   /* optional precomputed summaries [B][Hkv][N_cap][d], [B][Hkv][N_cap]; NULL -> computed here */
   const double* mu;
   const double* sigma;
@@ -341,11 +342,16 @@ int eta_oracle_decode(const eta_oracle_problem* P) {
       for (int64_t j = 0; j < N; ++j)
         bnd[j] = eta_oracle_bound(qh, mu + (bg * Ncap + j) * d, sg + (bg * Ncap + j) * d,
                                   mx[bg * Ncap + j], d, P->z);
-      resc = eta_oracle_select(bnd, N, tau_eff, P->c, P->lwb, P->screen_all, sel);
+      if (!P->bounds_only) resc = eta_oracle_select(bnd, N, tau_eff, P->c, P->lwb, P->screen_all, sel);
       if (P->bounds) {
         for (int64_t j = 0; j < Ncap; ++j) P->bounds[(int64_t)row * Ncap + j] = j < N ? bnd[j] : NAN;
       }
       free(bnd);
+    }
+    if (P->bounds_only) {
+      free(sel);
+      free(qh);
+      continue;
     }
     double lse;
     int64_t cnt;

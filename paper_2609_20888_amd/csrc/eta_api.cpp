@@ -1,0 +1,403 @@
+// Host side of libeta: argument validation, split planning, workspace
+// carve-up, optional kernel timing, and the extern "C" entry points declared
+// in include/eta.h.  Every entry point validates all arguments before it
+// enqueues anything, and never throws across the ABI.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "eta.h"
+#include "eta_internal.h"
+
+namespace eta {
+namespace {
+
+thread_local std::string g_err;
+
+eta_status_t fail(eta_status_t code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+eta_status_t ok() {
+  g_err.clear();
+  return ETA_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int elem_bytes(int dt) { return dt == ETA_DT_F32 ? 4 : 2; }
+
+bool valid_dtype(int dt) { return dt == ETA_DT_F32 || dt == ETA_DT_BF16; }
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Geometry checks shared by every entry point that takes an eta_kv_desc_t.
+eta_status_t check_kv(const eta_kv_desc_t* kv, Geom* g) {
+  if (kv == nullptr) return fail(ETA_ERR_INVALID_ARG, "kv descriptor is NULL");
+  if (kv->batch < 1) return fail(ETA_ERR_INVALID_ARG, "batch must be >= 1 (got %d)", kv->batch);
+  if (kv->num_q_heads < 1 || kv->num_kv_heads < 1)
+    return fail(ETA_ERR_INVALID_ARG, "head counts must be >= 1 (q %d, kv %d)", kv->num_q_heads,
+                kv->num_kv_heads);
+  if (kv->num_q_heads % kv->num_kv_heads != 0)
+    return fail(ETA_ERR_INVALID_ARG, "num_q_heads (%d) is not a multiple of num_kv_heads (%d)",
+                kv->num_q_heads, kv->num_kv_heads);
+  if (kv->head_dim < 1 || kv->block_size < 1)
+    return fail(ETA_ERR_INVALID_ARG, "head_dim and block_size must be >= 1");
+  if (kv->capacity_tokens < 1)
+    return fail(ETA_ERR_INVALID_ARG, "capacity_tokens must be >= 1 (got %lld)",
+                (long long)kv->capacity_tokens);
+  if (!valid_dtype(kv->kv_dtype)) return fail(ETA_ERR_INVALID_ARG, "kv_dtype %d is not an eta_dtype_t", kv->kv_dtype);
+  const int G = kv->num_q_heads / kv->num_kv_heads;
+  if (kv->head_dim != 64 && kv->head_dim != 128)
+    return fail(ETA_ERR_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", kv->head_dim);
+  if (kv->block_size != 64 && kv->block_size != 128)
+    return fail(ETA_ERR_UNSUPPORTED, "block_size %d unsupported (64 or 128)", kv->block_size);
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return fail(ETA_ERR_UNSUPPORTED, "GQA group size %d unsupported (1, 2, 4 or 8)", G);
+  if (kv->num_q_heads > 256) return fail(ETA_ERR_UNSUPPORTED, "num_q_heads > 256 unsupported");
+  const int64_t eb = elem_bytes(kv->kv_dtype);
+  if (kv->stride_t < kv->head_dim)
+    return fail(ETA_ERR_INVALID_ARG, "stride_t (%lld) < head_dim (%d)", (long long)kv->stride_t,
+                kv->head_dim);
+  if (kv->stride_h < 0 || kv->stride_b < 0)
+    return fail(ETA_ERR_INVALID_ARG, "negative stride");
+  if ((kv->stride_t * eb) % 16 || (kv->stride_h * eb) % 16 || (kv->stride_b * eb) % 16)
+    return fail(ETA_ERR_INVALID_ARG, "K/V strides must keep token rows 16-byte aligned");
+  g->B = kv->batch;
+  g->Hq = kv->num_q_heads;
+  g->Hkv = kv->num_kv_heads;
+  g->D = kv->head_dim;
+  g->BS = kv->block_size;
+  g->G = G;
+  g->kv_dtype = kv->kv_dtype;
+  g->cap = kv->capacity_tokens;
+  g->sb = kv->stride_b;
+  g->sh = kv->stride_h;
+  g->st = kv->stride_t;
+  g->ncap = kv->capacity_tokens / kv->block_size;
+  g->n_tiles = (int)((g->ncap + kScreenTile - 1) / kScreenTile);
+  if (g->n_tiles < 1) g->n_tiles = 1;
+  return ETA_OK;
+}
+
+eta_status_t check_summary(const eta_summary_t* s, Geom* g) {
+  if (s == nullptr) return fail(ETA_ERR_INVALID_ARG, "summary descriptor is NULL");
+  if (!s->mu || !s->sigma || !s->max_norm)
+    return fail(ETA_ERR_INVALID_ARG, "summary buffers must be non-NULL");
+  if (!aligned16(s->mu) || !aligned16(s->sigma) || !aligned16(s->max_norm))
+    return fail(ETA_ERR_INVALID_ARG, "summary buffers must be 16-byte aligned");
+  if (s->n_blk_cap < g->cap / g->BS)
+    return fail(ETA_ERR_INVALID_ARG, "n_blk_cap (%lld) < capacity_tokens / block_size (%lld)",
+                (long long)s->n_blk_cap, (long long)(g->cap / g->BS));
+  g->ncap = s->n_blk_cap;
+  g->n_tiles = (int)((g->ncap + kScreenTile - 1) / kScreenTile);
+  if (g->n_tiles < 1) g->n_tiles = 1;
+  if (g->n_tiles > kMaxTiles)
+    return fail(ETA_ERR_UNSUPPORTED, "n_blk_cap %lld exceeds %d screening tiles",
+                (long long)s->n_blk_cap, kMaxTiles);
+  return ETA_OK;
+}
+
+eta_status_t check_params(const eta_decode_params_t* p) {
+  if (p == nullptr) return fail(ETA_ERR_INVALID_ARG, "params is NULL");
+  if (!std::isfinite(p->beta) || p->beta < 0.f)
+    return fail(ETA_ERR_INVALID_ARG, "beta must be finite and >= 0");
+  if (!std::isfinite(p->z) || p->z < 0.f) return fail(ETA_ERR_INVALID_ARG, "z must be finite and >= 0");
+  if (!std::isfinite(p->offset_a)) return fail(ETA_ERR_INVALID_ARG, "offset_a must be finite");
+  if (p->rescue_window_blocks < 0) return fail(ETA_ERR_INVALID_ARG, "rescue_window_blocks < 0");
+  if (p->rescue_window_blocks > kScreenTile)
+    return fail(ETA_ERR_UNSUPPORTED, "rescue_window_blocks > %d unsupported", kScreenTile);
+  if (p->pin_recent_blocks < 0) return fail(ETA_ERR_INVALID_ARG, "pin_recent_blocks < 0");
+  if (p->num_splits < 0 || p->num_splits > kMaxSplits)
+    return fail(ETA_ERR_INVALID_ARG, "num_splits must be in [0, %d]", kMaxSplits);
+  return ETA_OK;
+}
+
+// ------------------------------------------------------------- kernel timer
+
+struct Profiler {
+  std::mutex mu;
+  bool on = false;
+  std::vector<hipEvent_t> pool;       // pairs: [2i] start, [2i+1] end
+  std::vector<int> kinds;
+  size_t used = 0;
+  static constexpr size_t kMaxPairs = 65536;
+};
+Profiler& prof() {
+  static Profiler p;
+  return p;
+}
+
+void hook_fn(int kind, hipStream_t st, bool after) {
+  Profiler& P = prof();
+  std::lock_guard<std::mutex> lk(P.mu);
+  if (!P.on) return;
+  if (!after) {
+    if (P.used >= Profiler::kMaxPairs) return;
+    if (2 * P.used + 2 > P.pool.size()) {
+      hipEvent_t a, b;
+      if (hipEventCreate(&a) != hipSuccess) return;
+      if (hipEventCreate(&b) != hipSuccess) { (void)hipEventDestroy(a); return; }
+      P.pool.push_back(a);
+      P.pool.push_back(b);
+    }
+    (void)hipEventRecord(P.pool[2 * P.used], st);
+    P.kinds.push_back(kind);
+  } else {
+    if (P.kinds.size() != P.used + 1) return;
+    (void)hipEventRecord(P.pool[2 * P.used + 1], st);
+    ++P.used;
+  }
+}
+
+LaunchHook active_hook() {
+  Profiler& P = prof();
+  std::lock_guard<std::mutex> lk(P.mu);
+  return P.on ? hook_fn : nullptr;
+}
+
+}  // namespace
+
+int default_splits(const Geom& g) {
+  // aim at about four workgroups per compute unit over the whole grid
+  const int64_t groups = (int64_t)g.B * g.Hkv;
+  int64_t S = (1024 + groups - 1) / groups;
+  if (S > 256) S = 256;
+  const int64_t half = g.ncap / 2 > 0 ? g.ncap / 2 : 1;
+  if (S > half) S = half;
+  if (S < 1) S = 1;
+  return (int)S;
+}
+
+size_t decode_ws_bytes(const Geom& g, int S, DecodeWs* c, void* base) {
+  const size_t nb = (size_t)g.B * g.Hkv * g.ncap;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align256(off + bytes);
+    return o;
+  };
+  const size_t o_hm = take(nb);
+  const size_t o_ids = take(nb * 4);
+  const size_t o_tc = take((size_t)g.B * g.Hkv * g.n_tiles * 4);
+  const size_t o_hc = take((size_t)g.B * g.Hq * g.n_tiles * 4);
+  const size_t o_ml = take((size_t)g.B * g.Hq * S * 8);
+  const size_t o_acc = take((size_t)g.B * g.Hq * S * g.D * 4);
+  if (c && base) {
+    char* p = static_cast<char*>(base);
+    c->hm = reinterpret_cast<uint8_t*>(p + o_hm);
+    c->ids = reinterpret_cast<int32_t*>(p + o_ids);
+    c->tile_cnt = reinterpret_cast<int32_t*>(p + o_tc);
+    c->head_cnt = reinterpret_cast<int32_t*>(p + o_hc);
+    c->part_ml = reinterpret_cast<float2*>(p + o_ml);
+    c->part_acc = reinterpret_cast<float*>(p + o_acc);
+  }
+  return off;
+}
+
+size_t dense_ws_bytes(const Geom& g, int S, DecodeWs* c, void* base) {
+  size_t off = 0;
+  const size_t o_ml = off;
+  off = align256(off + (size_t)g.B * g.Hq * S * 8);
+  const size_t o_acc = off;
+  off = align256(off + (size_t)g.B * g.Hq * S * g.D * 4);
+  if (c && base) {
+    char* p = static_cast<char*>(base);
+    *c = DecodeWs{};
+    c->part_ml = reinterpret_cast<float2*>(p + o_ml);
+    c->part_acc = reinterpret_cast<float*>(p + o_acc);
+  }
+  return off;
+}
+
+}  // namespace eta
+
+using namespace eta;
+
+extern "C" {
+
+const char* eta_last_error_string(void) { return g_err.c_str(); }
+
+int32_t eta_abi_version(void) { return 1; }
+
+eta_status_t eta_build_block_summaries(const eta_kv_desc_t* kv, const void* k,
+                                       const int32_t* seq_lens, const eta_summary_t* out,
+                                       void* stream) {
+  Geom g;
+  eta_status_t st = check_kv(kv, &g);
+  if (st) return st;
+  if (!k || !seq_lens) return fail(ETA_ERR_INVALID_ARG, "k and seq_lens must be non-NULL");
+  if (!aligned16(k) || !aligned16(seq_lens)) return fail(ETA_ERR_INVALID_ARG, "k / seq_lens must be 16-byte aligned");
+  if ((st = check_summary(out, &g))) return st;
+  hipError_t e = launch_summaries(g, k, seq_lens, *out, (hipStream_t)stream, active_hook());
+  if (e != hipSuccess) return fail(ETA_ERR_HIP, "summaries launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+eta_status_t eta_predict_threshold(int32_t batch, int32_t num_q_heads, int32_t head_dim,
+                                   int32_t q_dtype, const void* q, const float* W,
+                                   const float* bias, float* tau_out, void* stream) {
+  if (batch < 1 || num_q_heads < 1 || head_dim < 1)
+    return fail(ETA_ERR_INVALID_ARG, "batch, num_q_heads and head_dim must be >= 1");
+  if (num_q_heads > 256) return fail(ETA_ERR_UNSUPPORTED, "num_q_heads > 256 unsupported");
+  if (head_dim > 1024) return fail(ETA_ERR_UNSUPPORTED, "head_dim > 1024 unsupported");
+  if (!valid_dtype(q_dtype)) return fail(ETA_ERR_INVALID_ARG, "q_dtype %d is not an eta_dtype_t", q_dtype);
+  if (!q || !bias || !tau_out) return fail(ETA_ERR_INVALID_ARG, "q, bias and tau_out must be non-NULL");
+  if (!aligned16(q) || !aligned16(bias) || !aligned16(tau_out) || (W && !aligned16(W)))
+    return fail(ETA_ERR_INVALID_ARG, "q, W, bias and tau_out must be 16-byte aligned");
+  hipError_t e = launch_predict(batch, num_q_heads, head_dim, q_dtype, q, W, bias, tau_out,
+                                (hipStream_t)stream, active_hook());
+  if (e != hipSuccess) return fail(ETA_ERR_HIP, "predictor launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+eta_status_t eta_decode_workspace_size(const eta_kv_desc_t* kv, const eta_decode_params_t* p,
+                                       size_t* bytes) {
+  Geom g;
+  eta_status_t st = check_kv(kv, &g);
+  if (st) return st;
+  if ((st = check_params(p))) return st;
+  if (!bytes) return fail(ETA_ERR_INVALID_ARG, "bytes is NULL");
+  const int S = p->num_splits > 0 ? p->num_splits : default_splits(g);
+  *bytes = decode_ws_bytes(g, S, nullptr, nullptr);
+  return ok();
+}
+
+eta_status_t eta_decode(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q, const void* k,
+                        const void* v, const int32_t* seq_lens, const eta_summary_t* summ,
+                        const float* tau, const eta_decode_params_t* p, void* out,
+                        uint8_t* block_mask, int32_t* head_token_counts, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  Geom g;
+  eta_status_t st = check_kv(kv, &g);
+  if (st) return st;
+  if ((st = check_params(p))) return st;
+  if (!valid_dtype(q_dtype)) return fail(ETA_ERR_INVALID_ARG, "q_dtype %d is not an eta_dtype_t", q_dtype);
+  if (!q || !k || !v || !seq_lens || !tau || !out || !block_mask)
+    return fail(ETA_ERR_INVALID_ARG, "q, k, v, seq_lens, tau, out and block_mask must be non-NULL");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(seq_lens) || !aligned16(tau) ||
+      !aligned16(out) || !aligned16(block_mask) ||
+      (head_token_counts && !aligned16(head_token_counts)))
+    return fail(ETA_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
+  // the mask and the workspace are laid out with the summary capacity
+  if ((st = check_summary(summ, &g))) return st;
+  const int S = p->num_splits > 0 ? p->num_splits : default_splits(g);
+  if (!workspace) return fail(ETA_ERR_WORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(ETA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  DecodeWs ws;
+  const size_t need = decode_ws_bytes(g, S, &ws, workspace);
+  if (workspace_bytes < need)
+    return fail(ETA_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
+  DecodeCfg c{p->beta, p->z, p->offset_a, p->rescue_window_blocks, p->pin_recent_blocks,
+              p->self_ungated ? 1 : 0, p->screen_all ? 1 : 0, S};
+  hipError_t e = launch_decode(g, c, q_dtype, q, k, v, seq_lens, *summ, tau, out, block_mask,
+                               head_token_counts, ws, (hipStream_t)stream, active_hook());
+  if (e != hipSuccess) return fail(ETA_ERR_HIP, "decode launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+eta_status_t eta_block_bounds(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q,
+                              const int32_t* seq_lens, const eta_summary_t* summ, float z,
+                              float* bounds, void* stream) {
+  Geom g;
+  eta_status_t st = check_kv(kv, &g);
+  if (st) return st;
+  if (!valid_dtype(q_dtype)) return fail(ETA_ERR_INVALID_ARG, "q_dtype %d is not an eta_dtype_t", q_dtype);
+  if (!std::isfinite(z) || z < 0.f) return fail(ETA_ERR_INVALID_ARG, "z must be finite and >= 0");
+  if (!q || !seq_lens || !bounds) return fail(ETA_ERR_INVALID_ARG, "q, seq_lens and bounds must be non-NULL");
+  if (!aligned16(q) || !aligned16(seq_lens) || !aligned16(bounds))
+    return fail(ETA_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
+  if ((st = check_summary(summ, &g))) return st;
+  hipError_t e = launch_bounds(g, q_dtype, q, seq_lens, *summ, z, bounds, (hipStream_t)stream,
+                               active_hook());
+  if (e != hipSuccess) return fail(ETA_ERR_HIP, "bounds launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+eta_status_t eta_dense_workspace_size(const eta_kv_desc_t* kv, int32_t num_splits, size_t* bytes) {
+  Geom g;
+  eta_status_t st = check_kv(kv, &g);
+  if (st) return st;
+  if (num_splits < 0 || num_splits > kMaxSplits)
+    return fail(ETA_ERR_INVALID_ARG, "num_splits must be in [0, %d]", kMaxSplits);
+  if (!bytes) return fail(ETA_ERR_INVALID_ARG, "bytes is NULL");
+  const int S = num_splits > 0 ? num_splits : default_splits(g);
+  *bytes = dense_ws_bytes(g, S, nullptr, nullptr);
+  return ok();
+}
+
+eta_status_t eta_dense_decode(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q,
+                              const void* k, const void* v, const int32_t* seq_lens, void* out,
+                              int32_t num_splits, void* workspace, size_t workspace_bytes,
+                              void* stream) {
+  Geom g;
+  eta_status_t st = check_kv(kv, &g);
+  if (st) return st;
+  if (!valid_dtype(q_dtype)) return fail(ETA_ERR_INVALID_ARG, "q_dtype %d is not an eta_dtype_t", q_dtype);
+  if (num_splits < 0 || num_splits > kMaxSplits)
+    return fail(ETA_ERR_INVALID_ARG, "num_splits must be in [0, %d]", kMaxSplits);
+  if (!q || !k || !v || !seq_lens || !out)
+    return fail(ETA_ERR_INVALID_ARG, "q, k, v, seq_lens and out must be non-NULL");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(seq_lens) || !aligned16(out))
+    return fail(ETA_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
+  const int S = num_splits > 0 ? num_splits : default_splits(g);
+  if (!workspace) return fail(ETA_ERR_WORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(ETA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  DecodeWs ws;
+  const size_t need = dense_ws_bytes(g, S, &ws, workspace);
+  if (workspace_bytes < need)
+    return fail(ETA_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
+  hipError_t e = launch_dense(g, S, q_dtype, q, k, v, seq_lens, out, ws, (hipStream_t)stream,
+                              active_hook());
+  if (e != hipSuccess) return fail(ETA_ERR_HIP, "dense launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+eta_status_t eta_profile_begin(void) {
+  Profiler& P = prof();
+  std::lock_guard<std::mutex> lk(P.mu);
+  P.on = true;
+  P.used = 0;
+  P.kinds.clear();
+  return ok();
+}
+
+eta_status_t eta_profile_end(eta_kernel_time_t* out) {
+  Profiler& P = prof();
+  std::lock_guard<std::mutex> lk(P.mu);
+  if (!out) return fail(ETA_ERR_INVALID_ARG, "out is NULL");
+  for (int i = 0; i < ETA_KERNEL_KINDS; ++i) out[i] = eta_kernel_time_t{0.0, 0};
+  P.on = false;
+  for (size_t i = 0; i < P.used; ++i) {
+    hipError_t e = hipEventSynchronize(P.pool[2 * i + 1]);
+    if (e != hipSuccess) return fail(ETA_ERR_HIP, "event synchronize failed: %s", hipGetErrorString(e));
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, P.pool[2 * i], P.pool[2 * i + 1]);
+    if (e != hipSuccess) return fail(ETA_ERR_HIP, "event elapsed time failed: %s", hipGetErrorString(e));
+    const int k = P.kinds[i];
+    if (k >= 0 && k < ETA_KERNEL_KINDS) {
+      out[k].ms_total += ms;
+      out[k].launches += 1;
+    }
+  }
+  P.used = 0;
+  P.kinds.clear();
+  return ok();
+}
+
+}  // extern "C"

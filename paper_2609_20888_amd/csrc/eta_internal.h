@@ -1,0 +1,72 @@
+// Internal declarations shared by the host API (eta_api.cpp) and the HIP
+// kernels (eta_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "eta.h"
+
+namespace eta {
+
+// Blocks screened by one workgroup (one lane per block).  The top-1 rescue
+// window must fit in the first screening tile, so rescue_window_blocks <= kScreenTile.
+constexpr int kScreenTile = 256;
+constexpr int kMaxSplits = 1024;
+// Upper bound on screening tiles per (sequence, kv head): the split-decode
+// kernel keeps their prefix sum in LDS.
+constexpr int kMaxTiles = 2048;
+
+struct Geom {
+  int B, Hq, Hkv, D, BS, G;
+  int kv_dtype;
+  int64_t cap;               // capacity_tokens
+  int64_t sb, sh, st;        // K/V strides in elements
+  int64_t ncap;              // summary n_blk_cap
+  int n_tiles;               // ceil(ncap / kScreenTile)
+};
+
+// Workspace carve-up of eta_decode.
+struct DecodeWs {
+  uint8_t* hm;               // [B][Hkv][ncap]   per-block bitmask of the G heads that selected it
+  int32_t* ids;              // [B][Hkv][ncap]   union block ids, compacted per screening tile
+  int32_t* tile_cnt;         // [B][Hkv][n_tiles] union blocks per tile
+  int32_t* head_cnt;         // [B][Hq][n_tiles]  selected blocks per head per tile
+  float2* part_ml;           // [B][Hq][S]        (running max, running sum) per split
+  float* part_acc;           // [B][Hq][S][D]     unnormalised output per split
+};
+
+size_t decode_ws_bytes(const Geom& g, int S, DecodeWs* carve, void* base);
+size_t dense_ws_bytes(const Geom& g, int S, DecodeWs* carve, void* base);
+int default_splits(const Geom& g);
+
+struct DecodeCfg {
+  float beta, z, offset_a;
+  int rescue_window, lwb, self_ungated, screen_all;
+  int S;                     // splits per (sequence, kv head)
+};
+
+// Launchers: validated arguments in, one or more kernels enqueued on `stream`.
+// `kind_cb` brackets each launch for the optional kernel timer.
+using LaunchHook = void (*)(int kind, hipStream_t stream, bool after);
+
+hipError_t launch_summaries(const Geom& g, const void* k, const int32_t* seq_lens,
+                            const eta_summary_t& s, hipStream_t stream, LaunchHook hook);
+
+hipError_t launch_predict(int B, int Hq, int D, int q_dtype, const void* q, const float* W,
+                          const float* bias, float* tau, hipStream_t stream, LaunchHook hook);
+
+hipError_t launch_decode(const Geom& g, const DecodeCfg& c, int q_dtype, const void* q,
+                         const void* k, const void* v, const int32_t* seq_lens,
+                         const eta_summary_t& s, const float* tau, void* out, uint8_t* mask,
+                         int32_t* counts, const DecodeWs& ws, hipStream_t stream, LaunchHook hook);
+
+hipError_t launch_bounds(const Geom& g, int q_dtype, const void* q, const int32_t* seq_lens,
+                         const eta_summary_t& s, float z, float* bounds, hipStream_t stream,
+                         LaunchHook hook);
+
+hipError_t launch_dense(const Geom& g, int S, int q_dtype, const void* q, const void* k,
+                        const void* v, const int32_t* seq_lens, void* out, const DecodeWs& ws,
+                        hipStream_t stream, LaunchHook hook);
+
+}  // namespace eta

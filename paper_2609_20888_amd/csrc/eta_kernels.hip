@@ -1,0 +1,940 @@
+// HIP kernels of the ETA decode path for gfx950 (CDNA4, wave64).
+//
+// Kernels and what they compute (paper: "Elastic Threshold Attention: Learned
+// Contextual Sparsity for Long-Context Decoding"):
+//   summaries_kernel  mu, sigma, M of every full KV block   (Sec. "Block-Based Scanning via
+//                                                            Dual Metadata Caching")
+//   predict_kernel    tau = concat(q) W + bias                (Eq. tau_pred)
+//   screen_kernel     Score_dual per block and head, threshold, pins, top-1 rescue,
+//                     GQA union and its compaction           (Eq. dual_bound_eq; Alg.
+//                                                            "Hardware-Aligned Block-Sparse
+//                                                            Decoding (Inference)")
+//   split_kernel      gated online softmax over a slice of the union list plus the
+//                     tail; one (max, sum, acc) partial per head and split
+//                                                           (Eq. mult_attn; App. "Chunked
+//                                                            Decoding and Two-Stage Reduction")
+//   combine_kernel    log-sum-exp merge of the partials      (same appendix)
+// The dense baseline reuses split_kernel / combine_kernel with every block and
+// no gate.
+//
+// All arithmetic is fp32 (bf16 inputs are widened exactly); reductions use a
+// fixed order, so results are bitwise reproducible.
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "eta_internal.h"
+
+namespace eta {
+namespace {
+
+constexpr float kNegInf = -__builtin_inff();
+
+__device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// fp32 -> bf16, round to nearest even; NaN stays NaN.
+__device__ __forceinline__ uint16_t to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// Element access for the two storage types: float and bf16 (raw uint16 bits).
+template <typename T>
+struct Elem;
+
+template <>
+struct Elem<float> {
+  static __device__ __forceinline__ void load8(const float* p, float (&x)[8]) {
+    const float4 a = *reinterpret_cast<const float4*>(p);
+    const float4 b = *reinterpret_cast<const float4*>(p + 4);
+    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+    x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+  }
+  template <int N>
+  static __device__ __forceinline__ void loadn(const float* p, float (&x)[N]) {
+    if constexpr (N == 1) {
+      x[0] = *p;
+    } else {
+      const float2 a = *reinterpret_cast<const float2*>(p);
+      x[0] = a.x; x[1] = a.y;
+    }
+  }
+};
+
+template <>
+struct Elem<uint16_t> {
+  static __device__ __forceinline__ void load8(const uint16_t* p, float (&x)[8]) {
+    const uint4 a = *reinterpret_cast<const uint4*>(p);
+    x[0] = bf16lo(a.x); x[1] = bf16hi(a.x); x[2] = bf16lo(a.y); x[3] = bf16hi(a.y);
+    x[4] = bf16lo(a.z); x[5] = bf16hi(a.z); x[6] = bf16lo(a.w); x[7] = bf16hi(a.w);
+  }
+  template <int N>
+  static __device__ __forceinline__ void loadn(const uint16_t* p, float (&x)[N]) {
+    if constexpr (N == 1) {
+      x[0] = bf16lo(*p);
+    } else {
+      const uint32_t a = *reinterpret_cast<const uint32_t*>(p);
+      x[0] = bf16lo(a); x[1] = bf16hi(a);
+    }
+  }
+};
+
+__device__ __forceinline__ float load_q(const void* q, int q_dtype, int64_t idx) {
+  if (q_dtype == ETA_DT_F32) return reinterpret_cast<const float*>(q)[idx];
+  return bf16lo(reinterpret_cast<const uint16_t*>(q)[idx]);
+}
+
+__device__ __forceinline__ void store_out(void* o, int q_dtype, int64_t idx, float x) {
+  if (q_dtype == ETA_DT_F32)
+    reinterpret_cast<float*>(o)[idx] = x;
+  else
+    reinterpret_cast<uint16_t*>(o)[idx] = to_bf16(x);
+}
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+__device__ __forceinline__ int64_t clamp_len(const int32_t* seq_lens, int b, int64_t cap) {
+  int64_t T = seq_lens[b];
+  return T < 0 ? 0 : (T > cap ? cap : T);
+}
+
+// ---------------------------------------------------------------- summaries
+//
+// One workgroup handles kSumBlocks consecutive full blocks of one (sequence,
+// kv head).  Each block is staged in LDS as fp32 (padded rows, conflict-free
+// column and row access); the row norms are reduced while staging; the mean
+// and the mean squared deviation are column sums over the staged copy.
+// Consecutive blocks of one workgroup fill the same cache lines of the
+// dimension-major output, so the scattered 4-byte stores merge in L2.
+
+constexpr int kSumBlocks = 32;
+
+template <int D, int BS, typename KVT>
+__global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ k, Geom g,
+                                                        const int32_t* __restrict__ seq_lens,
+                                                        float* __restrict__ mu,
+                                                        float* __restrict__ sigma,
+                                                        float* __restrict__ mx) {
+  constexpr int LDR = D + 1;
+  constexpr int CPR = D / 8;        // 8-element chunks per row
+  constexpr int NCH = BS * CPR;
+  constexpr int P = 256 / D;        // partial column sums per coordinate
+  __shared__ float tile[BS * LDR];
+  __shared__ float red[256];
+  __shared__ float mean_s[D];
+  __shared__ float nmax_s[4];
+
+  const int gh = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
+  const int64_t T = clamp_len(seq_lens, b, g.cap);
+  const int64_t N = T / BS;
+  const int64_t j0 = (int64_t)blockIdx.x * kSumBlocks;
+  const KVT* kb = k + (int64_t)b * g.sb + (int64_t)gh * g.sh;
+  const int64_t bg = (int64_t)b * g.Hkv + gh;
+  float* mub = mu + bg * D * g.ncap;
+  float* sgb = sigma + bg * D * g.ncap;
+  float* mxb = mx + bg * g.ncap;
+
+  for (int jj = 0; jj < kSumBlocks; ++jj) {
+    const int64_t j = j0 + jj;
+    if (j >= N) break;
+    float n2max = 0.f;
+    for (int c = tid; c < NCH; c += 256) {
+      const int r = c / CPR, cc = c % CPR;
+      float x[8];
+      Elem<KVT>::load8(kb + (j * BS + r) * g.st + cc * 8, x);
+      float n2 = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        tile[r * LDR + cc * 8 + e] = x[e];
+        n2 = fmaf(x[e], x[e], n2);
+      }
+      // the CPR consecutive lanes holding row r reduce its squared norm
+#pragma unroll
+      for (int o = CPR / 2; o > 0; o >>= 1) n2 += __shfl_xor(n2, o, 64);
+      n2max = fmaxf(n2max, n2);
+    }
+    n2max = wave_max(n2max);
+    if ((tid & 63) == 0) nmax_s[tid >> 6] = n2max;
+    __syncthreads();
+    {
+      const int i = tid % D, part = tid / D;
+      float s = 0.f;
+      for (int r = part; r < BS; r += P) s += tile[r * LDR + i];
+      red[tid] = s;
+    }
+    __syncthreads();
+    if (tid < D) {
+      float s = 0.f;
+#pragma unroll
+      for (int p = 0; p < P; ++p) s += red[p * D + tid];
+      mean_s[tid] = s * (1.0f / BS);
+    }
+    __syncthreads();
+    {
+      const int i = tid % D, part = tid / D;
+      const float m = mean_s[i];
+      float s = 0.f;
+      for (int r = part; r < BS; r += P) {
+        const float dv = tile[r * LDR + i] - m;
+        s = fmaf(dv, dv, s);
+      }
+      red[tid] = s;
+    }
+    __syncthreads();
+    if (tid < D) {
+      float s = 0.f;
+#pragma unroll
+      for (int p = 0; p < P; ++p) s += red[p * D + tid];
+      mub[(int64_t)tid * g.ncap + j] = mean_s[tid];
+      sgb[(int64_t)tid * g.ncap + j] = sqrtf(s * (1.0f / BS));
+    }
+    if (tid == 0) {
+      const float a = fmaxf(fmaxf(nmax_s[0], nmax_s[1]), fmaxf(nmax_s[2], nmax_s[3]));
+      mxb[j] = sqrtf(a);
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------- predictor
+//
+// One workgroup per sequence.  Thread t accumulates column h = t % Hq over the
+// rows j = t / Hq, t / Hq + 256 / Hq, ... of W (coalesced over h); the partial
+// sums of each column are then added in a fixed order.
+
+__global__ __launch_bounds__(256) void predict_kernel(const void* __restrict__ q, int q_dtype,
+                                                      const float* __restrict__ W,
+                                                      const float* __restrict__ bias,
+                                                      float* __restrict__ tau, int Hq, int D) {
+  __shared__ float red[256];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int64_t J = (int64_t)Hq * D;
+  const int rps = 256 / Hq;         // rows per step
+  const int h = tid % Hq, r0 = tid / Hq;
+  float acc = 0.f;
+  if (W != nullptr && r0 < rps) {
+    for (int64_t j = r0; j < J; j += rps)
+      acc = fmaf(load_q(q, q_dtype, (int64_t)b * J + j), W[j * Hq + h], acc);
+  }
+  red[tid] = (r0 < rps) ? acc : 0.f;
+  __syncthreads();
+  if (tid < Hq) {
+    float s = 0.f;
+    for (int r = 0; r < rps; ++r) s += red[r * Hq + tid];
+    tau[(int64_t)b * Hq + tid] = s + bias[tid];
+  }
+}
+
+// ---------------------------------------------------------------- screening
+//
+// One workgroup per (screening tile of 256 blocks, kv head, sequence); lane =
+// block.  With the dimension-major summaries, coordinate i of the 64 blocks of
+// a wavefront is one coalesced 256-byte load; the G query heads of the group
+// are evaluated from the same loads (q broadcast from LDS), so no cross-lane
+// reduction is needed for the bound.
+
+struct ScreenArgs {
+  const void* q;
+  const int32_t* seq_lens;
+  const float* tau;
+  const float* mu;
+  const float* sigma;
+  const float* mx;
+  uint8_t* mask;
+  uint8_t* hm;
+  int32_t* ids;
+  int32_t* tile_cnt;
+  int32_t* head_cnt;
+  float* bounds;
+  Geom g;
+  int q_dtype;
+  float z, offset_a;
+  int c, lwb, screen_all;
+};
+
+// First index attaining the largest value among valid lanes of the workgroup;
+// -1 if no lane is valid.  Every thread of the workgroup must call it.
+__device__ int block_argmax_first(float v, bool valid, int idx, float* rv, int* ri) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  float bv = valid ? v : kNegInf;
+  int bi = valid ? idx : 0x7fffffff;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(bv, o, 64);
+    const int oi = __shfl_xor(bi, o, 64);
+    if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+  }
+  if (lane == 0) { rv[w] = bv; ri[w] = bi; }
+  __syncthreads();
+  if (tid == 0) {
+    float b2 = rv[0];
+    int i2 = ri[0];
+    for (int k = 1; k < 4; ++k)
+      if (rv[k] > b2 || (rv[k] == b2 && ri[k] < i2)) { b2 = rv[k]; i2 = ri[k]; }
+    ri[4] = (i2 == 0x7fffffff) ? -1 : i2;
+  }
+  __syncthreads();
+  const int r = ri[4];
+  __syncthreads();
+  return r;
+}
+
+template <int D, int G, bool BOUNDS_ONLY>
+__global__ __launch_bounds__(256) void screen_kernel(ScreenArgs a) {
+  const Geom& g = a.g;
+  const int tile = blockIdx.x, gh = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
+  __shared__ float q_s[D][G];
+  __shared__ float q2_s[D][G];
+  __shared__ float qn_s[G];
+  __shared__ float teff_s[G];
+  __shared__ float rv[4];
+  __shared__ int ri[5];
+  __shared__ int wtot[4];
+
+  const int64_t hq0 = (int64_t)b * g.Hq + (int64_t)gh * G;   // first query head row of the group
+  for (int idx = tid; idx < G * D; idx += 256) {
+    const int h = idx / D, i = idx % D;
+    const float x = load_q(a.q, a.q_dtype, (hq0 + h) * D + i);
+    q_s[i][h] = x;
+    q2_s[i][h] = x * x;
+  }
+  __syncthreads();
+  if (tid < G) {
+    float s = 0.f;
+    for (int i = 0; i < D; ++i) s = fmaf(q_s[i][tid], q_s[i][tid], s);
+    qn_s[tid] = sqrtf(s);
+    if (!BOUNDS_ONLY) teff_s[tid] = a.tau[hq0 + tid] - a.offset_a;
+  }
+  __syncthreads();
+
+  const int64_t T = clamp_len(a.seq_lens, b, g.cap);
+  const int64_t N = T / g.BS;
+  const int64_t j = (int64_t)tile * kScreenTile + tid;
+  const int64_t bg = (int64_t)b * g.Hkv + gh;
+  const float scale = 1.0f / sqrtf((float)D);
+
+  float bnd[G];
+  if (j < N) {
+    float dot[G], var[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) { dot[h] = 0.f; var[h] = 0.f; }
+    const float* mup = a.mu + bg * D * g.ncap + j;
+    const float* sgp = a.sigma + bg * D * g.ncap + j;
+#pragma unroll 8
+    for (int i = 0; i < D; ++i) {
+      const float m = mup[(int64_t)i * g.ncap];
+      const float s = sgp[(int64_t)i * g.ncap];
+      const float s2 = s * s;
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        dot[h] = fmaf(q_s[i][h], m, dot[h]);
+        var[h] = fmaf(q2_s[i][h], s2, var[h]);
+      }
+    }
+    const float M = a.mx[bg * g.ncap + j];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float gauss = dot[h] + a.z * sqrtf(var[h]);
+      const float spher = qn_s[h] * M;
+      float lo = gauss < spher ? gauss : spher;
+      if (isnan(gauss) || isnan(spher)) lo = __builtin_nanf("");
+      bnd[h] = lo * scale;
+    }
+  } else {
+#pragma unroll
+    for (int h = 0; h < G; ++h) bnd[h] = __builtin_nanf("");
+  }
+
+  if constexpr (BOUNDS_ONLY) {
+    if (j < g.ncap) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) a.bounds[(hq0 + h) * g.ncap + j] = bnd[h];
+    }
+    return;
+  } else {
+    uint32_t bits = 0;
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const bool s = (j < N) && (a.screen_all || bnd[h] >= teff_s[h] || j >= N - a.lwb);
+      bits |= (uint32_t)s << h;
+    }
+    // top-1 rescue: the window [0, min(c, N)) lies inside tile 0
+    if (tile == 0 && a.c > 0) {
+      const int64_t Wn = (int64_t)a.c < N ? (int64_t)a.c : N;
+      if (Wn >= 1) {
+        const bool inw = j < Wn;
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+          const int any = __syncthreads_or(inw && ((bits >> h) & 1u));
+          if (!any) {
+            const int js = block_argmax_first(bnd[h], inw && !isnan(bnd[h]), (int)j, rv, ri);
+            if (js >= 0 && j == js) bits |= 1u << h;
+          }
+        }
+      }
+    }
+    if (j < g.ncap) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) a.mask[(hq0 + h) * g.ncap + j] = (uint8_t)((bits >> h) & 1u);
+      a.hm[bg * g.ncap + j] = (uint8_t)bits;
+    }
+    // compaction of the union ids of this tile (ordered prefix sum)
+    const int lane = tid & 63, w = tid >> 6;
+    const bool u = bits != 0;
+    const unsigned long long bal = __ballot(u);
+    const int lp = __popcll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) wtot[w] = __popcll(bal);
+    __syncthreads();
+    int off = 0, total = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      off += (k < w) ? wtot[k] : 0;
+      total += wtot[k];
+    }
+    if (u) a.ids[bg * g.ncap + (int64_t)tile * kScreenTile + off + lp] = (int32_t)j;
+    if (tid == 0) a.tile_cnt[bg * g.n_tiles + tile] = total;
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const int cnt = __syncthreads_count((bits >> h) & 1u);
+      if (tid == 0) a.head_cnt[(hq0 + h) * g.n_tiles + tile] = cnt;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- split decode
+//
+// One workgroup (4 wavefronts) per (split, kv head, sequence).  The split owns
+// a contiguous slice of the (sequence, kv head)'s union list; wavefront w takes
+// the slice's blocks w, w+4, ...  A block is processed 64 tokens at a time,
+// lane = token for the scores (each lane reads its own K row with 16-byte
+// loads) and lane = head-dimension pair for p.V (coalesced rows of V), with
+// the weights p passed through the wavefront's LDS slice.  A head skips blocks
+// it did not select even when a sibling head of the group loaded them (the
+// union is loaded once, each head keeps its own online-softmax state).  The
+// last split also attends the partial tail.  The four wavefront states are
+// merged through LDS into one partial (max, sum, acc) per head and split.
+//
+// Scores of bf16 K on the matrix cores: v_mfma_f32_16x16x32_bf16 with a
+// block-diagonal A.  Row m = 4*tg + h of A holds query head h restricted to the
+// k-slots of lane group tg, so the 16x16 result hands lane l the G <= 4 head
+// scores of token l; the B operand is exactly each lane's own K row chunk.
+// G = 8 runs two head quads.  fp32 q is split into bf16 hi + lo parts (two
+// MFMAs) so the scores keep ~16 mantissa bits; fp32 K uses the vector ALUs.
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+struct SplitArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const int32_t* seq_lens;
+  const float* tau;
+  const uint8_t* hm;
+  const int32_t* ids;
+  const int32_t* tile_cnt;
+  float2* part_ml;
+  float* part_acc;
+  Geom g;
+  int q_dtype;
+  float beta, offset_a;
+  int self_ungated;
+};
+
+// Gated score S~ = S sigmoid(beta (S - tau_eff)); -inf when the head does not
+// attend the token.
+template <bool DENSE>
+__device__ __forceinline__ float gated(float S, bool attend, bool ungated, float teff, float beta) {
+  if (!attend) return kNegInf;
+  if (DENSE || ungated || teff == kNegInf) return S;
+  return S / (1.0f + __expf(-beta * (S - teff)));
+}
+
+// Online-softmax update of one head with this lane's score `sc`; returns the
+// lane's weight and rescales the head's accumulator.
+template <int DPL>
+__device__ __forceinline__ float softmax_step(float sc, float& m, float& l, float (&acc)[DPL]) {
+  const float bm = wave_max(sc);
+  const float mn = fmaxf(m, bm);
+  if (mn == kNegInf) return 0.f;
+  const float alpha = __expf(m - mn);
+  const float p = __expf(sc - mn);
+  l = l * alpha + wave_sum(p);
+  m = mn;
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) acc[e] *= alpha;
+  return p;
+}
+
+// fp32 K/V: scores on the vector ALUs.
+template <int D, int G, bool DENSE>
+__device__ __forceinline__ void attend_f32(const float* __restrict__ kb, const float* __restrict__ vb,
+                                           int64_t st, int64_t t0, int nvalid, uint32_t bits,
+                                           const float (*qf_s)[G], const float* teff_s,
+                                           float (*p_s)[G], float beta, int64_t self_t, int lane,
+                                           float (&m_)[G], float (&l_)[G], float (&acc)[G][D / 64]) {
+  constexpr int DPL = D / 64;
+  for (int sb = 0; sb < nvalid; sb += 64) {
+    asm volatile("" ::: "memory");
+    const int nv = nvalid - sb < 64 ? nvalid - sb : 64;
+    const bool valid = lane < nv;
+    const int64_t row = t0 + sb + (valid ? lane : 0);
+    float dot[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) dot[h] = 0.f;
+#pragma unroll 2
+    for (int i = 0; i < D; i += 8) {
+      float x[8];
+      Elem<float>::load8(kb + row * st + i, x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+#pragma unroll
+        for (int h = 0; h < G; ++h) dot[h] = fmaf(x[e], qf_s[i + e][h], dot[h]);
+    }
+    const bool ung = (t0 + sb + lane) == self_t;
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float sc = gated<DENSE>(dot[h], valid && ((bits >> h) & 1u), ung, teff_s[h], beta);
+      p_s[lane][h] = softmax_step<DPL>(sc, m_[h], l_[h], acc[h]);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    for (int t = 0; t < nv; ++t) {
+      float vv[DPL];
+      Elem<float>::template loadn<DPL>(vb + (t0 + sb + t) * st + lane * DPL, vv);
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float ph = p_s[t][h];
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) acc[h][e] = fmaf(ph, vv[e], acc[h][e]);
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+// bf16 K/V: scores on the matrix cores.
+template <int D, int G, bool DENSE>
+__device__ __forceinline__ void attend_bf16(const uint16_t* __restrict__ kb,
+                                            const uint16_t* __restrict__ vb, int64_t st, int64_t t0,
+                                            int nvalid, uint32_t bits, const bf16x8* qa_s,
+                                            bool use_lo, const float* teff_s, float* p_s,
+                                            float beta, float scale, int64_t self_t, int lane,
+                                            float (&m_)[G], float (&l_)[G],
+                                            float (&acc)[G][D / 64]) {
+  constexpr int DPL = D / 64;
+  constexpr int DC = D / 8;               // 16-byte chunks per row = MFMAs per head quad
+  constexpr int NQ = G > 4 ? G / 4 : 1;   // head quads
+  constexpr int GQ = 4 * NQ;              // padded heads (LDS row of p)
+  const bool diag = ((lane & 15) >> 2) == (lane >> 4);
+  const int qrow = lane & 3;
+  for (int sb = 0; sb < nvalid; sb += 64) {
+    asm volatile("" ::: "memory");
+    const int nv = nvalid - sb < 64 ? nvalid - sb : 64;
+    const bool valid = lane < nv;
+    const int64_t tb = t0 + sb;
+    // issue every load of the 64-token step first: this lane's K row and, for
+    // every token, this lane's head-dimension pair of V (rows past the valid
+    // ones read token tb again and get weight 0)
+    uint4 kr[DC];
+    const uint16_t* krow = kb + (tb + (valid ? lane : 0)) * st;
+#pragma unroll
+    for (int c = 0; c < DC; ++c) kr[c] = *reinterpret_cast<const uint4*>(krow + 8 * c);
+    uint32_t vr[64];
+#pragma unroll
+    for (int t = 0; t < 64; ++t) {
+      const int64_t r = tb + (t < nv ? t : 0);
+      if constexpr (DPL == 2)
+        vr[t] = *reinterpret_cast<const uint32_t*>(vb + r * st + 2 * lane);
+      else
+        vr[t] = vb[r * st + lane];
+    }
+    const bool ung = (tb + lane) == self_t;
+#pragma unroll
+    for (int hq = 0; hq < NQ; ++hq) {
+      f32x4 c = {0.f, 0.f, 0.f, 0.f};
+      const bf16x8 zero = {};
+#pragma unroll
+      for (int ch = 0; ch < DC; ++ch) {
+        const bf16x8 bk = __builtin_bit_cast(bf16x8, kr[ch]);
+        const bf16x8 ahi = diag ? qa_s[((hq * 2 + 0) * 4 + qrow) * DC + ch] : zero;
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, bk, c, 0, 0, 0);
+        if (use_lo) {
+          const bf16x8 alo = diag ? qa_s[((hq * 2 + 1) * 4 + qrow) * DC + ch] : zero;
+          c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, bk, c, 0, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int h = 4 * hq + r;
+        if (h < G) {
+          const float sc =
+              gated<DENSE>(c[r] * scale, valid && ((bits >> h) & 1u), ung, teff_s[h], beta);
+          p_s[lane * GQ + h] = softmax_step<DPL>(sc, m_[h], l_[h], acc[h]);
+        }
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int t = 0; t < 64; ++t) {
+      float vv[DPL];
+      if constexpr (DPL == 2) {
+        vv[0] = bf16lo(vr[t]);
+        vv[1] = bf16hi(vr[t]);
+      } else {
+        vv[0] = bf16lo(vr[t]);
+      }
+#pragma unroll
+      for (int hq = 0; hq < NQ; ++hq) {
+        const float4 p4 = *reinterpret_cast<const float4*>(p_s + t * GQ + 4 * hq);
+        const float pr[4] = {p4.x, p4.y, p4.z, p4.w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int h = 4 * hq + r;
+          if (h < G) {
+#pragma unroll
+            for (int e = 0; e < DPL; ++e) acc[h][e] = fmaf(pr[r], vv[e], acc[h][e]);
+          }
+        }
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+template <int D, int BS, int G, typename KVT, bool DENSE>
+__global__ __launch_bounds__(256) void split_kernel(SplitArgs a) {
+  constexpr int DPL = D / 64;
+  constexpr bool BF = sizeof(KVT) == 2;
+  constexpr int NQ = G > 4 ? G / 4 : 1;
+  constexpr int GQ = 4 * NQ;
+  constexpr int DC = D / 8;
+  const Geom& g = a.g;
+  const int s = blockIdx.x, gh = blockIdx.y, b = blockIdx.z;
+  const int S = gridDim.x;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  __shared__ float qf_s[BF ? 1 : D][G];                  // fp32 path: scaled q
+  __shared__ bf16x8 qa_s[BF ? NQ * 2 * 4 * DC : 1];      // bf16 path: q chunks (hi, lo)
+  __shared__ float teff_s[G];
+  __shared__ int pref_s[kMaxTiles + 1];
+  __shared__ int wsum_s[4];
+  __shared__ float mrg_ml[4][G][2];
+  __shared__ float mrg_acc[4][G][D];
+  __shared__ __attribute__((aligned(16))) float p_s[4][64 * GQ];
+
+  const int64_t T = clamp_len(a.seq_lens, b, g.cap);
+  const int64_t N = T / BS;
+  const int ntail = (int)(T - N * BS);
+  const int64_t hq0 = (int64_t)b * g.Hq + (int64_t)gh * G;
+  const int64_t bg = (int64_t)b * g.Hkv + gh;
+  const float scale = 1.0f / sqrtf((float)D);
+  if constexpr (BF) {
+    // chunk (quad, part, head r, c) = 8 bf16 of query head 4 quad + r, dims 8c..8c+7
+    uint16_t* qa16 = reinterpret_cast<uint16_t*>(qa_s);
+    for (int idx = tid; idx < NQ * 4 * D; idx += 256) {
+      const int hh = idx / D, i = idx % D;
+      const int quad = hh / 4, r = hh % 4;
+      const float x = hh < G ? load_q(a.q, a.q_dtype, (hq0 + hh) * D + i) : 0.f;
+      const uint16_t hi = to_bf16(x);
+      const uint16_t lo = to_bf16(x - bf16lo(hi));
+      qa16[(((quad * 2 + 0) * 4 + r) * DC) * 8 + i] = hi;
+      qa16[(((quad * 2 + 1) * 4 + r) * DC) * 8 + i] = lo;
+    }
+  } else {
+    for (int idx = tid; idx < G * D; idx += 256) {
+      const int h = idx / D, i = idx % D;
+      qf_s[i][h] = load_q(a.q, a.q_dtype, (hq0 + h) * D + i) * scale;
+    }
+  }
+  if (tid < G) teff_s[tid] = DENSE ? 0.f : a.tau[hq0 + tid] - a.offset_a;
+  for (int idx = tid; idx < 4 * 64 * GQ; idx += 256) (&p_s[0][0])[idx] = 0.f;
+
+  int64_t lo, hi;
+  if constexpr (DENSE) {
+    lo = (N * s) / S;
+    hi = (N * (s + 1)) / S;
+  } else {
+    // exclusive prefix sum of the per-tile union counts, 256 tiles at a time
+    const int32_t* tc = a.tile_cnt + bg * g.n_tiles;
+    int carry = 0;
+    for (int base = 0; base < g.n_tiles; base += 256) {
+      const int t = base + tid;
+      const int x = t < g.n_tiles ? tc[t] : 0;
+      int incl = x;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += y;
+      }
+      if (lane == 63) wsum_s[w] = incl;
+      __syncthreads();
+      int woff = 0, tot = 0;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        woff += (k < w) ? wsum_s[k] : 0;
+        tot += wsum_s[k];
+      }
+      if (t < g.n_tiles) pref_s[t] = carry + woff + incl - x;
+      carry += tot;
+      __syncthreads();
+    }
+    if (tid == 0) pref_s[g.n_tiles] = carry;
+    const int64_t U = carry;
+    lo = (U * s) / S;
+    hi = (U * (s + 1)) / S;
+  }
+  __syncthreads();
+
+  const KVT* kb = reinterpret_cast<const KVT*>(a.k) + (int64_t)b * g.sb + (int64_t)gh * g.sh;
+  const KVT* vb = reinterpret_cast<const KVT*>(a.v) + (int64_t)b * g.sb + (int64_t)gh * g.sh;
+  const int64_t self_t = (!DENSE && a.self_ungated) ? T - 1 : -1;
+  const bool use_lo = a.q_dtype == ETA_DT_F32;
+  float m_[G], l_[G], acc[G][DPL];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    m_[h] = kNegInf;
+    l_[h] = 0.f;
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) acc[h][e] = 0.f;
+  }
+  auto attend = [&](int64_t t0, int nvalid, uint32_t bits) {
+    if constexpr (BF)
+      attend_bf16<D, G, DENSE>(kb, vb, g.st, t0, nvalid, bits, qa_s, use_lo, teff_s, p_s[w],
+                               a.beta, scale, self_t, lane, m_, l_, acc);
+    else
+      attend_f32<D, G, DENSE>(kb, vb, g.st, t0, nvalid, bits, qf_s,
+                              teff_s, reinterpret_cast<float (*)[G]>(p_s[w]), a.beta, self_t, lane,
+                              m_, l_, acc);
+  };
+  constexpr uint32_t all_bits = (1u << G) - 1u;
+  for (int64_t it = lo + w; it < hi; it += 4) {
+    int64_t j;
+    uint32_t bits;
+    if constexpr (DENSE) {
+      j = it;
+      bits = all_bits;
+    } else {
+      int tl = 0, th = g.n_tiles;       // pref_s[tl] <= it < pref_s[th]
+      while (th - tl > 1) {
+        const int mid = (tl + th) >> 1;
+        if (pref_s[mid] <= it) tl = mid; else th = mid;
+      }
+      j = a.ids[bg * g.ncap + (int64_t)tl * kScreenTile + (it - pref_s[tl])];
+      bits = a.hm[bg * g.ncap + j];
+    }
+    attend(j * BS, BS, bits);
+  }
+  if (s == S - 1 && ntail > 0 && w == 0) attend(N * BS, ntail, all_bits);
+
+  // merge the four wavefront states
+  if (lane == 0) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) { mrg_ml[w][h][0] = m_[h]; mrg_ml[w][h][1] = l_[h]; }
+  }
+#pragma unroll
+  for (int h = 0; h < G; ++h)
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) mrg_acc[w][h][lane * DPL + e] = acc[h][e];
+  __syncthreads();
+  for (int idx = tid; idx < G * D; idx += 256) {
+    const int h = idx / D, i = idx % D;
+    float ms = kNegInf;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) ms = fmaxf(ms, mrg_ml[k][h][0]);
+    float L = 0.f, o = 0.f;
+    if (ms != kNegInf) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float mk = mrg_ml[k][h][0];
+        if (mk == kNegInf) continue;
+        const float wk = __expf(mk - ms);
+        L = fmaf(mrg_ml[k][h][1], wk, L);
+        o = fmaf(mrg_acc[k][h][i], wk, o);
+      }
+    }
+    const int64_t row = (hq0 + h) * S + s;
+    a.part_acc[row * D + i] = o;
+    if (i == 0) a.part_ml[row] = make_float2(ms, L);
+  }
+}
+
+// ---------------------------------------------------------------- combine
+
+struct CombineArgs {
+  const float2* part_ml;
+  const float* part_acc;
+  const int32_t* head_cnt;
+  const int32_t* seq_lens;
+  int32_t* counts;
+  void* out;
+  Geom g;
+  int q_dtype;
+  int S;
+};
+
+template <int D>
+__global__ __launch_bounds__(D) void combine_kernel(CombineArgs a) {
+  const Geom& g = a.g;
+  const int h = blockIdx.x, b = blockIdx.y, i = threadIdx.x;
+  const int64_t row = (int64_t)b * g.Hq + h;
+  const float2* ml = a.part_ml + row * a.S;
+  float ms = kNegInf;
+  for (int s = 0; s < a.S; ++s) ms = fmaxf(ms, ml[s].x);
+  float L = 0.f, o = 0.f;
+  if (ms != kNegInf) {
+    for (int s = 0; s < a.S; ++s) {
+      const float2 e = ml[s];
+      if (e.x == kNegInf) continue;
+      const float wk = __expf(e.x - ms);
+      L = fmaf(e.y, wk, L);
+      o = fmaf(wk, a.part_acc[(row * a.S + s) * D + i], o);
+    }
+  }
+  store_out(a.out, a.q_dtype, row * D + i, L > 0.f ? o / L : 0.f);
+  if (a.counts != nullptr && i == 0) {
+    const int64_t T = clamp_len(a.seq_lens, b, g.cap);
+    const int64_t N = T / g.BS;
+    int64_t c = 0;
+    for (int t = 0; t < g.n_tiles; ++t) c += a.head_cnt[row * g.n_tiles + t];
+    a.counts[row] = (int32_t)(c * g.BS + (T - N * g.BS));
+  }
+}
+
+template <typename F>
+hipError_t with_hook(LaunchHook hook, int kind, hipStream_t st, F&& f) {
+  if (hook) hook(kind, st, false);
+  f();
+  hipError_t e = hipGetLastError();
+  if (hook) hook(kind, st, true);
+  return e;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- launchers
+
+hipError_t launch_summaries(const Geom& g, const void* k, const int32_t* seq_lens,
+                            const eta_summary_t& s, hipStream_t stream, LaunchHook hook) {
+  const int64_t nblk = g.cap / g.BS;
+  if (nblk <= 0) return hipSuccess;
+  dim3 grid((unsigned)((nblk + kSumBlocks - 1) / kSumBlocks), g.Hkv, g.B);
+  return with_hook(hook, ETA_KERNEL_SUMMARIES, stream, [&] {
+#define ETA_SUM(D_, BS_, T_)                                                                    \
+  if (g.D == D_ && g.BS == BS_)                                                                 \
+    hipLaunchKernelGGL((summaries_kernel<D_, BS_, T_>), grid, dim3(256), 0, stream,             \
+                       reinterpret_cast<const T_*>(k), g, seq_lens, s.mu, s.sigma, s.max_norm);
+    if (g.kv_dtype == ETA_DT_F32) {
+      ETA_SUM(64, 64, float) ETA_SUM(64, 128, float) ETA_SUM(128, 64, float) ETA_SUM(128, 128, float)
+    } else {
+      ETA_SUM(64, 64, uint16_t) ETA_SUM(64, 128, uint16_t) ETA_SUM(128, 64, uint16_t)
+      ETA_SUM(128, 128, uint16_t)
+    }
+#undef ETA_SUM
+  });
+}
+
+hipError_t launch_predict(int B, int Hq, int D, int q_dtype, const void* q, const float* W,
+                          const float* bias, float* tau, hipStream_t stream, LaunchHook hook) {
+  return with_hook(hook, ETA_KERNEL_PREDICT, stream, [&] {
+    hipLaunchKernelGGL(predict_kernel, dim3(B), dim3(256), 0, stream, q, q_dtype, W, bias, tau, Hq,
+                       D);
+  });
+}
+
+namespace {
+
+template <bool BOUNDS_ONLY>
+void launch_screen_impl(const Geom& g, const ScreenArgs& sa, hipStream_t stream) {
+  dim3 grid(g.n_tiles, g.Hkv, g.B);
+#define ETA_SCR(D_, G_)                                                                         \
+  if (g.D == D_ && g.G == G_)                                                                   \
+    hipLaunchKernelGGL((screen_kernel<D_, G_, BOUNDS_ONLY>), grid, dim3(256), 0, stream, sa);
+  ETA_SCR(64, 1) ETA_SCR(64, 2) ETA_SCR(64, 4) ETA_SCR(64, 8)
+  ETA_SCR(128, 1) ETA_SCR(128, 2) ETA_SCR(128, 4) ETA_SCR(128, 8)
+#undef ETA_SCR
+}
+
+template <bool DENSE>
+void launch_split_impl(const Geom& g, int S, const SplitArgs& sp, hipStream_t stream) {
+  dim3 grid(S, g.Hkv, g.B);
+#define ETA_SPL(D_, BS_, G_, T_)                                                                \
+  if (g.D == D_ && g.BS == BS_ && g.G == G_)                                                    \
+    hipLaunchKernelGGL((split_kernel<D_, BS_, G_, T_, DENSE>), grid, dim3(256), 0, stream, sp);
+#define ETA_SPL_G(D_, BS_, T_) \
+  ETA_SPL(D_, BS_, 1, T_) ETA_SPL(D_, BS_, 2, T_) ETA_SPL(D_, BS_, 4, T_) ETA_SPL(D_, BS_, 8, T_)
+  if (g.kv_dtype == ETA_DT_F32) {
+    ETA_SPL_G(64, 64, float) ETA_SPL_G(64, 128, float) ETA_SPL_G(128, 64, float)
+    ETA_SPL_G(128, 128, float)
+  } else {
+    ETA_SPL_G(64, 64, uint16_t) ETA_SPL_G(64, 128, uint16_t) ETA_SPL_G(128, 64, uint16_t)
+    ETA_SPL_G(128, 128, uint16_t)
+  }
+#undef ETA_SPL_G
+#undef ETA_SPL
+}
+
+void launch_combine_impl(const Geom& g, const CombineArgs& ca, hipStream_t stream) {
+  dim3 grid(g.Hq, g.B);
+  if (g.D == 64) hipLaunchKernelGGL(combine_kernel<64>, grid, dim3(64), 0, stream, ca);
+  if (g.D == 128) hipLaunchKernelGGL(combine_kernel<128>, grid, dim3(128), 0, stream, ca);
+}
+
+}  // namespace
+
+hipError_t launch_decode(const Geom& g, const DecodeCfg& c, int q_dtype, const void* q,
+                         const void* k, const void* v, const int32_t* seq_lens,
+                         const eta_summary_t& s, const float* tau, void* out, uint8_t* mask,
+                         int32_t* counts, const DecodeWs& ws, hipStream_t stream,
+                         LaunchHook hook) {
+  ScreenArgs sa{q, seq_lens, tau, s.mu, s.sigma, s.max_norm, mask, ws.hm, ws.ids, ws.tile_cnt,
+                ws.head_cnt, nullptr, g, q_dtype, c.z, c.offset_a, c.rescue_window, c.lwb,
+                c.screen_all};
+  hipError_t e = with_hook(hook, ETA_KERNEL_SCREEN, stream,
+                           [&] { launch_screen_impl<false>(g, sa, stream); });
+  if (e != hipSuccess) return e;
+  SplitArgs sp{q, k, v, seq_lens, tau, ws.hm, ws.ids, ws.tile_cnt, ws.part_ml, ws.part_acc,
+               g, q_dtype, c.beta, c.offset_a, c.self_ungated};
+  e = with_hook(hook, ETA_KERNEL_SPLIT_DECODE, stream,
+                [&] { launch_split_impl<false>(g, c.S, sp, stream); });
+  if (e != hipSuccess) return e;
+  CombineArgs ca{ws.part_ml, ws.part_acc, ws.head_cnt, seq_lens, counts, out, g, q_dtype, c.S};
+  return with_hook(hook, ETA_KERNEL_COMBINE, stream, [&] { launch_combine_impl(g, ca, stream); });
+}
+
+hipError_t launch_bounds(const Geom& g, int q_dtype, const void* q, const int32_t* seq_lens,
+                         const eta_summary_t& s, float z, float* bounds, hipStream_t stream,
+                         LaunchHook hook) {
+  ScreenArgs sa{q, seq_lens, nullptr, s.mu, s.sigma, s.max_norm, nullptr, nullptr, nullptr,
+                nullptr, nullptr, bounds, g, q_dtype, z, 0.f, 0, 0, 0};
+  return with_hook(hook, ETA_KERNEL_BOUNDS, stream,
+                   [&] { launch_screen_impl<true>(g, sa, stream); });
+}
+
+hipError_t launch_dense(const Geom& g, int S, int q_dtype, const void* q, const void* k,
+                        const void* v, const int32_t* seq_lens, void* out, const DecodeWs& ws,
+                        hipStream_t stream, LaunchHook hook) {
+  SplitArgs sp{q, k, v, seq_lens, nullptr, nullptr, nullptr, nullptr, ws.part_ml, ws.part_acc,
+               g, q_dtype, 0.f, 0.f, 0};
+  hipError_t e = with_hook(hook, ETA_KERNEL_DENSE_SPLIT, stream,
+                           [&] { launch_split_impl<true>(g, S, sp, stream); });
+  if (e != hipSuccess) return e;
+  CombineArgs ca{ws.part_ml, ws.part_acc, nullptr, seq_lens, nullptr, out, g, q_dtype, S};
+  return with_hook(hook, ETA_KERNEL_DENSE_COMBINE, stream,
+                   [&] { launch_combine_impl(g, ca, stream); });
+}
+
+}  // namespace eta

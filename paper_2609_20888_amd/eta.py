@@ -1,0 +1,286 @@
+"""Python binding of libeta (include/eta.h): argument marshalling only.
+
+Every function here hands torch tensors' device pointers and the current HIP
+stream to the C ABI of the same name; all computation runs in the library's
+HIP kernels.  There is no fallback: if ``libeta.so`` is missing or a call
+fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libeta.so")
+
+ETA_OK, ETA_ERR_INVALID_ARG, ETA_ERR_UNSUPPORTED, ETA_ERR_WORKSPACE, ETA_ERR_HIP = range(5)
+ETA_DT_F32, ETA_DT_BF16 = 0, 1
+KERNEL_KINDS = ("summaries", "predict", "screen", "split_decode", "combine", "dense_split",
+                "dense_combine", "bounds")
+
+_vp = ctypes.c_void_p
+
+
+class KvDesc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("block_size", ctypes.c_int32), ("kv_dtype", ctypes.c_int32),
+                ("capacity_tokens", ctypes.c_int64),
+                ("stride_b", ctypes.c_int64), ("stride_h", ctypes.c_int64),
+                ("stride_t", ctypes.c_int64)]
+
+
+class SummaryDesc(ctypes.Structure):
+    _fields_ = [("mu", _vp), ("sigma", _vp), ("max_norm", _vp), ("n_blk_cap", ctypes.c_int64)]
+
+
+class DecodeParams(ctypes.Structure):
+    _fields_ = [("beta", ctypes.c_float), ("z", ctypes.c_float), ("offset_a", ctypes.c_float),
+                ("rescue_window_blocks", ctypes.c_int32), ("pin_recent_blocks", ctypes.c_int32),
+                ("self_ungated", ctypes.c_int32), ("screen_all", ctypes.c_int32),
+                ("num_splits", ctypes.c_int32)]
+
+
+class KernelTime(ctypes.Structure):
+    _fields_ = [("ms_total", ctypes.c_double), ("launches", ctypes.c_int64)]
+
+
+# Symbols include/eta.h declares (the CPU test checks the library exports each).
+EXPORTS = ("eta_build_block_summaries", "eta_predict_threshold", "eta_decode_workspace_size",
+           "eta_decode", "eta_block_bounds", "eta_dense_workspace_size", "eta_dense_decode",
+           "eta_last_error_string", "eta_abi_version", "eta_profile_begin", "eta_profile_end")
+
+
+class EtaError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"libeta status {status}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def load_library(path: Optional[str] = None):
+    """Load libeta.so (built by ``paper_2609_20888_amd.build``); raise if it is missing."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"{p} is not built: run `python -m paper_2609_20888_amd.build` "
+                           "(there is no non-HIP fallback)")
+    lib = ctypes.CDLL(p)
+    P = ctypes.POINTER
+    i32, i64, f32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+    sz = ctypes.c_size_t
+    sigs = {
+        "eta_build_block_summaries": [P(KvDesc), _vp, _vp, P(SummaryDesc), _vp],
+        "eta_predict_threshold": [i32, i32, i32, i32, _vp, _vp, _vp, _vp, _vp],
+        "eta_decode_workspace_size": [P(KvDesc), P(DecodeParams), P(sz)],
+        "eta_decode": [P(KvDesc), i32, _vp, _vp, _vp, _vp, P(SummaryDesc), _vp, P(DecodeParams),
+                       _vp, _vp, _vp, _vp, sz, _vp],
+        "eta_block_bounds": [P(KvDesc), i32, _vp, _vp, P(SummaryDesc), f32, _vp, _vp],
+        "eta_dense_workspace_size": [P(KvDesc), i32, P(sz)],
+        "eta_dense_decode": [P(KvDesc), i32, _vp, _vp, _vp, _vp, _vp, i32, _vp, sz, _vp],
+        "eta_profile_begin": [],
+        "eta_profile_end": [P(KernelTime)],
+    }
+    for name, args in sigs.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    lib.eta_last_error_string.restype = ctypes.c_char_p
+    lib.eta_last_error_string.argtypes = []
+    lib.eta_abi_version.restype = ctypes.c_int32
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != ETA_OK:
+        raise EtaError(status, load_library().eta_last_error_string().decode())
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return ETA_DT_F32
+    if t.dtype == torch.bfloat16:
+        return ETA_DT_BF16
+    raise TypeError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else _vp(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return _vp(s.cuda_stream)
+
+
+# ---------------------------------------------------------------- descriptors
+
+def kv_desc(k: torch.Tensor, num_q_heads: int, block_size: int) -> KvDesc:
+    """Descriptor of a [B][Hkv][T_cap][d] cache (any strides, head dim contiguous)."""
+    if k.dim() != 4 or k.stride(3) != 1:
+        raise ValueError("K/V must be 4-D [B][Hkv][T_cap][d] with a contiguous head dimension")
+    B, Hkv, T_cap, d = k.shape
+    return KvDesc(batch=B, num_q_heads=num_q_heads, num_kv_heads=Hkv, head_dim=d,
+                  block_size=block_size, kv_dtype=_dtype_code(k), capacity_tokens=T_cap,
+                  stride_b=k.stride(0), stride_h=k.stride(1), stride_t=k.stride(2))
+
+
+@dataclass
+class Summaries:
+    """Block index: mu, sigma [B][Hkv][d][n_blk_cap] (dimension-major), max_norm [B][Hkv][n_blk_cap]."""
+    mu: torch.Tensor
+    sigma: torch.Tensor
+    max_norm: torch.Tensor
+
+    @property
+    def n_blk_cap(self) -> int:
+        return self.mu.shape[-1]
+
+    def desc(self) -> SummaryDesc:
+        return SummaryDesc(mu=_ptr(self.mu), sigma=_ptr(self.sigma), max_norm=_ptr(self.max_norm),
+                           n_blk_cap=self.n_blk_cap)
+
+    @staticmethod
+    def empty(B: int, Hkv: int, d: int, n_blk_cap: int, device) -> "Summaries":
+        n = max(int(n_blk_cap), 1)
+        return Summaries(mu=torch.zeros(B, Hkv, d, n, device=device, dtype=torch.float32),
+                         sigma=torch.zeros(B, Hkv, d, n, device=device, dtype=torch.float32),
+                         max_norm=torch.zeros(B, Hkv, n, device=device, dtype=torch.float32))
+
+
+def decode_params(*, beta=4.0, z=1.0, offset_a=0.0, rescue_window=128, lwb=0,
+                  self_ungated=False, screen_all=False, num_splits=0) -> DecodeParams:
+    return DecodeParams(beta=beta, z=z, offset_a=offset_a, rescue_window_blocks=rescue_window,
+                        pin_recent_blocks=lwb, self_ungated=int(bool(self_ungated)),
+                        screen_all=int(bool(screen_all)), num_splits=num_splits)
+
+
+# ---------------------------------------------------------------- entry points
+
+def build_block_summaries(k: torch.Tensor, seq_lens: torch.Tensor, block_size: int, *,
+                          num_q_heads: Optional[int] = None, out: Optional[Summaries] = None,
+                          stream=None) -> Summaries:
+    """eta_build_block_summaries: mu, sigma, M of every full block of K."""
+    B, Hkv, T_cap, d = k.shape
+    desc = kv_desc(k, num_q_heads or Hkv, block_size)
+    if out is None:
+        out = Summaries.empty(B, Hkv, d, T_cap // block_size, k.device)
+    sd = out.desc()
+    _check(load_library().eta_build_block_summaries(ctypes.byref(desc), _ptr(k), _ptr(seq_lens),
+                                                    ctypes.byref(sd), _stream(stream)))
+    return out
+
+
+def predict_threshold(q: torch.Tensor, W: Optional[torch.Tensor], bias: torch.Tensor, *,
+                      out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """eta_predict_threshold: tau[B][Hq] = concat(q[b]) W + bias (W None: tau = bias)."""
+    B, Hq, d = q.shape
+    if out is None:
+        out = torch.empty(B, Hq, device=q.device, dtype=torch.float32)
+    _check(load_library().eta_predict_threshold(B, Hq, d, _dtype_code(q), _ptr(q), _ptr(W),
+                                                _ptr(bias), _ptr(out), _stream(stream)))
+    return out
+
+
+def decode_workspace_size(desc: KvDesc, params: DecodeParams) -> int:
+    n = ctypes.c_size_t()
+    _check(load_library().eta_decode_workspace_size(ctypes.byref(desc), ctypes.byref(params),
+                                                    ctypes.byref(n)))
+    return n.value
+
+
+def alloc_workspace(nbytes: int, device) -> torch.Tensor:
+    """Workspace buffer (torch's caching allocator returns 256-byte aligned blocks)."""
+    t = torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+    assert t.data_ptr() % 256 == 0
+    return t
+
+
+@dataclass
+class DecodeOut:
+    out: torch.Tensor            # [B][Hq][d], dtype of q
+    mask: torch.Tensor           # [B][Hq][n_blk_cap] uint8
+    counts: Optional[torch.Tensor]  # [B][Hq] int32
+
+
+def decode(q, k, v, seq_lens, summ: Summaries, tau, *, block_size: int,
+           params: Optional[DecodeParams] = None, out=None, mask=None, counts=None,
+           want_counts: bool = True, workspace: Optional[torch.Tensor] = None,
+           stream=None) -> DecodeOut:
+    """eta_decode: one ETA decode step -> output, selected-block mask, attended token counts."""
+    B, Hq, d = q.shape
+    p = params if params is not None else decode_params()
+    desc = kv_desc(k, Hq, block_size)
+    if v.shape != k.shape or v.stride() != k.stride() or v.dtype != k.dtype:
+        raise ValueError("K and V must share shape, strides and dtype")
+    if out is None:
+        out = torch.empty_like(q)
+    if mask is None:
+        mask = torch.empty(B, Hq, summ.n_blk_cap, dtype=torch.uint8, device=q.device)
+    if counts is None and want_counts:
+        counts = torch.empty(B, Hq, dtype=torch.int32, device=q.device)
+    nbytes = decode_workspace_size(desc, p)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = alloc_workspace(nbytes, q.device)
+    sd = summ.desc()
+    _check(load_library().eta_decode(ctypes.byref(desc), _dtype_code(q), _ptr(q), _ptr(k), _ptr(v),
+                                     _ptr(seq_lens), ctypes.byref(sd), _ptr(tau), ctypes.byref(p),
+                                     _ptr(out), _ptr(mask), _ptr(counts), _ptr(workspace),
+                                     workspace.numel(), _stream(stream)))
+    return DecodeOut(out=out, mask=mask, counts=counts)
+
+
+def block_bounds(q, seq_lens, summ: Summaries, k_like: torch.Tensor, *, block_size: int,
+                 z: float, out=None, stream=None) -> torch.Tensor:
+    """eta_block_bounds: the screening bound of every full block and query head (NaN beyond N_b)."""
+    B, Hq, d = q.shape
+    desc = kv_desc(k_like, Hq, block_size)
+    if out is None:
+        out = torch.empty(B, Hq, summ.n_blk_cap, dtype=torch.float32, device=q.device)
+    sd = summ.desc()
+    _check(load_library().eta_block_bounds(ctypes.byref(desc), _dtype_code(q), _ptr(q),
+                                           _ptr(seq_lens), ctypes.byref(sd), ctypes.c_float(z),
+                                           _ptr(out), _stream(stream)))
+    return out
+
+
+def dense_workspace_size(desc: KvDesc, num_splits: int = 0) -> int:
+    n = ctypes.c_size_t()
+    _check(load_library().eta_dense_workspace_size(ctypes.byref(desc), num_splits, ctypes.byref(n)))
+    return n.value
+
+
+def dense_decode(q, k, v, seq_lens, *, block_size: int = 64, num_splits: int = 0, out=None,
+                 workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """eta_dense_decode: plain softmax attention over every token (the dense baseline)."""
+    B, Hq, d = q.shape
+    desc = kv_desc(k, Hq, block_size)
+    if out is None:
+        out = torch.empty_like(q)
+    nbytes = dense_workspace_size(desc, num_splits)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = alloc_workspace(nbytes, q.device)
+    _check(load_library().eta_dense_decode(ctypes.byref(desc), _dtype_code(q), _ptr(q), _ptr(k),
+                                           _ptr(v), _ptr(seq_lens), _ptr(out), num_splits,
+                                           _ptr(workspace), workspace.numel(), _stream(stream)))
+    return out
+
+
+def profile_begin():
+    _check(load_library().eta_profile_begin())
+
+
+def profile_end() -> dict:
+    arr = (KernelTime * len(KERNEL_KINDS))()
+    _check(load_library().eta_profile_end(arr))
+    return {name: (arr[i].ms_total, arr[i].launches) for i, name in enumerate(KERNEL_KINDS)}

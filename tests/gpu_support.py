@@ -1,0 +1,195 @@
+"""Helpers for the GPU parity tests: run a workload through the HIP library
+(C ABI via the binding) and through the fp64 oracle, and compare.
+
+Parity rules (the path's contract):
+  * block masks: identical, except blocks whose oracle bound lies within
+    TIE_BAND of tau_eff (the fp32 GPU and fp64 oracle may decide those either
+    way).  Such a row is compared against the oracle re-run (external-mask
+    mode) on the variant of the oracle's own mask that flips exactly the band
+    blocks the GPU decided the other way.  A rescue decision may differ only
+    when the rescue window's two largest bounds are within TIE_BAND of each
+    other; such rows are checked outside the window only and counted as
+    skipped.
+  * attended-token counts: identical on rows compared.
+  * outputs: max_i |o_gpu - o_ref| / max_i |o_ref| per (sequence, head) row
+    <= 2e-2 for bf16 and <= 1e-4 for fp32.
+"""
+from __future__ import annotations
+
+import math
+import sys
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+import oracle
+from paper_2609_20888_amd import eta
+from synth import Workload, as_numpy, place_bias
+
+TIE_BAND = 1e-4
+TOL = {torch.bfloat16: 2e-2, torch.float32: 1e-4}
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def require_gpu():
+    if not torch.cuda.is_available():
+        raise RuntimeError("GPU test needs a ROCm GPU (torch.cuda.is_available() is False)")
+
+
+@dataclass
+class GpuRun:
+    out: torch.Tensor
+    mask: torch.Tensor
+    counts: torch.Tensor
+    tau: torch.Tensor
+    summ: eta.Summaries
+
+
+def oracle_inputs(wl: Workload):
+    return as_numpy(wl.q), as_numpy(wl.k), as_numpy(wl.v)
+
+
+def calibrate_bias(wl: Workload, np_inputs=None) -> None:
+    """Predictor-mode workloads: set wl.bias from the oracle's bounds for the target survival."""
+    if wl.W is None or wl.target_survival is None:
+        return
+    q, k, v = np_inputs or oracle_inputs(wl)
+    r = oracle.decode(q, k, v, wl.seq_lens, None, block_size=wl.block, z=wl.z, bounds_only=True)
+    qW = oracle.predict(q, as_numpy(wl.W), None)
+    nb = [t // wl.block for t in wl.seq_lens]
+    bias = place_bias(r.bounds, nb, qW, wl.target_survival, wl.a)
+    wl.bias = torch.as_tensor(bias, device=wl.bias.device)
+
+
+def run_gpu(wl: Workload, *, num_splits: int = 0, screen_all: bool = False,
+            self_ungated: bool = False, tau: Optional[torch.Tensor] = None,
+            rescue_window: Optional[int] = None) -> GpuRun:
+    dev = torch.device("cuda")
+    q, k, v = wl.q.to(dev), wl.k.to(dev), wl.v.to(dev)
+    sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
+    summ = eta.build_block_summaries(k, sl, wl.block, num_q_heads=wl.Hq)
+    if tau is None:
+        W = None if wl.W is None else wl.W.to(dev)
+        tau = eta.predict_threshold(q, W, wl.bias.to(dev))
+    p = eta.decode_params(beta=wl.beta, z=wl.z, offset_a=wl.a,
+                          rescue_window=wl.rescue_window if rescue_window is None else rescue_window,
+                          lwb=wl.lwb, self_ungated=self_ungated, screen_all=screen_all,
+                          num_splits=num_splits)
+    r = eta.decode(q, k, v, sl, summ, tau, block_size=wl.block, params=p)
+    torch.cuda.synchronize()
+    return GpuRun(out=r.out, mask=r.mask, counts=r.counts, tau=tau, summ=summ)
+
+
+def run_oracle(wl: Workload, np_inputs=None, rows: Optional[Sequence[int]] = None,
+               screen_all: bool = False, self_ungated: bool = False, tau=None,
+               rescue_window: Optional[int] = None):
+    q, k, v = np_inputs or oracle_inputs(wl)
+    if tau is None:
+        W = None if wl.W is None else as_numpy(wl.W)
+        tau = oracle.predict(q, W, as_numpy(wl.bias))
+    return oracle.decode(q, k, v, wl.seq_lens, tau, block_size=wl.block, beta=wl.beta, z=wl.z,
+                         a=wl.a,
+                         rescue_window=wl.rescue_window if rescue_window is None else rescue_window,
+                         lwb=wl.lwb, self_ungated=self_ungated, screen_all=screen_all, rows=rows,
+                         n_threads=0), tau
+
+
+def _f64(t: torch.Tensor) -> np.ndarray:
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def _band_variants(om: np.ndarray, band_idx: np.ndarray):
+    """The oracle's mask with every subset of the tie-band blocks flipped."""
+    k = band_idx.size
+    for bitsel in range(1 << k):
+        m = om.copy()
+        for t in range(k):
+            if (bitsel >> t) & 1:
+                m[band_idx[t]] ^= 1
+        yield m
+
+
+def compare(wl: Workload, g: GpuRun, orc, tau_oracle: np.ndarray,
+            rows: Optional[Sequence[int]] = None, min_compared: float = 0.9,
+            rescue_window: Optional[int] = None, np_inputs=None, screen_all: bool = False,
+            self_ungated: bool = False, max_band: int = 6) -> dict:
+    """Check masks / counts / outputs of the given rows; returns statistics.
+
+    A row whose oracle bounds put blocks inside the tie band is compared
+    against the oracle run on each of its own masks with those blocks flipped
+    (the oracle's external-mask mode): the GPU mask must be one of them and the
+    GPU output must match the oracle output for that mask.
+    """
+    B, Hq = wl.B, wl.Hq
+    rows = list(range(B * Hq)) if rows is None else list(rows)
+    c = wl.rescue_window if rescue_window is None else rescue_window
+    mask = g.mask.cpu().numpy()
+    counts = g.counts.cpu().numpy()
+    out = _f64(g.out)
+    tol = TOL[wl.dtype]
+    Ncap = wl.n_blk_cap
+    compared, banded, skipped, worst = 0, 0, 0, 0.0
+    for row in rows:
+        b, h = divmod(row, Hq)
+        N = wl.seq_lens[b] // wl.block
+        gm = mask[b, h]
+        om = orc.sel[b, h, :N]
+        assert np.all(gm[N:Ncap] == 0), f"row {row}: mask set beyond the full blocks"
+        bnd = orc.bounds[b, h, :N]
+        teff = tau_oracle[b, h] - wl.a
+        band = (np.abs(bnd - teff) <= TIE_BAND) if not screen_all else np.zeros(N, bool)
+        Wn = min(c, N)
+        rescue_tie = False
+        if Wn >= 2 and c > 0 and orc.rescued[b, h] >= 0:
+            top = np.sort(bnd[:Wn])[::-1]
+            rescue_tie = bool(top[0] - top[1] <= TIE_BAND)
+        diff = np.nonzero(gm[:N] != om)[0]
+        ref_o, ref_n = orc.o[b, h], orc.counts[b, h]
+        if rescue_tie:
+            skipped += 1
+            bad = [j for j in diff if not band[j] and j >= Wn]
+            assert not bad, f"row {row}: mask differs outside the rescue window / tie band at {bad[:8]}"
+            continue
+        if band.any():
+            banded += 1
+            bad = [j for j in diff if not band[j]]
+            assert not bad, f"row {row}: mask differs outside the tie band at blocks {bad[:8]}"
+            bidx = np.nonzero(band)[0]
+            if bidx.size > max_band:
+                skipped += 1
+                continue
+            assert np_inputs is not None, "tie-band rows need the oracle inputs"
+            q, k, v = np_inputs
+            found = False
+            for var in _band_variants(om, bidx):
+                full = np.zeros((B, Hq, max(Ncap, 1)), np.uint8)
+                full[b, h, :N] = var
+                rv = oracle.decode(q, k, v, wl.seq_lens, tau_oracle, block_size=wl.block,
+                                   beta=wl.beta, z=wl.z, a=wl.a, rescue_window=c, lwb=wl.lwb,
+                                   self_ungated=self_ungated, rows=[row], sel_in=full[:, :, :Ncap])
+                if np.array_equal(var, gm[:N]):
+                    ref_o, ref_n = rv.o[b, h], rv.counts[b, h]
+                    found = True
+            assert found, f"row {row}: GPU mask is not any tie-band variant of the oracle mask"
+        else:
+            assert diff.size == 0, (f"row {row}: mask differs at blocks {diff[:8].tolist()} "
+                                    f"(bounds {bnd[diff[:4]]}, tau_eff {teff})")
+        assert counts[b, h] == ref_n, f"row {row}: counts {counts[b, h]} vs {ref_n}"
+        scale = np.max(np.abs(ref_o))
+        if scale == 0.0:
+            assert np.all(out[b, h] == 0.0), f"row {row}: expected a zero output"
+            compared += 1
+            continue
+        err = float(np.max(np.abs(out[b, h] - ref_o)) / scale)
+        worst = max(worst, err)
+        assert err <= tol, f"row {row}: max rel error {err:.3e} > {tol:.1e}"
+        compared += 1
+    assert compared >= min_compared * len(rows), \
+        f"only {compared} of {len(rows)} rows compared ({skipped} skipped)"
+    return {"compared": compared, "band_rows": banded, "skipped": skipped, "worst_rel_err": worst}

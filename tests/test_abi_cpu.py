@@ -1,0 +1,145 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, and rejects bad arguments on the host before any launch."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_20888_amd import eta
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "eta.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return eta.load_library()
+
+
+def test_header_declarations_are_all_exported(lib):
+    text = open(HEADER).read()
+    declared = set(re.findall(r"^\s*(?:eta_status_t|const char\*|int32_t)\s+(eta_\w+)\s*\(", text, re.M))
+    assert declared == set(eta.EXPORTS), declared ^ set(eta.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert lib.eta_abi_version() == 1
+
+
+def good_desc(**kw):
+    d = dict(batch=1, num_q_heads=16, num_kv_heads=4, head_dim=128, block_size=64,
+             kv_dtype=eta.ETA_DT_BF16, capacity_tokens=4096, stride_b=4 * 4096 * 128,
+             stride_h=4096 * 128, stride_t=128)
+    d.update(kw)
+    return eta.KvDesc(**d)
+
+
+def ws_size(lib, desc, params):
+    n = ctypes.c_size_t()
+    st = lib.eta_decode_workspace_size(ctypes.byref(desc), ctypes.byref(params), ctypes.byref(n))
+    return st, n.value
+
+
+def test_workspace_size_valid_and_monotone(lib):
+    p = eta.decode_params()
+    st, n1 = ws_size(lib, good_desc(), p)
+    assert st == eta.ETA_OK and n1 > 0 and n1 % 256 == 0
+    st, n2 = ws_size(lib, good_desc(capacity_tokens=8192), p)
+    assert st == eta.ETA_OK and n2 > n1
+    st, n3 = ws_size(lib, good_desc(), eta.decode_params(num_splits=512))
+    assert st == eta.ETA_OK and n3 > n1
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(batch=0), eta.ETA_ERR_INVALID_ARG),
+    (dict(num_kv_heads=3), eta.ETA_ERR_INVALID_ARG),             # 16 % 3 != 0
+    (dict(num_q_heads=32, num_kv_heads=2), eta.ETA_ERR_UNSUPPORTED),  # G = 16
+    (dict(head_dim=96, stride_t=96), eta.ETA_ERR_UNSUPPORTED),
+    (dict(block_size=32), eta.ETA_ERR_UNSUPPORTED),
+    (dict(capacity_tokens=0), eta.ETA_ERR_INVALID_ARG),
+    (dict(kv_dtype=7), eta.ETA_ERR_INVALID_ARG),
+    (dict(stride_t=100), eta.ETA_ERR_INVALID_ARG),                # < head_dim
+    (dict(stride_t=132), eta.ETA_ERR_INVALID_ARG),                # rows not 16-byte aligned
+    (dict(stride_h=-1), eta.ETA_ERR_INVALID_ARG),
+])
+def test_geometry_rejected(lib, kw, code):
+    st, _ = ws_size(lib, good_desc(**kw), eta.decode_params())
+    assert st == code
+    assert lib.eta_last_error_string().decode() != ""
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(beta=float("nan")), eta.ETA_ERR_INVALID_ARG),
+    (dict(beta=-1.0), eta.ETA_ERR_INVALID_ARG),
+    (dict(z=float("inf")), eta.ETA_ERR_INVALID_ARG),
+    (dict(offset_a=float("nan")), eta.ETA_ERR_INVALID_ARG),
+    (dict(rescue_window=-1), eta.ETA_ERR_INVALID_ARG),
+    (dict(rescue_window=257), eta.ETA_ERR_UNSUPPORTED),
+    (dict(lwb=-2), eta.ETA_ERR_INVALID_ARG),
+    (dict(num_splits=2000), eta.ETA_ERR_INVALID_ARG),
+])
+def test_params_rejected(lib, kw, code):
+    st, _ = ws_size(lib, good_desc(), eta.decode_params(**kw))
+    assert st == code
+
+
+FAKE = 0x10000          # aligned, never dereferenced: validation fails first or nothing launches
+
+
+def decode_call(lib, desc=None, q=FAKE, tau=FAKE, out=FAKE, mask=FAKE, ws=FAKE, ws_bytes=1 << 30,
+                summ=None, params=None):
+    desc = desc or good_desc()
+    summ = summ or eta.SummaryDesc(mu=FAKE, sigma=FAKE, max_norm=FAKE, n_blk_cap=64)
+    params = params or eta.decode_params()
+    return lib.eta_decode(ctypes.byref(desc), eta.ETA_DT_BF16, q, FAKE, FAKE, FAKE,
+                          ctypes.byref(summ), tau, ctypes.byref(params), out, mask, None, ws,
+                          ws_bytes, None)
+
+
+def test_decode_rejects_null_and_misaligned(lib):
+    assert decode_call(lib, q=None) == eta.ETA_ERR_INVALID_ARG
+    assert decode_call(lib, tau=None) == eta.ETA_ERR_INVALID_ARG
+    assert decode_call(lib, mask=None) == eta.ETA_ERR_INVALID_ARG
+    assert decode_call(lib, out=FAKE + 2) == eta.ETA_ERR_INVALID_ARG
+    assert "aligned" in lib.eta_last_error_string().decode()
+
+
+def test_decode_rejects_workspace_problems(lib):
+    assert decode_call(lib, ws=None) == eta.ETA_ERR_WORKSPACE
+    assert decode_call(lib, ws=FAKE + 16) == eta.ETA_ERR_WORKSPACE
+    assert decode_call(lib, ws_bytes=100) == eta.ETA_ERR_WORKSPACE
+    assert "too small" in lib.eta_last_error_string().decode()
+
+
+def test_decode_rejects_small_summary_capacity(lib):
+    s = eta.SummaryDesc(mu=FAKE, sigma=FAKE, max_norm=FAKE, n_blk_cap=63)   # 4096 / 64 = 64 needed
+    assert decode_call(lib, summ=s) == eta.ETA_ERR_INVALID_ARG
+    s = eta.SummaryDesc(mu=None, sigma=FAKE, max_norm=FAKE, n_blk_cap=64)
+    assert decode_call(lib, summ=s) == eta.ETA_ERR_INVALID_ARG
+
+
+def test_predict_rejects(lib):
+    f = lib.eta_predict_threshold
+    assert f(0, 16, 128, eta.ETA_DT_BF16, FAKE, None, FAKE, FAKE, None) == eta.ETA_ERR_INVALID_ARG
+    assert f(1, 300, 128, eta.ETA_DT_BF16, FAKE, None, FAKE, FAKE, None) == eta.ETA_ERR_UNSUPPORTED
+    assert f(1, 16, 128, 5, FAKE, None, FAKE, FAKE, None) == eta.ETA_ERR_INVALID_ARG
+    assert f(1, 16, 128, eta.ETA_DT_BF16, FAKE, None, None, FAKE, None) == eta.ETA_ERR_INVALID_ARG
+
+
+def test_dense_and_bounds_reject(lib):
+    d = good_desc()
+    n = ctypes.c_size_t()
+    assert lib.eta_dense_workspace_size(ctypes.byref(d), -1, ctypes.byref(n)) == eta.ETA_ERR_INVALID_ARG
+    assert lib.eta_dense_workspace_size(ctypes.byref(d), 0, ctypes.byref(n)) == eta.ETA_OK
+    assert lib.eta_dense_decode(ctypes.byref(d), eta.ETA_DT_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, 0,
+                                None, 1 << 20, None) == eta.ETA_ERR_WORKSPACE
+    s = eta.SummaryDesc(mu=FAKE, sigma=FAKE, max_norm=FAKE, n_blk_cap=64)
+    assert lib.eta_block_bounds(ctypes.byref(d), eta.ETA_DT_BF16, FAKE, FAKE, ctypes.byref(s),
+                                ctypes.c_float(-1.0), FAKE, None) == eta.ETA_ERR_INVALID_ARG
+
+
+def test_profile_roundtrip_without_launches(lib):
+    assert lib.eta_profile_begin() == eta.ETA_OK
+    arr = (eta.KernelTime * len(eta.KERNEL_KINDS))()
+    assert lib.eta_profile_end(arr) == eta.ETA_OK
+    assert all(arr[i].launches == 0 for i in range(len(eta.KERNEL_KINDS)))

@@ -1,0 +1,256 @@
+"""GPU parity of the HIP path against the fp64 oracle (needs an MI355X).
+
+Every test calls the C ABI through the binding on cuda:0 and compares with the
+oracle on the same seeded inputs: element by element at sizes that span several
+screening tiles and a ragged tail, and on sampled (sequence, head) rows at the
+full workload sizes, in the launch configuration the benchmark times.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_support import (GpuRun, calibrate_bias, compare, oracle_inputs, require_gpu, run_gpu,
+                         run_oracle, say)
+from paper_2609_20888_amd import eta
+from synth import as_numpy, config1, config2, config3, config4, config5, make_workload
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu(request):
+    require_gpu()
+    say(f"\n[gpu] {request.node.nodeid}")
+    yield
+    torch.cuda.synchronize()
+
+
+# ------------------------------------------------------------------ building blocks
+
+SUMMARY_CASES = [
+    # B, Hkv, d, b, lens, dtype
+    (2, 2, 128, 64, [20000, 17001], torch.bfloat16),
+    (1, 3, 64, 128, [9000], torch.bfloat16),
+    (2, 1, 64, 64, [5000, 63], torch.float32),
+    (1, 2, 128, 128, [128 * 40 + 5], torch.float32),
+]
+
+
+@pytest.mark.parametrize("case", range(len(SUMMARY_CASES)))
+def test_block_summaries_match_oracle(case):
+    B, Hkv, d, b, lens, dt = SUMMARY_CASES[case]
+    wl = make_workload(B=B, Hq=Hkv, Hkv=Hkv, d=d, block=b, seq_lens=lens, dtype=dt,
+                       planted={"frac": 0.1}, predictor=False, tau_const=1.0, seed=case)
+    dev = torch.device("cuda")
+    k = wl.k.to(dev)
+    sl = torch.tensor(lens, dtype=torch.int32, device=dev)
+    s = eta.build_block_summaries(k, sl, b)
+    torch.cuda.synchronize()
+    mu, sg, mx = s.mu.cpu().numpy(), s.sigma.cpu().numpy(), s.max_norm.cpu().numpy()
+    kn = as_numpy(wl.k)
+    for bb in range(B):
+        for g in range(Hkv):
+            N = lens[bb] // b
+            omu, osg, omx = oracle.summaries(kn[bb, g, :lens[bb]], b)
+            np.testing.assert_allclose(mu[bb, g, :, :N].T, omu, rtol=1e-5, atol=1e-5)
+            np.testing.assert_allclose(sg[bb, g, :, :N].T, osg, rtol=1e-5, atol=1e-5)
+            np.testing.assert_allclose(mx[bb, g, :N], omx, rtol=1e-6, atol=1e-6)
+
+
+@pytest.mark.parametrize("dt", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("Hq,d", [(16, 128), (32, 128), (4, 64), (12, 64)])
+def test_predict_threshold_matches_oracle(dt, Hq, d):
+    g = torch.Generator().manual_seed(Hq * d)
+    q = torch.randn(5, Hq, d, generator=g).to(dt)
+    W = torch.randn(Hq * d, Hq, generator=g) * 0.02
+    bias = torch.randn(Hq, generator=g)
+    dev = torch.device("cuda")
+    tau = eta.predict_threshold(q.to(dev), W.to(dev), bias.to(dev)).cpu().numpy()
+    ref = oracle.predict(as_numpy(q), W.numpy(), bias.numpy())
+    np.testing.assert_allclose(tau, ref, rtol=1e-5, atol=1e-5)
+    tau0 = eta.predict_threshold(q.to(dev), None, bias.to(dev)).cpu().numpy()
+    np.testing.assert_array_equal(tau0, np.tile(bias.numpy(), (5, 1)))
+
+
+@pytest.mark.parametrize("G,d,b,dt", [(4, 128, 64, torch.bfloat16), (8, 64, 128, torch.bfloat16),
+                                      (1, 64, 64, torch.float32), (2, 128, 128, torch.float32)])
+def test_block_bounds_match_oracle(G, d, b, dt):
+    wl = make_workload(B=2, Hq=2 * G, Hkv=2, d=d, block=b, seq_lens=[b * 300 + 7, b * 3],
+                       dtype=dt, planted={"frac": 0.05}, predictor=False, tau_const=1.0, seed=G)
+    dev = torch.device("cuda")
+    k = wl.k.to(dev)
+    sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
+    s = eta.build_block_summaries(k, sl, b, num_q_heads=wl.Hq)
+    for z in (0.0, 1.0, 2.0, 50.0):
+        gb = eta.block_bounds(wl.q.to(dev), sl, s, k, block_size=b, z=z).cpu().numpy()
+        q, kn, vn = oracle_inputs(wl)
+        r = oracle.decode(q, kn, vn, wl.seq_lens, None, block_size=b, z=z, bounds_only=True)
+        for bb in range(2):
+            N = wl.seq_lens[bb] // b
+            np.testing.assert_allclose(gb[bb, :, :N], r.bounds[bb, :, :N], rtol=2e-5, atol=2e-5)
+            assert np.all(np.isnan(gb[bb, :, N:]))
+
+
+# ------------------------------------------------------------------ decode parity
+
+DECODE_CASES = {
+    # name: (workload kwargs, run kwargs)
+    "gqa4_bf16_two_tiles_ragged": (dict(B=2, Hq=8, Hkv=2, d=128, block=64, seq_lens=[20000, 17000],
+                                        planted={"frac": 0.05}, predictor=True, target_survival=0.1,
+                                        seed=11), {}),
+    "gqa8_bf16_d64_b128": (dict(B=1, Hq=16, Hkv=2, d=64, block=128, seq_lens=[40000],
+                                planted={"frac": 0.03}, predictor=True, target_survival=0.2,
+                                seed=12), {}),
+    "mha_fp32_planted": (dict(B=2, Hq=2, Hkv=2, d=64, block=64, seq_lens=[5000, 130],
+                              dtype=torch.float32, planted={"count": 6}, per_head_planting=True,
+                              predictor=False, tau_const=2.0, seed=13), {}),
+    "gqa2_fp32_b128_d128": (dict(B=2, Hq=4, Hkv=2, d=128, block=128, seq_lens=[9000, 300],
+                                 dtype=torch.float32, planted={"frac": 0.1}, predictor=True,
+                                 target_survival=0.3, seed=14), {}),
+    "rescue_only": (dict(B=2, Hq=8, Hkv=2, d=128, block=64, seq_lens=[30000, 3000],
+                         predictor=False, tau_const=50.0, seed=15), {}),
+    "rescue_window_small": (dict(B=1, Hq=4, Hkv=1, d=64, block=64, seq_lens=[4000],
+                                 predictor=False, tau_const=50.0, rescue_window=5, seed=16), {}),
+    "rescue_off": (dict(B=1, Hq=4, Hkv=1, d=64, block=64, seq_lens=[4096 + 10],
+                        predictor=False, tau_const=50.0, rescue_window=0, seed=17), {}),
+    "pins": (dict(B=1, Hq=8, Hkv=2, d=128, block=64, seq_lens=[10000], predictor=False,
+                  tau_const=50.0, lwb=2, seed=18), {}),
+    "self_ungated": (dict(B=2, Hq=8, Hkv=2, d=128, block=64, seq_lens=[6401, 6400],
+                          planted={"frac": 0.05}, predictor=True, target_survival=0.1, seed=19),
+                     dict(self_ungated=True)),
+    "screen_all_dense_gated": (dict(B=1, Hq=8, Hkv=2, d=128, block=64, seq_lens=[7777],
+                                    predictor=False, tau_const=0.5, seed=20),
+                               dict(screen_all=True)),
+    "tau_minus_inf_plain_softmax": (dict(B=1, Hq=4, Hkv=4, d=64, block=64, seq_lens=[3000],
+                                         predictor=False, tau_const=-math.inf, seed=21), {}),
+    "tail_only_and_empty": (dict(B=3, Hq=4, Hkv=2, d=128, block=128, seq_lens=[50, 0, 127],
+                                 T_cap=256, predictor=False, tau_const=1.0, seed=22), {}),
+    "slack_offset": (dict(B=1, Hq=8, Hkv=2, d=128, block=64, seq_lens=[12345],
+                          planted={"frac": 0.05}, predictor=False, tau_const=2.2, a=0.3, seed=23),
+                     {}),
+    "splits_1": (dict(B=2, Hq=8, Hkv=2, d=128, block=64, seq_lens=[20000, 640],
+                      planted={"frac": 0.05}, predictor=True, target_survival=0.15, seed=24),
+                 dict(num_splits=1)),
+    "splits_1024": (dict(B=1, Hq=8, Hkv=2, d=128, block=64, seq_lens=[20000],
+                         planted={"frac": 0.05}, predictor=True, target_survival=0.15, seed=25),
+                    dict(num_splits=1024)),
+}
+
+
+@pytest.mark.parametrize("name", sorted(DECODE_CASES))
+def test_decode_matches_oracle(name):
+    wkw, rkw = DECODE_CASES[name]
+    wl = make_workload(**wkw)
+    np_in = oracle_inputs(wl)
+    calibrate_bias(wl, np_in)
+    g = run_gpu(wl, **rkw)
+    okw = {k: v for k, v in rkw.items() if k in ("screen_all", "self_ungated")}
+    orc, tau_o = run_oracle(wl, np_in, **okw)
+    stats = compare(wl, g, orc, tau_o, np_inputs=np_in, **okw)
+    say(f"[gpu] {name}: {stats}")
+
+
+def test_decode_fp32_query_on_bf16_cache():
+    # fp32 q with bf16 K/V: the scores use the hi + lo bf16 split of q
+    wl = make_workload(B=1, Hq=8, Hkv=2, d=128, block=64, seq_lens=[9000],
+                       planted={"frac": 0.05}, predictor=True, target_survival=0.1, seed=31)
+    wl.q = torch.randn(wl.q.shape, generator=torch.Generator().manual_seed(5))
+    wl.W = wl.W.float()
+    np_in = oracle_inputs(wl)
+    calibrate_bias(wl, np_in)
+    g = run_gpu(wl)
+    orc, tau_o = run_oracle(wl, np_in)
+    say(compare(wl, g, orc, tau_o, np_inputs=np_in))
+
+
+def test_decode_is_deterministic_and_split_invariant():
+    wl = make_workload(B=2, Hq=8, Hkv=2, d=128, block=64, seq_lens=[30000, 20000],
+                       planted={"frac": 0.05}, predictor=False, tau_const=1.6, seed=41)
+    a = run_gpu(wl)
+    b = run_gpu(wl)
+    assert torch.equal(a.out, b.out) and torch.equal(a.mask, b.mask)
+    assert torch.equal(a.counts, b.counts)
+    outs = [run_gpu(wl, num_splits=s) for s in (1, 5, 64, 300)]
+    for r in outs:
+        assert torch.equal(r.mask, a.mask) and torch.equal(r.counts, a.counts)
+        diff = (r.out.float() - a.out.float()).abs().max().item()
+        # bf16 outputs: split order changes fp32 rounding, at most one bf16 ulp flip
+        assert diff <= 2e-2 * a.out.float().abs().max().item()
+
+
+def test_dense_decode_matches_oracle():
+    for dt, d, b, lens in ((torch.bfloat16, 128, 64, [20000, 333]), (torch.float32, 64, 128, [5000])):
+        wl = make_workload(B=len(lens), Hq=8, Hkv=2, d=d, block=b, seq_lens=lens, dtype=dt,
+                           predictor=False, tau_const=0.0, seed=d)
+        dev = torch.device("cuda")
+        sl = torch.tensor(lens, dtype=torch.int32, device=dev)
+        out = eta.dense_decode(wl.q.to(dev), wl.k.to(dev), wl.v.to(dev), sl, block_size=b)
+        torch.cuda.synchronize()
+        q, k, v = oracle_inputs(wl)
+        r = oracle.decode(q, k, v, lens, np.zeros((wl.B, 8)), block_size=b, screen_all=True,
+                          gate_off=True)
+        o = out.float().cpu().numpy()
+        tol = 2e-2 if dt == torch.bfloat16 else 1e-4
+        for bb in range(wl.B):
+            for h in range(8):
+                ref = r.o[bb, h]
+                assert np.max(np.abs(o[bb, h] - ref)) / np.max(np.abs(ref)) <= tol
+
+
+# ------------------------------------------------------------------ full-size workloads
+
+def _sample_rows(B, Hq, n, seed):
+    rng = np.random.default_rng(seed)
+    rows = rng.choice(B * Hq, size=min(n, B * Hq), replace=False)
+    return sorted(int(r) for r in rows)
+
+
+def test_config1_full():
+    wl = config1()
+    np_in = oracle_inputs(wl)
+    g = run_gpu(wl)
+    orc, tau_o = run_oracle(wl, np_in)
+    stats = compare(wl, g, orc, tau_o, min_compared=1.0, np_inputs=np_in)
+    # every planted block and nothing else
+    for h in range(4):
+        assert np.nonzero(g.mask[0, h].cpu().numpy())[0].tolist() == wl.planted[(0, h)].tolist()
+    say(stats)
+
+
+def test_config2_full():
+    wl = config2()
+    np_in = oracle_inputs(wl)
+    calibrate_bias(wl, np_in)
+    g = run_gpu(wl)
+    orc, tau_o = run_oracle(wl, np_in)
+    say(compare(wl, g, orc, tau_o, np_inputs=np_in))
+
+
+def _full_size(wl, n_rows, seed):
+    wl_dev = wl
+    np_in = oracle_inputs(wl_dev)          # host copies feed the oracle
+    calibrate_bias(wl_dev, np_in)
+    g = run_gpu(wl_dev)
+    rows = _sample_rows(wl.B, wl.Hq, n_rows, seed)
+    orc, tau_o = run_oracle(wl_dev, np_in, rows=rows)
+    return compare(wl_dev, g, orc, tau_o, rows=rows, min_compared=0.9, np_inputs=np_in)
+
+
+def test_config3_sampled_rows():
+    say(_full_size(config3(device="cuda"), 12, 3))
+
+
+@pytest.mark.parametrize("survival", [0.01, 0.05, 0.20, 1.0])
+def test_config4_sampled_rows(survival):
+    say(_full_size(config4(device="cuda", survival=survival), 6, 4))
+
+
+def test_config5_constant_thresholds_sampled_rows():
+    say(_full_size(config5(device="cuda"), 16, 5))
+
+
+def test_config5_predictor_sampled_rows():
+    say(_full_size(config5(device="cuda", predictor=True), 16, 6))
