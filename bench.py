@@ -5,16 +5,20 @@ Workload: one decode step at 512K context -- batch 1, 16 query / 4 KV heads
 (GQA 4), head_dim 128, KV blocks of 128 tokens, bf16 K/V ~N(0,1) with 1% of the
 blocks planted query-aligned, thresholds from the linear predictor with the
 bias placed for a given fraction of surviving blocks per head (synthetic data,
-see the design doc).  A timed step is eta_predict_threshold + eta_decode (screen,
-gated split decode over the surviving blocks, combine, mask); the KV cache and
-its block summaries are resident in HBM before timing starts.  The summary
+see the design doc).  A timed step is one eta_decode_predicted call (threshold
+prediction fused into the screening launch, gated split decode over the
+surviving blocks, combine, mask and counts); the KV cache and its block
+summaries are resident in HBM before timing starts.  The summary
 build (once per prefill) is timed on its own.
 
 One JSON line on stdout:
   value           microseconds per decode step at 20% head survival
   roofline        achieved HBM bandwidth of the split-decode kernel (the
-                  dominant one) on its algorithmic bytes, from HIP events
-                  recorded around each of its launches in the timed region
+                  dominant one) on its algorithmic bytes; its average launch
+                  duration comes from HIP events the library records on the
+                  launch stream around each launch, in a pass of the same K
+                  steps run right after the timed loop (the events are kept
+                  out of the timed loop itself)
   cpu_baseline    the fp64 oracle timed on this host's cores on the same step
   sweep           the same step at 1% / 5% / 20% / 100% survival, with the
                   dense decode baseline at the same shape
@@ -56,6 +60,10 @@ def parse():
                     help="approximate CPU time budget of the oracle baseline")
     ap.add_argument("--only-primary", action="store_true",
                     help="time only the 20%% survival point (profiling runs)")
+    ap.add_argument("--splits", type=int, default=0,
+                    help="splits per (sequence, kv head); 0 = the library's default")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay the step from a captured HIP graph")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run a plain device copy of this size (counter calibration)")
     return ap.parse_args()
@@ -111,18 +119,43 @@ def main():
     nblk = [t // bs for t in wl.seq_lens]
     biases = {s: torch.as_tensor(place_bias(bounds, nblk, qW, s, wl.a), device=dev) for s in SWEEP}
 
-    params = eta.decode_params(beta=wl.beta, z=wl.z, offset_a=wl.a, rescue_window=wl.rescue_window)
+    params = eta.decode_params(beta=wl.beta, z=wl.z, offset_a=wl.a, rescue_window=wl.rescue_window,
+                               num_splits=args.splits)
     desc = eta.kv_desc(k, Hq, bs)
-    ws = eta.alloc_workspace(eta.decode_workspace_size(desc, params), dev)
-    out = torch.empty_like(q)
-    mask = torch.empty(B, Hq, Ncap, dtype=torch.uint8, device=dev)
-    counts = torch.empty(B, Hq, dtype=torch.int32, device=dev)
-    tau = torch.empty(B, Hq, dtype=torch.float32, device=dev)
+    bias_buf = torch.empty(Hq, dtype=torch.float32, device=dev)
+    # one prepared call per step: thresholds predicted inside the screening launch,
+    # then the gated split decode over the surviving blocks and the combine
+    prepared = eta.DecodeStep(q, k, v, sl, summ, W, bias_buf, block_size=bs, params=params)
+    eager = prepared
+    mask = prepared.mask
 
-    def step(bias):
-        eta.predict_threshold(q, W, bias, out=tau)
-        eta.decode(q, k, v, sl, summ, tau, block_size=bs, params=params, out=out, mask=mask,
-                   counts=counts, workspace=ws)
+    def set_point(bias):
+        bias_buf.copy_(bias)
+        torch.cuda.synchronize()
+
+    graph = None
+    if args.graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            prepared_g = eta.DecodeStep(q, k, v, sl, summ, W, bias_buf, block_size=bs,
+                                        params=params, stream=side)
+            for _ in range(3):
+                prepared_g.run()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            prepared_c = eta.DecodeStep(q, k, v, sl, summ, W, bias_buf, block_size=bs,
+                                        params=params)
+            prepared_c.run()
+        prepared, mask = prepared_c, prepared_c.mask
+
+    def step(_bias=None):
+        if graph is not None:
+            graph.replay()
+        else:
+            prepared.run()
 
     def algorithmic(mask_np):
         """Bytes the step must move (mask -> union of the group's heads)."""
@@ -140,33 +173,44 @@ def main():
         d_union = union_blocks / float(B * Hkv * nblk[0])
         return kv, kv + summaries + small, union_blocks, d_head, d_union
 
-    def time_point(bias, steps, warmup, profile):
+    def time_point(bias, steps, warmup):
+        """K timed steps (wall clock between synchronisations, and GPU events)."""
+        set_point(bias)
         for _ in range(warmup):
-            step(bias)
+            step()
         torch.cuda.synchronize()
-        if profile:
-            eta.profile_begin()
         ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
         t0 = time.perf_counter()
         ev0.record()
         for _ in range(steps):
-            step(bias)
+            step()
         ev1.record()
         torch.cuda.synchronize()
         wall_ms = (time.perf_counter() - t0) * 1e3
-        kt = eta.profile_end() if profile else None
-        return wall_ms / steps, ev0.elapsed_time(ev1) / steps, kt
+        return wall_ms / steps, ev0.elapsed_time(ev1) / steps
+
+    def kernel_times(bias, steps):
+        """Per-kernel durations: HIP events recorded by the library around each launch."""
+        set_point(bias)
+        torch.cuda.synchronize()
+        eta.profile_begin()
+        for _ in range(steps):
+            eager.run()
+        torch.cuda.synchronize()
+        return eta.profile_end()
 
     def cold_point(bias, steps):
         """Per-step GPU time with the 256 MB last-level cache flushed before each step."""
-        flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+        set_point(bias)
+        # a read-only sweep over 512 MB (twice the last-level cache): a write-based
+        # flush would leave dirty lines whose write-back overlaps the timed step
+        flush = torch.ones(512 << 18, dtype=torch.int32, device=dev)
         times = []
         for _ in range(steps):
-            flush.fill_(1)
+            flush.sum(dtype=torch.int64)
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record()
-            step(bias)
+            step()
             b.record()
             torch.cuda.synchronize()
             times.append(a.elapsed_time(b))
@@ -174,15 +218,17 @@ def main():
         return float(np.median(times))
 
     def dense_point(steps, warmup):
-        dws = eta.alloc_workspace(eta.dense_workspace_size(desc), dev)
+        dws = eta.alloc_workspace(eta.dense_workspace_size(desc, args.splits), dev)
         dout = torch.empty_like(q)
         for _ in range(warmup):
-            eta.dense_decode(q, k, v, sl, block_size=bs, out=dout, workspace=dws)
+            eta.dense_decode(q, k, v, sl, block_size=bs, num_splits=args.splits, out=dout,
+                             workspace=dws)
         torch.cuda.synchronize()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
         for _ in range(steps):
-            eta.dense_decode(q, k, v, sl, block_size=bs, out=dout, workspace=dws)
+            eta.dense_decode(q, k, v, sl, block_size=bs, num_splits=args.splits, out=dout,
+                             workspace=dws)
         b.record()
         torch.cuda.synchronize()
         return a.elapsed_time(b) / steps
@@ -197,8 +243,9 @@ def main():
         is_primary = abs(s - PRIMARY_SURVIVAL) < 1e-9
         steps = args.steps if is_primary else max(20, args.steps // 4)
         warm = args.warmup if is_primary else 5
-        ms, gpu_ms, kt = time_point(biases[s], steps, warm, profile=is_primary)
+        ms, gpu_ms = time_point(biases[s], steps, warm)
         kv_b, step_b, ub, dh, du = algorithmic(mask.cpu().numpy())
+        kt = kernel_times(biases[s], steps) if is_primary else None
         cold_ms = cold_point(biases[s], 20)
         entry = {"survival_target": s, "us_per_step": round(ms * 1e3, 2),
                  "gpu_us_per_step": round(gpu_ms * 1e3, 2), "cold_us_per_step": round(cold_ms * 1e3, 2),

@@ -90,7 +90,8 @@ typedef struct {
  *   max_norm[(b*num_kv_heads + h)*n_blk_cap + j]              largest key L2 norm
  * The standard deviation (not the variance) is stored, as the paper does
  * (App. "GQA-Grouped Execution and Compact Metadata Layout").
- * n_blk_cap >= capacity_tokens / block_size.
+ * n_blk_cap >= capacity_tokens / block_size, n_blk_cap < 2^24 and
+ * n_blk_cap <= 131072 (2048 screening tiles of 64 blocks).
  */
 typedef struct {
   float* mu;
@@ -181,6 +182,23 @@ eta_status_t eta_decode(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q,
                         const float* tau, const eta_decode_params_t* p, void* out,
                         uint8_t* block_mask, int32_t* head_token_counts, void* workspace,
                         size_t workspace_bytes, void* stream);
+
+/*
+ * eta_decode_predicted -- eta_decode with the threshold predictor of Eq.
+ * (tau_pred) fused into the screening launch: tau = concat(q) W + bias (W ==
+ * NULL: the frozen constants bias), computed with the same summation order as
+ * eta_predict_threshold, so the thresholds are bit-identical to it.  This is
+ * one whole decode step of the paper's layer: predict, screen, attend.
+ *   W, bias   as in eta_predict_threshold (bias required)
+ *   tau_out   fp32 [batch][num_q_heads] receives the thresholds, or NULL
+ * Every other argument, the results and the workspace size are as for eta_decode.
+ */
+eta_status_t eta_decode_predicted(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q,
+                                  const void* k, const void* v, const int32_t* seq_lens,
+                                  const eta_summary_t* summ, const float* W, const float* bias,
+                                  const eta_decode_params_t* p, void* out, uint8_t* block_mask,
+                                  int32_t* head_token_counts, float* tau_out, void* workspace,
+                                  size_t workspace_bytes, void* stream);
 
 /*
  * eta_block_bounds -- the screening bound of Eq. (dual_bound_eq) for every

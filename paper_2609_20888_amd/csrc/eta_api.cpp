@@ -105,9 +105,9 @@ eta_status_t check_summary(const eta_summary_t* s, Geom* g) {
   g->ncap = s->n_blk_cap;
   g->n_tiles = (int)((g->ncap + kScreenTile - 1) / kScreenTile);
   if (g->n_tiles < 1) g->n_tiles = 1;
-  if (g->n_tiles > kMaxTiles)
-    return fail(ETA_ERR_UNSUPPORTED, "n_blk_cap %lld exceeds %d screening tiles",
-                (long long)s->n_blk_cap, kMaxTiles);
+  if (g->n_tiles > kMaxTiles || s->n_blk_cap >= kMaxBlocks)
+    return fail(ETA_ERR_UNSUPPORTED, "n_blk_cap %lld exceeds %d screening tiles of %d blocks",
+                (long long)s->n_blk_cap, kMaxTiles, kScreenTile);
   return ETA_OK;
 }
 
@@ -118,8 +118,8 @@ eta_status_t check_params(const eta_decode_params_t* p) {
   if (!std::isfinite(p->z) || p->z < 0.f) return fail(ETA_ERR_INVALID_ARG, "z must be finite and >= 0");
   if (!std::isfinite(p->offset_a)) return fail(ETA_ERR_INVALID_ARG, "offset_a must be finite");
   if (p->rescue_window_blocks < 0) return fail(ETA_ERR_INVALID_ARG, "rescue_window_blocks < 0");
-  if (p->rescue_window_blocks > kScreenTile)
-    return fail(ETA_ERR_UNSUPPORTED, "rescue_window_blocks > %d unsupported", kScreenTile);
+  if (p->rescue_window_blocks > kMaxRescueWindow)
+    return fail(ETA_ERR_UNSUPPORTED, "rescue_window_blocks > %d unsupported", kMaxRescueWindow);
   if (p->pin_recent_blocks < 0) return fail(ETA_ERR_INVALID_ARG, "pin_recent_blocks < 0");
   if (p->num_splits < 0 || p->num_splits > kMaxSplits)
     return fail(ETA_ERR_INVALID_ARG, "num_splits must be in [0, %d]", kMaxSplits);
@@ -172,9 +172,9 @@ LaunchHook active_hook() {
 }  // namespace
 
 int default_splits(const Geom& g) {
-  // aim at about four workgroups per compute unit over the whole grid
+  // about one resident round of split workgroups (two per compute unit)
   const int64_t groups = (int64_t)g.B * g.Hkv;
-  int64_t S = (1024 + groups - 1) / groups;
+  int64_t S = (512 + groups - 1) / groups;
   if (S > 256) S = 256;
   const int64_t half = g.ncap / 2 > 0 ? g.ncap / 2 : 1;
   if (S > half) S = half;
@@ -190,15 +190,15 @@ size_t decode_ws_bytes(const Geom& g, int S, DecodeWs* c, void* base) {
     off = align256(off + bytes);
     return o;
   };
-  const size_t o_hm = take(nb);
   const size_t o_ids = take(nb * 4);
   const size_t o_tc = take((size_t)g.B * g.Hkv * g.n_tiles * 4);
   const size_t o_hc = take((size_t)g.B * g.Hq * g.n_tiles * 4);
   const size_t o_ml = take((size_t)g.B * g.Hq * S * 8);
   const size_t o_acc = take((size_t)g.B * g.Hq * S * g.D * 4);
+  const size_t o_tau = take((size_t)g.B * g.Hq * 4);
   if (c && base) {
     char* p = static_cast<char*>(base);
-    c->hm = reinterpret_cast<uint8_t*>(p + o_hm);
+    c->tau = reinterpret_cast<float*>(p + o_tau);
     c->ids = reinterpret_cast<int32_t*>(p + o_ids);
     c->tile_cnt = reinterpret_cast<int32_t*>(p + o_tc);
     c->head_cnt = reinterpret_cast<int32_t*>(p + o_hc);
@@ -276,21 +276,24 @@ eta_status_t eta_decode_workspace_size(const eta_kv_desc_t* kv, const eta_decode
   return ok();
 }
 
-eta_status_t eta_decode(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q, const void* k,
-                        const void* v, const int32_t* seq_lens, const eta_summary_t* summ,
-                        const float* tau, const eta_decode_params_t* p, void* out,
-                        uint8_t* block_mask, int32_t* head_token_counts, void* workspace,
-                        size_t workspace_bytes, void* stream) {
+static eta_status_t decode_impl(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q,
+                                const void* k, const void* v, const int32_t* seq_lens,
+                                const eta_summary_t* summ, const float* tau, const float* W,
+                                const float* bias, float* tau_out,
+                                const eta_decode_params_t* p, void* out, uint8_t* block_mask,
+                                int32_t* head_token_counts, void* workspace,
+                                size_t workspace_bytes, void* stream) {
   Geom g;
   eta_status_t st = check_kv(kv, &g);
   if (st) return st;
   if ((st = check_params(p))) return st;
   if (!valid_dtype(q_dtype)) return fail(ETA_ERR_INVALID_ARG, "q_dtype %d is not an eta_dtype_t", q_dtype);
-  if (!q || !k || !v || !seq_lens || !tau || !out || !block_mask)
-    return fail(ETA_ERR_INVALID_ARG, "q, k, v, seq_lens, tau, out and block_mask must be non-NULL");
-  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(seq_lens) || !aligned16(tau) ||
+  if (!q || !k || !v || !seq_lens || !out || !block_mask)
+    return fail(ETA_ERR_INVALID_ARG, "q, k, v, seq_lens, out and block_mask must be non-NULL");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(seq_lens) ||
       !aligned16(out) || !aligned16(block_mask) ||
-      (head_token_counts && !aligned16(head_token_counts)))
+      (head_token_counts && !aligned16(head_token_counts)) || (tau && !aligned16(tau)) ||
+      (W && !aligned16(W)) || (bias && !aligned16(bias)) || (tau_out && !aligned16(tau_out)))
     return fail(ETA_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
   // the mask and the workspace are laid out with the summary capacity
   if ((st = check_summary(summ, &g))) return st;
@@ -304,10 +307,32 @@ eta_status_t eta_decode(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q,
     return fail(ETA_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
   DecodeCfg c{p->beta, p->z, p->offset_a, p->rescue_window_blocks, p->pin_recent_blocks,
               p->self_ungated ? 1 : 0, p->screen_all ? 1 : 0, S};
-  hipError_t e = launch_decode(g, c, q_dtype, q, k, v, seq_lens, *summ, tau, out, block_mask,
-                               head_token_counts, ws, (hipStream_t)stream, active_hook());
+  hipError_t e = launch_decode(g, c, q_dtype, q, k, v, seq_lens, *summ, tau, W, bias, tau_out,
+                               out, block_mask, head_token_counts, ws, (hipStream_t)stream,
+                               active_hook());
   if (e != hipSuccess) return fail(ETA_ERR_HIP, "decode launch failed: %s", hipGetErrorString(e));
   return ok();
+}
+
+eta_status_t eta_decode(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q, const void* k,
+                        const void* v, const int32_t* seq_lens, const eta_summary_t* summ,
+                        const float* tau, const eta_decode_params_t* p, void* out,
+                        uint8_t* block_mask, int32_t* head_token_counts, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  if (!tau) return fail(ETA_ERR_INVALID_ARG, "tau must be non-NULL");
+  return decode_impl(kv, q_dtype, q, k, v, seq_lens, summ, tau, nullptr, nullptr, nullptr, p, out,
+                     block_mask, head_token_counts, workspace, workspace_bytes, stream);
+}
+
+eta_status_t eta_decode_predicted(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q,
+                                  const void* k, const void* v, const int32_t* seq_lens,
+                                  const eta_summary_t* summ, const float* W, const float* bias,
+                                  const eta_decode_params_t* p, void* out, uint8_t* block_mask,
+                                  int32_t* head_token_counts, float* tau_out, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  if (!bias) return fail(ETA_ERR_INVALID_ARG, "bias must be non-NULL");
+  return decode_impl(kv, q_dtype, q, k, v, seq_lens, summ, nullptr, W, bias, tau_out, p, out,
+                     block_mask, head_token_counts, workspace, workspace_bytes, stream);
 }
 
 eta_status_t eta_block_bounds(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q,

@@ -9,13 +9,16 @@
 
 namespace eta {
 
-// Blocks screened by one workgroup (one lane per block).  The top-1 rescue
-// window must fit in the first screening tile, so rescue_window_blocks <= kScreenTile.
-constexpr int kScreenTile = 256;
+// Blocks screened by one workgroup (one lane per block), and the largest top-1
+// rescue window (rescue_window_blocks <= kMaxRescueWindow).
+constexpr int kScreenTile = 64;
+constexpr int kMaxRescueWindow = 256;
 constexpr int kMaxSplits = 1024;
 // Upper bound on screening tiles per (sequence, kv head): the split-decode
 // kernel keeps their prefix sum in LDS.
 constexpr int kMaxTiles = 2048;
+// Union ids pack the block index below bit 24 and the head bits above it.
+constexpr int64_t kMaxBlocks = int64_t(1) << 24;
 
 struct Geom {
   int B, Hq, Hkv, D, BS, G;
@@ -28,12 +31,14 @@ struct Geom {
 
 // Workspace carve-up of eta_decode.
 struct DecodeWs {
-  uint8_t* hm;               // [B][Hkv][ncap]   per-block bitmask of the G heads that selected it
-  int32_t* ids;              // [B][Hkv][ncap]   union block ids, compacted per screening tile
+  int32_t* ids;              // [B][Hkv][ncap]   union block ids | head bits << 24, compacted
+                             //                  per screening tile (tile t's ids start at
+                             //                  t * kScreenTile)
   int32_t* tile_cnt;         // [B][Hkv][n_tiles] union blocks per tile
   int32_t* head_cnt;         // [B][Hq][n_tiles]  selected blocks per head per tile
   float2* part_ml;           // [B][Hq][S]        (running max, running sum) per split
   float* part_acc;           // [B][Hq][S][D]     unnormalised output per split
+  float* tau;                // [B][Hq]           thresholds predicted by the screening kernel
 };
 
 size_t decode_ws_bytes(const Geom& g, int S, DecodeWs* carve, void* base);
@@ -56,9 +61,12 @@ hipError_t launch_summaries(const Geom& g, const void* k, const int32_t* seq_len
 hipError_t launch_predict(int B, int Hq, int D, int q_dtype, const void* q, const float* W,
                           const float* bias, float* tau, hipStream_t stream, LaunchHook hook);
 
+// tau == nullptr: the screening kernel predicts the thresholds from (W, bias)
+// and, if tau_out is given, stores them there too.
 hipError_t launch_decode(const Geom& g, const DecodeCfg& c, int q_dtype, const void* q,
                          const void* k, const void* v, const int32_t* seq_lens,
-                         const eta_summary_t& s, const float* tau, void* out, uint8_t* mask,
+                         const eta_summary_t& s, const float* tau, const float* W,
+                         const float* bias, float* tau_out, void* out, uint8_t* mask,
                          int32_t* counts, const DecodeWs& ws, hipStream_t stream, LaunchHook hook);
 
 hipError_t launch_bounds(const Geom& g, int q_dtype, const void* q, const int32_t* seq_lens,

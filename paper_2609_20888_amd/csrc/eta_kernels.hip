@@ -23,6 +23,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "eta_internal.h"
 
 namespace eta {
@@ -211,205 +213,330 @@ __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ 
 
 // ---------------------------------------------------------------- predictor
 //
-// One workgroup per sequence.  Thread t accumulates column h = t % Hq over the
-// rows j = t / Hq, t / Hq + 256 / Hq, ... of W (coalesced over h); the partial
-// sums of each column are then added in a fixed order.
+// tau[b][h] = sum_j qbar[b][j] W[j][h] + bias[h] with one fixed summation
+// order shared by the stand-alone predictor and the screening kernel's fused
+// prediction, so both give bit-identical thresholds: thread t of a 256-thread
+// workgroup accumulates rows j = t, t + 256, ... (independent loads, all in
+// flight); each wavefront reduces by butterfly; the four wavefront sums are
+// added in order; the bias is added last.
 
-__global__ __launch_bounds__(256) void predict_kernel(const void* __restrict__ q, int q_dtype,
-                                                      const float* __restrict__ W,
-                                                      const float* __restrict__ bias,
-                                                      float* __restrict__ tau, int Hq, int D) {
-  __shared__ float red[256];
-  const int b = blockIdx.x, tid = threadIdx.x;
-  const int64_t J = (int64_t)Hq * D;
-  const int rps = 256 / Hq;         // rows per step
-  const int h = tid % Hq, r0 = tid / Hq;
-  float acc = 0.f;
-  if (W != nullptr && r0 < rps) {
-    for (int64_t j = r0; j < J; j += rps)
-      acc = fmaf(load_q(q, q_dtype, (int64_t)b * J + j), W[j * Hq + h], acc);
+constexpr int kPredThreads = 256;
+constexpr int kPredCols = 4;     // columns per stand-alone predictor workgroup
+
+// Per-thread partial sums of columns h0 .. h0 + ncols - 1 (ncols <= NC).
+template <int NC, typename QT>
+__device__ __forceinline__ void pred_loop(const QT* __restrict__ q, const float* __restrict__ W,
+                                          int Hq, int64_t J, int h0, int ncols, float (&acc)[NC]) {
+#pragma unroll 8
+  for (int64_t j = threadIdx.x; j < J; j += kPredThreads) {
+    float x;
+    if constexpr (sizeof(QT) == 4)
+      x = q[j];
+    else
+      x = bf16lo(q[j]);
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+      if (c < ncols) acc[c] = fmaf(x, W[j * Hq + h0 + c], acc[c]);
   }
-  red[tid] = (r0 < rps) ? acc : 0.f;
+}
+
+template <int NC>
+__device__ __forceinline__ void pred_partials(const void* __restrict__ q, int q_dtype, int64_t qoff,
+                                              const float* __restrict__ W, int Hq, int64_t J,
+                                              int h0, int ncols, float (&acc)[NC]) {
+#pragma unroll
+  for (int c = 0; c < NC; ++c) acc[c] = 0.f;
+  if (q_dtype == ETA_DT_F32)
+    pred_loop<NC>(reinterpret_cast<const float*>(q) + qoff, W, Hq, J, h0, ncols, acc);
+  else
+    pred_loop<NC>(reinterpret_cast<const uint16_t*>(q) + qoff, W, Hq, J, h0, ncols, acc);
+}
+
+// Reduces the partials of the workgroup (kPredThreads threads); red holds
+// [4][NC] floats.  Thread c < ncols gets column c's total in *tot (bias not added).
+template <int NC>
+__device__ __forceinline__ void pred_reduce(const float (&acc)[NC], int ncols, float* red,
+                                            float* tot) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const float x = wave_sum(acc[c]);
+    if (lane == 0) red[w * NC + c] = x;
+  }
   __syncthreads();
-  if (tid < Hq) {
-    float s = 0.f;
-    for (int r = 0; r < rps; ++r) s += red[r * Hq + tid];
-    tau[(int64_t)b * Hq + tid] = s + bias[tid];
+  if ((int)threadIdx.x < ncols) {
+    float t = 0.f;
+#pragma unroll
+    for (int k = 0; k < kPredThreads / 64; ++k) t += red[k * NC + threadIdx.x];
+    *tot = t;
   }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(kPredThreads) void predict_kernel(const void* __restrict__ q,
+                                                               int q_dtype,
+                                                               const float* __restrict__ W,
+                                                               const float* __restrict__ bias,
+                                                               float* __restrict__ tau, int Hq,
+                                                               int D) {
+  __shared__ float red[4 * kPredCols];
+  const int b = blockIdx.x, h0 = blockIdx.y * kPredCols;
+  const int ncols = Hq - h0 < kPredCols ? Hq - h0 : kPredCols;
+  const int64_t J = (int64_t)Hq * D;
+  float acc[kPredCols];
+  if (W != nullptr) {
+    pred_partials<kPredCols>(q, q_dtype, (int64_t)b * J, W, Hq, J, h0, ncols, acc);
+  } else {
+#pragma unroll
+    for (int c = 0; c < kPredCols; ++c) acc[c] = 0.f;
+  }
+  float t = 0.f;
+  pred_reduce<kPredCols>(acc, ncols, red, &t);
+  if ((int)threadIdx.x < ncols) tau[(int64_t)b * Hq + h0 + threadIdx.x] = t + bias[h0 + threadIdx.x];
 }
 
 // ---------------------------------------------------------------- screening
 //
-// One workgroup per (screening tile of 256 blocks, kv head, sequence); lane =
-// block.  With the dimension-major summaries, coordinate i of the 64 blocks of
-// a wavefront is one coalesced 256-byte load; the G query heads of the group
-// are evaluated from the same loads (q broadcast from LDS), so no cross-lane
-// reduction is needed for the bound.
+// One workgroup of 256 threads per (tile of 64 blocks, kv head, sequence).
+// Lane l of wavefront w owns block 64 * tile + l and head-dimension quarter w:
+// with the dimension-major summaries, coordinate i of the tile's 64 blocks is
+// one coalesced 256-byte load, and each lane keeps its quarter's loads in
+// flight together.  These loads are issued first, before the query, length and
+// threshold loads they do not depend on.  The G query heads of the group are
+// evaluated from the same loads (q broadcast from LDS).  Wavefront 0 adds the
+// four quarter partials in a fixed order and owns everything per block after
+// that: selection, rescue, mask, and the ordered compaction of the tile's
+// union ids (one ballot).  A union id carries the block's head bits in its top
+// byte.
+//
+// Top-1 rescue needs the selection state of the whole window [0, min(c, N)),
+// which can span up to four tiles.  Every workgroup whose tile intersects the
+// window evaluates the window's bounds itself, with the same arithmetic as the
+// owning tiles (so the decisions agree bit for bit), and sets the rescued
+// block's bit only if that block is its own.
+//
+// With a predictor (W, bias), every workgroup computes the thresholds of its
+// G heads itself, with the stand-alone predictor's summation order (so they
+// are bit-identical to eta_predict_threshold's); tile 0 stores them.
 
 struct ScreenArgs {
   const void* q;
   const int32_t* seq_lens;
-  const float* tau;
+  const float* tau;          // given thresholds, or nullptr with `predict`
+  const float* W;            // predictor weights (may be nullptr: constants)
+  const float* bias;
+  float* tau_store;          // predicted thresholds for the decode kernel (tile 0 writes)
+  float* tau_out;            // optional copy for the caller
   const float* mu;
   const float* sigma;
   const float* mx;
   uint8_t* mask;
-  uint8_t* hm;
   int32_t* ids;
   int32_t* tile_cnt;
   int32_t* head_cnt;
   float* bounds;
   Geom g;
   int q_dtype;
+  int predict;
   float z, offset_a;
   int c, lwb, screen_all;
 };
 
-// First index attaining the largest value among valid lanes of the workgroup;
-// -1 if no lane is valid.  Every thread of the workgroup must call it.
-__device__ int block_argmax_first(float v, bool valid, int idx, float* rv, int* ri) {
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  float bv = valid ? v : kNegInf;
-  int bi = valid ? idx : 0x7fffffff;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float ov = __shfl_xor(bv, o, 64);
-    const int oi = __shfl_xor(bi, o, 64);
-    if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
-  }
-  if (lane == 0) { rv[w] = bv; ri[w] = bi; }
-  __syncthreads();
-  if (tid == 0) {
-    float b2 = rv[0];
-    int i2 = ri[0];
-    for (int k = 1; k < 4; ++k)
-      if (rv[k] > b2 || (rv[k] == b2 && ri[k] < i2)) { b2 = rv[k]; i2 = ri[k]; }
-    ri[4] = (i2 == 0x7fffffff) ? -1 : i2;
-  }
-  __syncthreads();
-  const int r = ri[4];
-  __syncthreads();
-  return r;
-}
+constexpr int kScreenThreads = 256;
+constexpr uint32_t kIdMask = 0x00ffffffu;   // union id: block index | head bits << 24
 
 template <int D, int G, bool BOUNDS_ONLY>
-__global__ __launch_bounds__(256) void screen_kernel(ScreenArgs a) {
+__global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
+  constexpr int DQ = D / 4;            // dimensions per quarter
   const Geom& g = a.g;
   const int tile = blockIdx.x, gh = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
   __shared__ float q_s[D][G];
   __shared__ float q2_s[D][G];
   __shared__ float qn_s[G];
   __shared__ float teff_s[G];
-  __shared__ float rv[4];
-  __shared__ int ri[5];
-  __shared__ int wtot[4];
+  __shared__ float part_s[3][2 * G][kScreenTile];
+  __shared__ float pred_red[4 * G];
 
   const int64_t hq0 = (int64_t)b * g.Hq + (int64_t)gh * G;   // first query head row of the group
-  for (int idx = tid; idx < G * D; idx += 256) {
-    const int h = idx / D, i = idx % D;
-    const float x = load_q(a.q, a.q_dtype, (hq0 + h) * D + i);
-    q_s[i][h] = x;
-    q2_s[i][h] = x * x;
+  const int64_t bg = (int64_t)b * g.Hkv + gh;
+  const float scale = 1.0f / sqrtf((float)D);
+  const float z = a.z;
+
+  // this lane's summary loads for blocks jb + lane (indexes clamped into the
+  // buffers; values of blocks that are not full are discarded later)
+  auto issue = [&](int64_t jb, float (&m)[DQ], float (&sd)[DQ], float& M) {
+    int64_t jc = jb + lane;
+    jc = jc < g.ncap ? jc : g.ncap - 1;
+    const float* mup = a.mu + (bg * D + w * DQ) * g.ncap + jc;
+    const float* sgp = a.sigma + (bg * D + w * DQ) * g.ncap + jc;
+#pragma unroll
+    for (int i = 0; i < DQ; ++i) {
+      m[i] = mup[(int64_t)i * g.ncap];
+      sd[i] = sgp[(int64_t)i * g.ncap];
+    }
+    M = a.mx[bg * g.ncap + jc];
+  };
+  float m0[DQ], sd0[DQ], M0;
+  issue((int64_t)tile * kScreenTile, m0, sd0, M0);
+
+  // the group's queries, their norms (one wavefront per head), thresholds
+  for (int h = w; h < G; h += 4) {
+    float ss = 0.f;
+    for (int i = lane; i < D; i += 64) {
+      const float x = load_q(a.q, a.q_dtype, (hq0 + h) * D + i);
+      q_s[i][h] = x;
+      q2_s[i][h] = x * x;
+      ss = fmaf(x, x, ss);
+    }
+    ss = wave_sum(ss);
+    if (lane == 0) qn_s[h] = sqrtf(ss);
   }
-  __syncthreads();
-  if (tid < G) {
-    float s = 0.f;
-    for (int i = 0; i < D; ++i) s = fmaf(q_s[i][tid], q_s[i][tid], s);
-    qn_s[tid] = sqrtf(s);
-    if (!BOUNDS_ONLY) teff_s[tid] = a.tau[hq0 + tid] - a.offset_a;
+  if constexpr (!BOUNDS_ONLY) {
+    if (a.predict) {
+      float acc[G];
+      const int64_t J = (int64_t)g.Hq * D;
+      if (a.W != nullptr) {
+        pred_partials<G>(a.q, a.q_dtype, (int64_t)b * J, a.W, g.Hq, J, gh * G, G, acc);
+      } else {
+#pragma unroll
+        for (int h = 0; h < G; ++h) acc[h] = 0.f;
+      }
+      float t = 0.f;
+      pred_reduce<G>(acc, G, pred_red, &t);
+      if (tid < G) {
+        const float tau = t + a.bias[gh * G + tid];
+        teff_s[tid] = tau - a.offset_a;
+        if (tile == 0) {
+          a.tau_store[hq0 + tid] = tau;
+          if (a.tau_out != nullptr) a.tau_out[hq0 + tid] = tau;
+        }
+      }
+    } else if (tid < G) {
+      teff_s[tid] = a.tau[hq0 + tid] - a.offset_a;
+    }
   }
   __syncthreads();
 
   const int64_t T = clamp_len(a.seq_lens, b, g.cap);
   const int64_t N = T / g.BS;
-  const int64_t j = (int64_t)tile * kScreenTile + tid;
-  const int64_t bg = (int64_t)b * g.Hkv + gh;
-  const float scale = 1.0f / sqrtf((float)D);
 
-  float bnd[G];
-  if (j < N) {
+  // Bounds of blocks jb + lane from loads issued by `issue` (all four
+  // wavefronts take part); valid in wavefront 0, NaN for blocks not full.
+  auto finish = [&](int64_t jb, const float (&m)[DQ], const float (&sd)[DQ], float M,
+                    float (&bnd)[G]) {
+    const int64_t j = jb + lane;
     float dot[G], var[G];
 #pragma unroll
     for (int h = 0; h < G; ++h) { dot[h] = 0.f; var[h] = 0.f; }
-    const float* mup = a.mu + bg * D * g.ncap + j;
-    const float* sgp = a.sigma + bg * D * g.ncap + j;
-#pragma unroll 8
-    for (int i = 0; i < D; ++i) {
-      const float m = mup[(int64_t)i * g.ncap];
-      const float s = sgp[(int64_t)i * g.ncap];
-      const float s2 = s * s;
+#pragma unroll
+    for (int i = 0; i < DQ; ++i) {
+      const float s2 = sd[i] * sd[i];
 #pragma unroll
       for (int h = 0; h < G; ++h) {
-        dot[h] = fmaf(q_s[i][h], m, dot[h]);
-        var[h] = fmaf(q2_s[i][h], s2, var[h]);
+        dot[h] = fmaf(q_s[w * DQ + i][h], m[i], dot[h]);
+        var[h] = fmaf(q2_s[w * DQ + i][h], s2, var[h]);
       }
     }
-    const float M = a.mx[bg * g.ncap + j];
+    if (w > 0) {
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float gauss = dot[h] + a.z * sqrtf(var[h]);
-      const float spher = qn_s[h] * M;
-      float lo = gauss < spher ? gauss : spher;
-      if (isnan(gauss) || isnan(spher)) lo = __builtin_nanf("");
-      bnd[h] = lo * scale;
+      for (int h = 0; h < G; ++h) {
+        part_s[w - 1][h][lane] = dot[h];
+        part_s[w - 1][G + h][lane] = var[h];
+      }
     }
-  } else {
+    __syncthreads();
 #pragma unroll
     for (int h = 0; h < G; ++h) bnd[h] = __builtin_nanf("");
-  }
+    if (w == 0 && j < N) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float dt = ((dot[h] + part_s[0][h][lane]) + part_s[1][h][lane]) + part_s[2][h][lane];
+        const float vr =
+            ((var[h] + part_s[0][G + h][lane]) + part_s[1][G + h][lane]) + part_s[2][G + h][lane];
+        const float gauss = fmaf(z, sqrtf(vr), dt);
+        const float spher = qn_s[h] * M;
+        float lo = gauss < spher ? gauss : spher;
+        if (isnan(gauss) || isnan(spher)) lo = __builtin_nanf("");
+        bnd[h] = lo * scale;
+      }
+    }
+    __syncthreads();
+  };
+
+  const int64_t j = (int64_t)tile * kScreenTile + lane;
+  float bnd[G];
+  finish((int64_t)tile * kScreenTile, m0, sd0, M0, bnd);
 
   if constexpr (BOUNDS_ONLY) {
-    if (j < g.ncap) {
+    if (w == 0 && j < g.ncap) {
 #pragma unroll
       for (int h = 0; h < G; ++h) a.bounds[(hq0 + h) * g.ncap + j] = bnd[h];
     }
     return;
   } else {
+    auto selected = [&](int64_t jj, float bd, int h) {
+      return jj < N && (a.screen_all || bd >= teff_s[h] || jj >= N - a.lwb);
+    };
     uint32_t bits = 0;
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const bool s = (j < N) && (a.screen_all || bnd[h] >= teff_s[h] || j >= N - a.lwb);
-      bits |= (uint32_t)s << h;
-    }
-    // top-1 rescue: the window [0, min(c, N)) lies inside tile 0
-    if (tile == 0 && a.c > 0) {
-      const int64_t Wn = (int64_t)a.c < N ? (int64_t)a.c : N;
-      if (Wn >= 1) {
-        const bool inw = j < Wn;
+    for (int h = 0; h < G; ++h) bits |= (uint32_t)selected(j, bnd[h], h) << h;
+
+    // top-1 rescue over the window [0, min(c, N))
+    const int64_t Wn = (int64_t)a.c < N ? (int64_t)a.c : N;
+    if (a.c > 0 && (int64_t)tile * kScreenTile < Wn) {
+      bool any[G];
+      float best[G];
+      int64_t arg[G];
+#pragma unroll
+      for (int h = 0; h < G; ++h) { any[h] = false; best[h] = kNegInf; arg[h] = -1; }
+      for (int64_t jb = 0; jb < Wn; jb += kScreenTile) {
+        float wb[G];
+        if (jb == (int64_t)tile * kScreenTile) {
+#pragma unroll
+          for (int h = 0; h < G; ++h) wb[h] = bnd[h];
+        } else {
+          float m1[DQ], sd1[DQ], M1;
+          issue(jb, m1, sd1, M1);
+          finish(jb, m1, sd1, M1, wb);
+        }
+        const int64_t jj = jb + lane;
+        const bool inw = jj < Wn;
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-          const int any = __syncthreads_or(inw && ((bits >> h) & 1u));
-          if (!any) {
-            const int js = block_argmax_first(bnd[h], inw && !isnan(bnd[h]), (int)j, rv, ri);
-            if (js >= 0 && j == js) bits |= 1u << h;
+          any[h] = any[h] || (__ballot(inw && selected(jj, wb[h], h)) != 0ull);
+          // first index of the chunk's largest non-NaN bound
+          const bool ok = inw && !isnan(wb[h]);
+          float bv = ok ? wb[h] : kNegInf;
+          int bi = ok ? (int)jj : 0x7fffffff;
+#pragma unroll
+          for (int o = 32; o > 0; o >>= 1) {
+            const float ov = __shfl_xor(bv, o, 64);
+            const int oi = __shfl_xor(bi, o, 64);
+            if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
           }
+          if (bi != 0x7fffffff && (arg[h] < 0 || bv > best[h])) { best[h] = bv; arg[h] = bi; }
         }
       }
+#pragma unroll
+      for (int h = 0; h < G; ++h)
+        if (!any[h] && arg[h] == j) bits |= 1u << h;
     }
+    if (w != 0) return;
     if (j < g.ncap) {
 #pragma unroll
       for (int h = 0; h < G; ++h) a.mask[(hq0 + h) * g.ncap + j] = (uint8_t)((bits >> h) & 1u);
-      a.hm[bg * g.ncap + j] = (uint8_t)bits;
     }
-    // compaction of the union ids of this tile (ordered prefix sum)
-    const int lane = tid & 63, w = tid >> 6;
-    const bool u = bits != 0;
-    const unsigned long long bal = __ballot(u);
-    const int lp = __popcll(bal & ((1ull << lane) - 1ull));
-    if (lane == 0) wtot[w] = __popcll(bal);
-    __syncthreads();
-    int off = 0, total = 0;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      off += (k < w) ? wtot[k] : 0;
-      total += wtot[k];
-    }
-    if (u) a.ids[bg * g.ncap + (int64_t)tile * kScreenTile + off + lp] = (int32_t)j;
-    if (tid == 0) a.tile_cnt[bg * g.n_tiles + tile] = total;
+    // ordered compaction of the tile's union ids and the per-head counts
+    const unsigned long long bal = __ballot(bits != 0);
+    if (bits != 0)
+      a.ids[bg * g.ncap + (int64_t)tile * kScreenTile + __popcll(bal & ((1ull << lane) - 1ull))] =
+          (int32_t)((uint32_t)j | (bits << 24));
+    if (lane == 0) a.tile_cnt[bg * g.n_tiles + tile] = __popcll(bal);
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      const int cnt = __syncthreads_count((bits >> h) & 1u);
-      if (tid == 0) a.head_cnt[(hq0 + h) * g.n_tiles + tile] = cnt;
+      const unsigned long long bh = __ballot((bits >> h) & 1u);
+      if (lane == 0) a.head_cnt[(hq0 + h) * g.n_tiles + tile] = __popcll(bh);
     }
   }
 }
@@ -443,7 +570,6 @@ struct SplitArgs {
   const void* v;
   const int32_t* seq_lens;
   const float* tau;
-  const uint8_t* hm;
   const int32_t* ids;
   const int32_t* tile_cnt;
   float2* part_ml;
@@ -616,6 +742,130 @@ __device__ __forceinline__ void attend_bf16(const uint16_t* __restrict__ kb,
   }
 }
 
+// bf16 K/V, full 64-token tiles of one wavefront, software-pipelined: the next
+// tile's K loads are issued as soon as this tile's MFMAs have consumed the K
+// registers, and its V loads as soon as p.V has consumed the V registers, so
+// each wavefront keeps about one tile of K and V in flight while it computes.
+// tile_base(u) gives the first token of tile u, tile_bits(u) its head mask.
+template <int D, int G, bool DENSE, typename TB, typename BITS>
+__device__ __forceinline__ void attend_bf16_stream(const uint16_t* __restrict__ kb,
+                                                   const uint16_t* __restrict__ vb, int64_t st,
+                                                   int ntiles, TB tile_base, BITS tile_bits,
+                                                   const bf16x8* qa_s, bool use_lo,
+                                                   const float* teff_s, float* p_s, float beta,
+                                                   float scale, int64_t self_t, int lane,
+                                                   float (&m_)[G], float (&l_)[G],
+                                                   float (&acc)[G][D / 64]) {
+  constexpr int DPL = D / 64;
+  constexpr int DC = D / 8;
+  constexpr int NQ = G > 4 ? G / 4 : 1;
+  constexpr int GQ = 4 * NQ;
+  if (ntiles <= 0) return;
+  const bool diag = ((lane & 15) >> 2) == (lane >> 4);
+  const int qrow = lane & 3;
+  uint4 kr[DC];
+  uint32_t vr[64];
+  auto load_k = [&](int64_t tb) {
+    const uint16_t* krow = kb + (tb + lane) * st;
+#pragma unroll
+    for (int c = 0; c < DC; ++c) kr[c] = *reinterpret_cast<const uint4*>(krow + 8 * c);
+  };
+  auto load_v = [&](int64_t tb) {
+#pragma unroll
+    for (int t = 0; t < 64; ++t) {
+      if constexpr (DPL == 2)
+        vr[t] = *reinterpret_cast<const uint32_t*>(vb + (tb + t) * st + 2 * lane);
+      else
+        vr[t] = vb[(tb + t) * st + lane];
+    }
+  };
+  // One tile: scores on the MFMAs, then (MORE) the next tile's K loads into the
+  // freed K registers, the softmax update, p.V, then (MORE) the next tile's V
+  // loads.  The last tile is peeled (MORE = false) so that the loads inside the
+  // loop are unconditional: a conditional reload would keep two copies of the
+  // K/V registers alive across the branch.
+  auto tile = [&](int u, int64_t tb, int64_t tbn, auto more_tag) {
+    constexpr bool MORE = decltype(more_tag)::value;
+    asm volatile("" ::: "memory");
+    const uint32_t bits = tile_bits(u);
+    const bool ung = (tb + lane) == self_t;
+    f32x4 c[NQ];
+#pragma unroll
+    for (int hq = 0; hq < NQ; ++hq) {
+      c[hq] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const bf16x8 zero = {};
+#pragma unroll
+      for (int ch = 0; ch < DC; ++ch) {
+        const bf16x8 bk = __builtin_bit_cast(bf16x8, kr[ch]);
+        const bf16x8 ahi = diag ? qa_s[((hq * 2 + 0) * 4 + qrow) * DC + ch] : zero;
+        c[hq] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, bk, c[hq], 0, 0, 0);
+        if (use_lo) {
+          const bf16x8 alo = diag ? qa_s[((hq * 2 + 1) * 4 + qrow) * DC + ch] : zero;
+          c[hq] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, bk, c[hq], 0, 0, 0);
+        }
+      }
+    }
+    if constexpr (MORE) {
+      __builtin_amdgcn_sched_barrier(0);
+      load_k(tbn);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int hq = 0; hq < NQ; ++hq) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int h = 4 * hq + r;
+        if (h < G) {
+          const float sc = gated<DENSE>(c[hq][r] * scale, (bits >> h) & 1u, ung, teff_s[h], beta);
+          p_s[lane * GQ + h] = softmax_step<DPL>(sc, m_[h], l_[h], acc[h]);
+        }
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int t = 0; t < 64; ++t) {
+      float vv[DPL];
+      if constexpr (DPL == 2) {
+        vv[0] = bf16lo(vr[t]);
+        vv[1] = bf16hi(vr[t]);
+      } else {
+        vv[0] = bf16lo(vr[t]);
+      }
+#pragma unroll
+      for (int hq = 0; hq < NQ; ++hq) {
+        const float4 p4 = *reinterpret_cast<const float4*>(p_s + t * GQ + 4 * hq);
+        const float pr[4] = {p4.x, p4.y, p4.z, p4.w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int h = 4 * hq + r;
+          if (h < G) {
+#pragma unroll
+            for (int e = 0; e < DPL; ++e) acc[h][e] = fmaf(pr[r], vv[e], acc[h][e]);
+          }
+        }
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    if constexpr (MORE) {
+      __builtin_amdgcn_sched_barrier(0);
+      load_v(tbn);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  int64_t tb = tile_base(0);
+  load_k(tb);
+  load_v(tb);
+  for (int u = 0; u + 1 < ntiles; ++u) {
+    const int64_t tbn = tile_base(u + 1);
+    tile(u, tb, tbn, std::integral_constant<bool, true>{});
+    tb = tbn;
+  }
+  tile(ntiles - 1, tb, tb, std::integral_constant<bool, false>{});
+}
+
+constexpr int kItemChunk = 256;
+
 template <int D, int BS, int G, typename KVT, bool DENSE>
 __global__ __launch_bounds__(256) void split_kernel(SplitArgs a) {
   constexpr int DPL = D / 64;
@@ -635,6 +885,8 @@ __global__ __launch_bounds__(256) void split_kernel(SplitArgs a) {
   __shared__ float mrg_ml[4][G][2];
   __shared__ float mrg_acc[4][G][D];
   __shared__ __attribute__((aligned(16))) float p_s[4][64 * GQ];
+  __shared__ int32_t item_j[kItemChunk];
+  __shared__ uint8_t item_bits[kItemChunk];
 
   const int64_t T = clamp_len(a.seq_lens, b, g.cap);
   const int64_t N = T / BS;
@@ -721,22 +973,45 @@ __global__ __launch_bounds__(256) void split_kernel(SplitArgs a) {
                               m_, l_, acc);
   };
   constexpr uint32_t all_bits = (1u << G) - 1u;
-  for (int64_t it = lo + w; it < hi; it += 4) {
-    int64_t j;
-    uint32_t bits;
-    if constexpr (DENSE) {
-      j = it;
-      bits = all_bits;
-    } else {
-      int tl = 0, th = g.n_tiles;       // pref_s[tl] <= it < pref_s[th]
-      while (th - tl > 1) {
-        const int mid = (tl + th) >> 1;
-        if (pref_s[mid] <= it) tl = mid; else th = mid;
+  // The split's items are resolved (union slot -> block id -> head bits) 256 at
+  // a time by all threads at once and kept in LDS, so a wavefront's K/V loads
+  // never wait on those lookups.
+  for (int64_t base = lo; base < hi; base += kItemChunk) {
+    const int n = (int)(hi - base < kItemChunk ? hi - base : kItemChunk);
+    if (tid < n) {
+      const int64_t it = base + tid;
+      int64_t j;
+      uint32_t bits;
+      if constexpr (DENSE) {
+        j = it;
+        bits = all_bits;
+      } else {
+        int tl = 0, th = g.n_tiles;       // pref_s[tl] <= it < pref_s[th]
+        while (th - tl > 1) {
+          const int mid = (tl + th) >> 1;
+          if (pref_s[mid] <= it) tl = mid; else th = mid;
+        }
+        const uint32_t id = (uint32_t)a.ids[bg * g.ncap + (int64_t)tl * kScreenTile + (it - pref_s[tl])];
+        j = id & kIdMask;
+        bits = id >> 24;
       }
-      j = a.ids[bg * g.ncap + (int64_t)tl * kScreenTile + (it - pref_s[tl])];
-      bits = a.hm[bg * g.ncap + j];
+      item_j[tid] = (int32_t)j;
+      item_bits[tid] = (uint8_t)bits;
     }
-    attend(j * BS, BS, bits);
+    __syncthreads();
+    if constexpr (BF) {
+      // this wavefront's items are k = w, w + 4, ...; each is BS / 64 tiles of 64 tokens
+      constexpr int SPB = BS / 64;
+      const int nmine = n > w ? (n - w + 3) / 4 : 0;
+      attend_bf16_stream<D, G, DENSE>(
+          kb, vb, g.st, nmine * SPB,
+          [&](int u) { return (int64_t)item_j[w + 4 * (u / SPB)] * BS + 64 * (u % SPB); },
+          [&](int u) { return (uint32_t)item_bits[w + 4 * (u / SPB)]; }, qa_s, use_lo, teff_s,
+          p_s[w], a.beta, scale, self_t, lane, m_, l_, acc);
+    } else {
+      for (int k = w; k < n; k += 4) attend((int64_t)item_j[k] * BS, BS, item_bits[k]);
+    }
+    __syncthreads();
   }
   if (s == S - 1 && ntail > 0 && w == 0) attend(N * BS, ntail, all_bits);
 
@@ -786,26 +1061,78 @@ struct CombineArgs {
   int S;
 };
 
+// One workgroup of 1024 threads per (sequence, query head).  Thread (i, part)
+// owns head dimension i and the splits s = part, part + P, ... (P = 1024 / D):
+// it issues the loads of its splits' maxima and accumulators together, the
+// workgroup takes the largest maximum, and each thread adds its weighted
+// accumulators exp(m_s - m) acc_s[i] (the part-0 threads also the weighted
+// sums l_s); the P partial sums are then added in order.
+constexpr int kCombThreads = 1024;
+constexpr int kCombPrefetch = 16;
+
+__device__ __forceinline__ float block_reduce(float x, bool is_max, float* red) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  x = is_max ? wave_max(x) : wave_sum(x);
+  if (lane == 0) red[w] = x;
+  __syncthreads();
+  float r = red[0];
+  for (int k = 1; k < (int)(blockDim.x >> 6); ++k) r = is_max ? fmaxf(r, red[k]) : r + red[k];
+  __syncthreads();
+  return r;
+}
+
 template <int D>
-__global__ __launch_bounds__(D) void combine_kernel(CombineArgs a) {
+__global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
+  constexpr int P = kCombThreads / D;
+  __shared__ float red[kCombThreads];
+  __shared__ float lred[P];
   const Geom& g = a.g;
-  const int h = blockIdx.x, b = blockIdx.y, i = threadIdx.x;
+  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  const int i = tid % D, part = tid / D;
   const int64_t row = (int64_t)b * g.Hq + h;
   const float2* ml = a.part_ml + row * a.S;
-  float ms = kNegInf;
-  for (int s = 0; s < a.S; ++s) ms = fmaxf(ms, ml[s].x);
-  float L = 0.f, o = 0.f;
+  const float* accp = a.part_acc + row * a.S * D + i;
+  float2 mv[kCombPrefetch];
+  float av[kCombPrefetch];
+  float mloc = kNegInf;
+#pragma unroll
+  for (int k = 0; k < kCombPrefetch; ++k) {
+    const int sidx = part + P * k;
+    const bool in = sidx < a.S;
+    mv[k] = in ? ml[sidx] : make_float2(kNegInf, 0.f);
+    av[k] = in ? accp[(int64_t)sidx * D] : 0.f;
+    mloc = fmaxf(mloc, mv[k].x);
+  }
+  for (int sidx = part + P * kCombPrefetch; sidx < a.S; sidx += P) mloc = fmaxf(mloc, ml[sidx].x);
+  const float ms = block_reduce(mloc, true, red);
+  float o = 0.f, L = 0.f;
   if (ms != kNegInf) {
-    for (int s = 0; s < a.S; ++s) {
-      const float2 e = ml[s];
-      if (e.x == kNegInf) continue;
-      const float wk = __expf(e.x - ms);
+#pragma unroll
+    for (int k = 0; k < kCombPrefetch; ++k) {
+      const float wk = mv[k].x == kNegInf ? 0.f : __expf(mv[k].x - ms);
+      o = fmaf(wk, av[k], o);
+      L = fmaf(mv[k].y, wk, L);
+    }
+    for (int sidx = part + P * kCombPrefetch; sidx < a.S; sidx += P) {
+      const float2 e = ml[sidx];
+      const float wk = e.x == kNegInf ? 0.f : __expf(e.x - ms);
+      o = fmaf(wk, accp[(int64_t)sidx * D], o);
       L = fmaf(e.y, wk, L);
-      o = fmaf(wk, a.part_acc[(row * a.S + s) * D + i], o);
     }
   }
-  store_out(a.out, a.q_dtype, row * D + i, L > 0.f ? o / L : 0.f);
-  if (a.counts != nullptr && i == 0) {
+  red[tid] = o;
+  if (i == 0) lred[part] = L;
+  __syncthreads();
+  if (tid < D) {
+    float x = 0.f, Lt = 0.f;
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      x += red[p * D + tid];
+      Lt += lred[p];
+    }
+    store_out(a.out, a.q_dtype, row * D + tid, Lt > 0.f ? x / Lt : 0.f);
+  }
+  if (a.counts != nullptr && tid == 0) {
     const int64_t T = clamp_len(a.seq_lens, b, g.cap);
     const int64_t N = T / g.BS;
     int64_t c = 0;
@@ -850,8 +1177,8 @@ hipError_t launch_summaries(const Geom& g, const void* k, const int32_t* seq_len
 hipError_t launch_predict(int B, int Hq, int D, int q_dtype, const void* q, const float* W,
                           const float* bias, float* tau, hipStream_t stream, LaunchHook hook) {
   return with_hook(hook, ETA_KERNEL_PREDICT, stream, [&] {
-    hipLaunchKernelGGL(predict_kernel, dim3(B), dim3(256), 0, stream, q, q_dtype, W, bias, tau, Hq,
-                       D);
+    hipLaunchKernelGGL(predict_kernel, dim3(B, (Hq + kPredCols - 1) / kPredCols), dim3(kPredThreads),
+                       0, stream, q, q_dtype, W, bias, tau, Hq, D);
   });
 }
 
@@ -862,7 +1189,7 @@ void launch_screen_impl(const Geom& g, const ScreenArgs& sa, hipStream_t stream)
   dim3 grid(g.n_tiles, g.Hkv, g.B);
 #define ETA_SCR(D_, G_)                                                                         \
   if (g.D == D_ && g.G == G_)                                                                   \
-    hipLaunchKernelGGL((screen_kernel<D_, G_, BOUNDS_ONLY>), grid, dim3(256), 0, stream, sa);
+    hipLaunchKernelGGL((screen_kernel<D_, G_, BOUNDS_ONLY>), grid, dim3(kScreenThreads), 0, stream, sa);
   ETA_SCR(64, 1) ETA_SCR(64, 2) ETA_SCR(64, 4) ETA_SCR(64, 8)
   ETA_SCR(128, 1) ETA_SCR(128, 2) ETA_SCR(128, 4) ETA_SCR(128, 8)
 #undef ETA_SCR
@@ -889,25 +1216,27 @@ void launch_split_impl(const Geom& g, int S, const SplitArgs& sp, hipStream_t st
 
 void launch_combine_impl(const Geom& g, const CombineArgs& ca, hipStream_t stream) {
   dim3 grid(g.Hq, g.B);
-  if (g.D == 64) hipLaunchKernelGGL(combine_kernel<64>, grid, dim3(64), 0, stream, ca);
-  if (g.D == 128) hipLaunchKernelGGL(combine_kernel<128>, grid, dim3(128), 0, stream, ca);
+  if (g.D == 64) hipLaunchKernelGGL(combine_kernel<64>, grid, dim3(kCombThreads), 0, stream, ca);
+  if (g.D == 128) hipLaunchKernelGGL(combine_kernel<128>, grid, dim3(kCombThreads), 0, stream, ca);
 }
 
 }  // namespace
 
 hipError_t launch_decode(const Geom& g, const DecodeCfg& c, int q_dtype, const void* q,
                          const void* k, const void* v, const int32_t* seq_lens,
-                         const eta_summary_t& s, const float* tau, void* out, uint8_t* mask,
+                         const eta_summary_t& s, const float* tau, const float* W,
+                         const float* bias, float* tau_out, void* out, uint8_t* mask,
                          int32_t* counts, const DecodeWs& ws, hipStream_t stream,
                          LaunchHook hook) {
-  ScreenArgs sa{q, seq_lens, tau, s.mu, s.sigma, s.max_norm, mask, ws.hm, ws.ids, ws.tile_cnt,
-                ws.head_cnt, nullptr, g, q_dtype, c.z, c.offset_a, c.rescue_window, c.lwb,
-                c.screen_all};
+  const bool predict = tau == nullptr;
+  ScreenArgs sa{q, seq_lens, tau, W, bias, ws.tau, tau_out, s.mu, s.sigma, s.max_norm, mask,
+                ws.ids, ws.tile_cnt, ws.head_cnt, nullptr, g, q_dtype, predict ? 1 : 0, c.z,
+                c.offset_a, c.rescue_window, c.lwb, c.screen_all};
   hipError_t e = with_hook(hook, ETA_KERNEL_SCREEN, stream,
                            [&] { launch_screen_impl<false>(g, sa, stream); });
   if (e != hipSuccess) return e;
-  SplitArgs sp{q, k, v, seq_lens, tau, ws.hm, ws.ids, ws.tile_cnt, ws.part_ml, ws.part_acc,
-               g, q_dtype, c.beta, c.offset_a, c.self_ungated};
+  SplitArgs sp{q, k, v, seq_lens, predict ? ws.tau : tau, ws.ids, ws.tile_cnt, ws.part_ml,
+               ws.part_acc, g, q_dtype, c.beta, c.offset_a, c.self_ungated};
   e = with_hook(hook, ETA_KERNEL_SPLIT_DECODE, stream,
                 [&] { launch_split_impl<false>(g, c.S, sp, stream); });
   if (e != hipSuccess) return e;
@@ -918,8 +1247,9 @@ hipError_t launch_decode(const Geom& g, const DecodeCfg& c, int q_dtype, const v
 hipError_t launch_bounds(const Geom& g, int q_dtype, const void* q, const int32_t* seq_lens,
                          const eta_summary_t& s, float z, float* bounds, hipStream_t stream,
                          LaunchHook hook) {
-  ScreenArgs sa{q, seq_lens, nullptr, s.mu, s.sigma, s.max_norm, nullptr, nullptr, nullptr,
-                nullptr, nullptr, bounds, g, q_dtype, z, 0.f, 0, 0, 0};
+  ScreenArgs sa{q, seq_lens, nullptr, nullptr, nullptr, nullptr, nullptr, s.mu, s.sigma,
+                s.max_norm, nullptr, nullptr, nullptr, nullptr, bounds, g, q_dtype, 0, z, 0.f,
+                0, 0, 0};
   return with_hook(hook, ETA_KERNEL_BOUNDS, stream,
                    [&] { launch_screen_impl<true>(g, sa, stream); });
 }
@@ -927,7 +1257,7 @@ hipError_t launch_bounds(const Geom& g, int q_dtype, const void* q, const int32_
 hipError_t launch_dense(const Geom& g, int S, int q_dtype, const void* q, const void* k,
                         const void* v, const int32_t* seq_lens, void* out, const DecodeWs& ws,
                         hipStream_t stream, LaunchHook hook) {
-  SplitArgs sp{q, k, v, seq_lens, nullptr, nullptr, nullptr, nullptr, ws.part_ml, ws.part_acc,
+  SplitArgs sp{q, k, v, seq_lens, nullptr, nullptr, nullptr, ws.part_ml, ws.part_acc,
                g, q_dtype, 0.f, 0.f, 0};
   hipError_t e = with_hook(hook, ETA_KERNEL_DENSE_SPLIT, stream,
                            [&] { launch_split_impl<true>(g, S, sp, stream); });

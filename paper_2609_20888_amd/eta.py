@@ -51,7 +51,7 @@ class KernelTime(ctypes.Structure):
 
 # Symbols include/eta.h declares (the CPU test checks the library exports each).
 EXPORTS = ("eta_build_block_summaries", "eta_predict_threshold", "eta_decode_workspace_size",
-           "eta_decode", "eta_block_bounds", "eta_dense_workspace_size", "eta_dense_decode",
+           "eta_decode", "eta_decode_predicted", "eta_block_bounds", "eta_dense_workspace_size", "eta_dense_decode",
            "eta_last_error_string", "eta_abi_version", "eta_profile_begin", "eta_profile_end")
 
 
@@ -83,6 +83,8 @@ def load_library(path: Optional[str] = None):
         "eta_decode_workspace_size": [P(KvDesc), P(DecodeParams), P(sz)],
         "eta_decode": [P(KvDesc), i32, _vp, _vp, _vp, _vp, P(SummaryDesc), _vp, P(DecodeParams),
                        _vp, _vp, _vp, _vp, sz, _vp],
+        "eta_decode_predicted": [P(KvDesc), i32, _vp, _vp, _vp, _vp, P(SummaryDesc), _vp, _vp,
+                                 P(DecodeParams), _vp, _vp, _vp, _vp, _vp, sz, _vp],
         "eta_block_bounds": [P(KvDesc), i32, _vp, _vp, P(SummaryDesc), f32, _vp, _vp],
         "eta_dense_workspace_size": [P(KvDesc), i32, P(sz)],
         "eta_dense_decode": [P(KvDesc), i32, _vp, _vp, _vp, _vp, _vp, i32, _vp, sz, _vp],
@@ -238,6 +240,65 @@ def decode(q, k, v, seq_lens, summ: Summaries, tau, *, block_size: int,
                                      _ptr(out), _ptr(mask), _ptr(counts), _ptr(workspace),
                                      workspace.numel(), _stream(stream)))
     return DecodeOut(out=out, mask=mask, counts=counts)
+
+
+def decode_predicted(q, k, v, seq_lens, summ: Summaries, W, bias, *, block_size: int,
+                     params: Optional[DecodeParams] = None, out=None, mask=None, counts=None,
+                     tau_out=None, want_counts: bool = True,
+                     workspace: Optional[torch.Tensor] = None, stream=None) -> DecodeOut:
+    """eta_decode_predicted: predictor fused into the decode step (tau = concat(q) W + bias)."""
+    B, Hq, d = q.shape
+    p = params if params is not None else decode_params()
+    desc = kv_desc(k, Hq, block_size)
+    if v.shape != k.shape or v.stride() != k.stride() or v.dtype != k.dtype:
+        raise ValueError("K and V must share shape, strides and dtype")
+    if out is None:
+        out = torch.empty_like(q)
+    if mask is None:
+        mask = torch.empty(B, Hq, summ.n_blk_cap, dtype=torch.uint8, device=q.device)
+    if counts is None and want_counts:
+        counts = torch.empty(B, Hq, dtype=torch.int32, device=q.device)
+    nbytes = decode_workspace_size(desc, p)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = alloc_workspace(nbytes, q.device)
+    sd = summ.desc()
+    _check(load_library().eta_decode_predicted(
+        ctypes.byref(desc), _dtype_code(q), _ptr(q), _ptr(k), _ptr(v), _ptr(seq_lens),
+        ctypes.byref(sd), _ptr(W), _ptr(bias), ctypes.byref(p), _ptr(out), _ptr(mask),
+        _ptr(counts), _ptr(tau_out), _ptr(workspace), workspace.numel(), _stream(stream)))
+    return DecodeOut(out=out, mask=mask, counts=counts)
+
+
+class DecodeStep:
+    """A prepared eta_decode_predicted call: descriptors, parameters, output
+    buffers and the workspace are set up once; ``run()`` is a single C call
+    with cached arguments (what a serving loop would do every token).  The
+    thresholds are read from ``bias`` (and W) at every call, so updating those
+    tensors in place takes effect on the next step."""
+
+    def __init__(self, q, k, v, seq_lens, summ: Summaries, W, bias, *, block_size: int,
+                 params: Optional[DecodeParams] = None, want_counts: bool = True, stream=None):
+        B, Hq, d = q.shape
+        self.tensors = (q, k, v, seq_lens, summ.mu, summ.sigma, summ.max_norm, W, bias)
+        self.params = params if params is not None else decode_params()
+        self.desc = kv_desc(k, Hq, block_size)
+        self.sdesc = summ.desc()
+        self.out = torch.empty_like(q)
+        self.mask = torch.empty(B, Hq, summ.n_blk_cap, dtype=torch.uint8, device=q.device)
+        self.counts = torch.empty(B, Hq, dtype=torch.int32, device=q.device) if want_counts else None
+        self.tau = torch.empty(B, Hq, dtype=torch.float32, device=q.device)
+        self.workspace = alloc_workspace(decode_workspace_size(self.desc, self.params), q.device)
+        self._fn = load_library().eta_decode_predicted
+        self._args = (ctypes.byref(self.desc), _dtype_code(q), _ptr(q), _ptr(k), _ptr(v),
+                      _ptr(seq_lens), ctypes.byref(self.sdesc), _ptr(W), _ptr(bias),
+                      ctypes.byref(self.params), _ptr(self.out), _ptr(self.mask),
+                      _ptr(self.counts), _ptr(self.tau), _ptr(self.workspace),
+                      self.workspace.numel(), _stream(stream))
+
+    def run(self) -> None:
+        st = self._fn(*self._args)
+        if st != ETA_OK:
+            _check(st)
 
 
 def block_bounds(q, seq_lens, summ: Summaries, k_like: torch.Tensor, *, block_size: int,

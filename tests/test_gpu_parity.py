@@ -166,6 +166,45 @@ def test_decode_fp32_query_on_bf16_cache():
     say(compare(wl, g, orc, tau_o, np_inputs=np_in))
 
 
+@pytest.mark.parametrize("G,d,b,dt", [(4, 128, 128, torch.bfloat16), (8, 64, 64, torch.bfloat16),
+                                      (1, 64, 64, torch.float32), (2, 128, 64, torch.bfloat16)])
+def test_decode_predicted_equals_predict_then_decode(G, d, b, dt):
+    # the fused predictor uses the stand-alone predictor's summation order:
+    # thresholds, masks and outputs must be bit-identical to the two-call path
+    wl = make_workload(B=3, Hq=2 * G, Hkv=2, d=d, block=b, seq_lens=[b * 90 + 5, b * 33, 70],
+                       dtype=dt, planted={"frac": 0.05}, predictor=True, target_survival=0.15,
+                       seed=50 + G)
+    np_in = oracle_inputs(wl)
+    calibrate_bias(wl, np_in)
+    dev = torch.device("cuda")
+    q, k, v = wl.q.to(dev), wl.k.to(dev), wl.v.to(dev)
+    sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
+    summ = eta.build_block_summaries(k, sl, b, num_q_heads=wl.Hq)
+    W, bias = wl.W.to(dev), wl.bias.to(dev)
+    p = eta.decode_params(beta=wl.beta, z=wl.z, rescue_window=wl.rescue_window)
+    tau = eta.predict_threshold(q, W, bias)
+    ref = eta.decode(q, k, v, sl, summ, tau, block_size=b, params=p)
+    tau_out = torch.full_like(tau, float("nan"))
+    fused = eta.decode_predicted(q, k, v, sl, summ, W, bias, block_size=b, params=p,
+                                 tau_out=tau_out)
+    torch.cuda.synchronize()
+    assert torch.equal(tau_out, tau)
+    assert torch.equal(fused.mask, ref.mask) and torch.equal(fused.counts, ref.counts)
+    assert torch.equal(fused.out, ref.out)
+    # and the fused path against the oracle
+    g = GpuRun(out=fused.out, mask=fused.mask, counts=fused.counts, tau=tau_out, summ=summ)
+    orc, tau_o = run_oracle(wl, np_in)
+    say(compare(wl, g, orc, tau_o, np_inputs=np_in))
+    # constant thresholds through the fused entry point (W = NULL)
+    fused0 = eta.decode_predicted(q, k, v, sl, summ, None, bias, block_size=b, params=p,
+                                  tau_out=tau_out)
+    torch.cuda.synchronize()
+    assert torch.equal(tau_out, bias.expand_as(tau_out))
+    ref0 = eta.decode(q, k, v, sl, summ, bias.expand_as(tau).contiguous(), block_size=b, params=p)
+    torch.cuda.synchronize()
+    assert torch.equal(fused0.out, ref0.out) and torch.equal(fused0.mask, ref0.mask)
+
+
 def test_decode_is_deterministic_and_split_invariant():
     wl = make_workload(B=2, Hq=8, Hkv=2, d=128, block=64, seq_lens=[30000, 20000],
                        planted={"frac": 0.05}, predictor=False, tau_const=1.6, seed=41)
