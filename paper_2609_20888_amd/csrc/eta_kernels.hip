@@ -49,6 +49,7 @@ struct Elem;
 
 template <>
 struct Elem<float> {
+  static __device__ __forceinline__ float get(const float* p, int64_t i) { return p[i]; }
   static __device__ __forceinline__ void load8(const float* p, float (&x)[8]) {
     const float4 a = *reinterpret_cast<const float4*>(p);
     const float4 b = *reinterpret_cast<const float4*>(p + 4);
@@ -68,6 +69,7 @@ struct Elem<float> {
 
 template <>
 struct Elem<uint16_t> {
+  static __device__ __forceinline__ float get(const uint16_t* p, int64_t i) { return bf16lo(p[i]); }
   static __device__ __forceinline__ void load8(const uint16_t* p, float (&x)[8]) {
     const uint4 a = *reinterpret_cast<const uint4*>(p);
     x[0] = bf16lo(a.x); x[1] = bf16hi(a.x); x[2] = bf16lo(a.y); x[3] = bf16hi(a.y);
@@ -224,32 +226,59 @@ constexpr int kPredThreads = 256;
 constexpr int kPredCols = 4;     // columns per stand-alone predictor workgroup
 
 // Per-thread partial sums of columns h0 .. h0 + ncols - 1 (ncols <= NC).
-template <int NC, typename QT>
-__device__ __forceinline__ void pred_loop(const QT* __restrict__ q, const float* __restrict__ W,
-                                          int Hq, int64_t J, int h0, int ncols, float (&acc)[NC]) {
-#pragma unroll 8
-  for (int64_t j = threadIdx.x; j < J; j += kPredThreads) {
-    float x;
-    if constexpr (sizeof(QT) == 4)
-      x = q[j];
-    else
-      x = bf16lo(q[j]);
+// The first kPredRows rows of each thread are loaded into registers by
+// pred_load (so a caller can issue them ahead of other loads) and consumed by
+// pred_sum, which then continues over any further rows in the same order.
+constexpr int kPredRows = 8;
+
+template <int NC>
+struct PredRows {
+  uint32_t x[kPredRows];     // raw query bits (fp32, or bf16 in the low half)
+  float w[kPredRows][NC];
+};
+
+__device__ __forceinline__ float pred_x(uint32_t raw, int q_dtype) {
+  return q_dtype == ETA_DT_F32 ? __uint_as_float(raw) : __uint_as_float(raw << 16);
+}
+
+// All loads unconditional (indexes clamped, the unused values zeroed in
+// pred_sum) so that the kPredRows rows are in flight together; the query is
+// kept as raw bits until pred_sum so that no conversion waits for its load.
+template <int NC>
+__device__ __forceinline__ void pred_load(const void* __restrict__ q, int q_dtype, int64_t qoff,
+                                          const float* __restrict__ W, int Hq, int J, int h0,
+                                          int ncols, PredRows<NC>& r) {
 #pragma unroll
-    for (int c = 0; c < NC; ++c)
-      if (c < ncols) acc[c] = fmaf(x, W[j * Hq + h0 + c], acc[c]);
+  for (int k = 0; k < kPredRows; ++k) {
+    const int j = (int)threadIdx.x + kPredThreads * k;
+    const int jc = j < J ? j : 0;
+    r.x[k] = q_dtype == ETA_DT_F32 ? reinterpret_cast<const uint32_t*>(q)[qoff + jc]
+                                   : (uint32_t)reinterpret_cast<const uint16_t*>(q)[qoff + jc];
+    const float* wr = W + (int64_t)jc * Hq + h0;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) r.w[k][c] = wr[c < ncols ? c : 0];
   }
 }
 
 template <int NC>
-__device__ __forceinline__ void pred_partials(const void* __restrict__ q, int q_dtype, int64_t qoff,
-                                              const float* __restrict__ W, int Hq, int64_t J,
-                                              int h0, int ncols, float (&acc)[NC]) {
+__device__ __forceinline__ void pred_sum(const void* __restrict__ q, int q_dtype, int64_t qoff,
+                                         const float* __restrict__ W, int Hq, int J, int h0,
+                                         int ncols, const PredRows<NC>& r, float (&acc)[NC]) {
 #pragma unroll
   for (int c = 0; c < NC; ++c) acc[c] = 0.f;
-  if (q_dtype == ETA_DT_F32)
-    pred_loop<NC>(reinterpret_cast<const float*>(q) + qoff, W, Hq, J, h0, ncols, acc);
-  else
-    pred_loop<NC>(reinterpret_cast<const uint16_t*>(q) + qoff, W, Hq, J, h0, ncols, acc);
+#pragma unroll
+  for (int k = 0; k < kPredRows; ++k) {
+    const bool in = (int)threadIdx.x + kPredThreads * k < J;
+    const float x = in ? pred_x(r.x[k], q_dtype) : 0.f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) acc[c] = fmaf(x, (in && c < ncols) ? r.w[k][c] : 0.f, acc[c]);
+  }
+  for (int j = (int)threadIdx.x + kPredThreads * kPredRows; j < J; j += kPredThreads) {
+    const float x = load_q(q, q_dtype, qoff + j);
+    const float* wr = W + (int64_t)j * Hq + h0;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) acc[c] = fmaf(x, (c < ncols) ? wr[c] : 0.f, acc[c]);
+  }
 }
 
 // Reduces the partials of the workgroup (kPredThreads threads); red holds
@@ -285,7 +314,9 @@ __global__ __launch_bounds__(kPredThreads) void predict_kernel(const void* __res
   const int64_t J = (int64_t)Hq * D;
   float acc[kPredCols];
   if (W != nullptr) {
-    pred_partials<kPredCols>(q, q_dtype, (int64_t)b * J, W, Hq, J, h0, ncols, acc);
+    PredRows<kPredCols> rows;
+    pred_load<kPredCols>(q, q_dtype, (int64_t)b * J, W, Hq, (int)J, h0, ncols, rows);
+    pred_sum<kPredCols>(q, q_dtype, (int64_t)b * J, W, Hq, (int)J, h0, ncols, rows, acc);
   } else {
 #pragma unroll
     for (int c = 0; c < kPredCols; ++c) acc[c] = 0.f;
@@ -377,6 +408,11 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
     }
     M = a.mx[bg * g.ncap + jc];
   };
+  // predictor rows first (they are consumed first), then this tile's summaries
+  const bool predict = !BOUNDS_ONLY && a.predict && a.W != nullptr;
+  const int64_t Jq = (int64_t)g.Hq * D;
+  PredRows<G> prow;
+  if (predict) pred_load<G>(a.q, a.q_dtype, (int64_t)b * Jq, a.W, g.Hq, (int)Jq, gh * G, G, prow);
   float m0[DQ], sd0[DQ], M0;
   issue((int64_t)tile * kScreenTile, m0, sd0, M0);
 
@@ -395,9 +431,8 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
   if constexpr (!BOUNDS_ONLY) {
     if (a.predict) {
       float acc[G];
-      const int64_t J = (int64_t)g.Hq * D;
-      if (a.W != nullptr) {
-        pred_partials<G>(a.q, a.q_dtype, (int64_t)b * J, a.W, g.Hq, J, gh * G, G, acc);
+      if (predict) {
+        pred_sum<G>(a.q, a.q_dtype, (int64_t)b * Jq, a.W, g.Hq, (int)Jq, gh * G, G, prow, acc);
       } else {
 #pragma unroll
         for (int h = 0; h < G; ++h) acc[h] = 0.f;
@@ -770,14 +805,18 @@ __device__ __forceinline__ void attend_bf16_stream(const uint16_t* __restrict__ 
 #pragma unroll
     for (int c = 0; c < DC; ++c) kr[c] = *reinterpret_cast<const uint4*>(krow + 8 * c);
   };
-  auto load_v = [&](int64_t tb) {
+  auto load_v_rows = [&](int64_t tb, int t0) {
 #pragma unroll
-    for (int t = 0; t < 64; ++t) {
+    for (int t = t0; t < t0 + 16; ++t) {
       if constexpr (DPL == 2)
         vr[t] = *reinterpret_cast<const uint32_t*>(vb + (tb + t) * st + 2 * lane);
       else
         vr[t] = vb[(tb + t) * st + lane];
     }
+  };
+  auto load_v = [&](int64_t tb) {
+#pragma unroll
+    for (int qt = 0; qt < 4; ++qt) load_v_rows(tb, 16 * qt);
   };
   // One tile: scores on the MFMAs, then (MORE) the next tile's K loads into the
   // freed K registers, the softmax update, p.V, then (MORE) the next tile's V
@@ -823,35 +862,41 @@ __device__ __forceinline__ void attend_bf16_stream(const uint16_t* __restrict__ 
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
+    // p.V in four quarters of 16 tokens; as soon as a quarter's V registers
+    // are consumed, that quarter of the next tile's V rows is requested, so
+    // those loads overlap the rest of this tile and the next tile's scores
 #pragma unroll
-    for (int t = 0; t < 64; ++t) {
-      float vv[DPL];
-      if constexpr (DPL == 2) {
-        vv[0] = bf16lo(vr[t]);
-        vv[1] = bf16hi(vr[t]);
-      } else {
-        vv[0] = bf16lo(vr[t]);
-      }
+    for (int qt = 0; qt < 4; ++qt) {
 #pragma unroll
-      for (int hq = 0; hq < NQ; ++hq) {
-        const float4 p4 = *reinterpret_cast<const float4*>(p_s + t * GQ + 4 * hq);
-        const float pr[4] = {p4.x, p4.y, p4.z, p4.w};
+      for (int t = 16 * qt; t < 16 * qt + 16; ++t) {
+        float vv[DPL];
+        if constexpr (DPL == 2) {
+          vv[0] = bf16lo(vr[t]);
+          vv[1] = bf16hi(vr[t]);
+        } else {
+          vv[0] = bf16lo(vr[t]);
+        }
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int h = 4 * hq + r;
-          if (h < G) {
+        for (int hq = 0; hq < NQ; ++hq) {
+          const float4 p4 = *reinterpret_cast<const float4*>(p_s + t * GQ + 4 * hq);
+          const float pr[4] = {p4.x, p4.y, p4.z, p4.w};
 #pragma unroll
-            for (int e = 0; e < DPL; ++e) acc[h][e] = fmaf(pr[r], vv[e], acc[h][e]);
+          for (int r = 0; r < 4; ++r) {
+            const int h = 4 * hq + r;
+            if (h < G) {
+#pragma unroll
+              for (int e = 0; e < DPL; ++e) acc[h][e] = fmaf(pr[r], vv[e], acc[h][e]);
+            }
           }
         }
       }
+      if constexpr (MORE) {
+        __builtin_amdgcn_sched_barrier(0);
+        load_v_rows(tbn, 16 * qt);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
     __builtin_amdgcn_wave_barrier();
-    if constexpr (MORE) {
-      __builtin_amdgcn_sched_barrier(0);
-      load_v(tbn);
-      __builtin_amdgcn_sched_barrier(0);
-    }
   };
   int64_t tb = tile_base(0);
   load_k(tb);
@@ -1000,13 +1045,18 @@ __global__ __launch_bounds__(256) void split_kernel(SplitArgs a) {
     }
     __syncthreads();
     if constexpr (BF) {
-      // this wavefront's items are k = w, w + 4, ...; each is BS / 64 tiles of 64 tokens
+      // the chunk's n items are n * BS / 64 tiles of 64 tokens; wavefront w
+      // takes tiles w, w + 4, ... so the four finish within one tile
       constexpr int SPB = BS / 64;
-      const int nmine = n > w ? (n - w + 3) / 4 : 0;
+      const int ntl = n * SPB;
+      const int nmine = ntl > w ? (ntl - w + 3) / 4 : 0;
       attend_bf16_stream<D, G, DENSE>(
-          kb, vb, g.st, nmine * SPB,
-          [&](int u) { return (int64_t)item_j[w + 4 * (u / SPB)] * BS + 64 * (u % SPB); },
-          [&](int u) { return (uint32_t)item_bits[w + 4 * (u / SPB)]; }, qa_s, use_lo, teff_s,
+          kb, vb, g.st, nmine,
+          [&](int u) {
+            const int x = w + 4 * u;
+            return (int64_t)item_j[x / SPB] * BS + 64 * (x % SPB);
+          },
+          [&](int u) { return (uint32_t)item_bits[(w + 4 * u) / SPB]; }, qa_s, use_lo, teff_s,
           p_s[w], a.beta, scale, self_t, lane, m_, l_, acc);
     } else {
       for (int k = w; k < n; k += 4) attend((int64_t)item_j[k] * BS, BS, item_bits[k]);
@@ -1092,6 +1142,10 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
   const int64_t row = (int64_t)b * g.Hq + h;
   const float2* ml = a.part_ml + row * a.S;
   const float* accp = a.part_acc + row * a.S * D + i;
+  // per-head selected blocks: wavefront 0 sums the tile counts (issued first)
+  int cnt = 0;
+  if (a.counts != nullptr && tid < 64)
+    for (int t = tid; t < g.n_tiles; t += 64) cnt += a.head_cnt[row * g.n_tiles + t];
   float2 mv[kCombPrefetch];
   float av[kCombPrefetch];
   float mloc = kNegInf;
@@ -1132,12 +1186,14 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
     }
     store_out(a.out, a.q_dtype, row * D + tid, Lt > 0.f ? x / Lt : 0.f);
   }
-  if (a.counts != nullptr && tid == 0) {
-    const int64_t T = clamp_len(a.seq_lens, b, g.cap);
-    const int64_t N = T / g.BS;
-    int64_t c = 0;
-    for (int t = 0; t < g.n_tiles; ++t) c += a.head_cnt[row * g.n_tiles + t];
-    a.counts[row] = (int32_t)(c * g.BS + (T - N * g.BS));
+  if (a.counts != nullptr && tid < 64) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
+    if (tid == 0) {
+      const int64_t T = clamp_len(a.seq_lens, b, g.cap);
+      const int64_t N = T / g.BS;
+      a.counts[row] = (int32_t)((int64_t)cnt * g.BS + (T - N * g.BS));
+    }
   }
 }
 
