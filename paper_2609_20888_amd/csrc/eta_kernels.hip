@@ -98,16 +98,34 @@ __device__ __forceinline__ void store_out(void* o, int q_dtype, int64_t idx, flo
     reinterpret_cast<uint16_t*>(o)[idx] = to_bf16(x);
 }
 
-__device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
-  return x;
+// Wavefront-wide butterfly reductions on the vector ALUs (no LDS round trips):
+// quad permutes pair lane ^ 1 and lane ^ 2; the 8- and 16-lane mirrors then
+// pair lanes holding the same values as lane ^ 4 and lane ^ 8 (all lanes of a
+// quad, then of an 8-lane half, are equal by then); the row and half-wave
+// swaps hand each lane both operands of lane ^ 16 and lane ^ 32.  Every lane
+// ends with the same, bitwise identical result.  Full EXEC only.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
 }
 
+template <typename Op>
+__device__ __forceinline__ float wave_reduce(float x, Op op) {
+  x = op(x, dpp_mov<0xB1>(x));    // quad_perm [1,0,3,2]
+  x = op(x, dpp_mov<0x4E>(x));    // quad_perm [2,3,0,1]
+  x = op(x, dpp_mov<0x141>(x));   // row_half_mirror
+  x = op(x, dpp_mov<0x140>(x));   // row_mirror
+  const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = op(__uint_as_float(r16[0]), __uint_as_float(r16[1]));
+  const auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return op(__uint_as_float(r32[0]), __uint_as_float(r32[1]));
+}
+
+__device__ __forceinline__ float wave_max(float x) {
+  return wave_reduce(x, [](float a, float b) { return fmaxf(a, b); });
+}
 __device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
-  return x;
+  return wave_reduce(x, [](float a, float b) { return a + b; });
 }
 
 __device__ __forceinline__ int64_t clamp_len(const int32_t* seq_lens, int b, int64_t cap) {
@@ -408,7 +426,11 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
     }
     M = a.mx[bg * g.ncap + jc];
   };
-  // predictor rows first (they are consumed first), then this tile's summaries
+  // the bias (or given threshold) and the predictor rows first, then this
+  // tile's summaries: each is consumed in that order, so no wait for a later
+  // load holds up an earlier step
+  float tau_in = 0.f;
+  if (!BOUNDS_ONLY && tid < G) tau_in = a.predict ? a.bias[gh * G + tid] : a.tau[hq0 + tid];
   const bool predict = !BOUNDS_ONLY && a.predict && a.W != nullptr;
   const int64_t Jq = (int64_t)g.Hq * D;
   PredRows<G> prow;
@@ -440,7 +462,7 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
       float t = 0.f;
       pred_reduce<G>(acc, G, pred_red, &t);
       if (tid < G) {
-        const float tau = t + a.bias[gh * G + tid];
+        const float tau = t + tau_in;
         teff_s[tid] = tau - a.offset_a;
         if (tile == 0) {
           a.tau_store[hq0 + tid] = tau;
@@ -448,7 +470,7 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
         }
       }
     } else if (tid < G) {
-      teff_s[tid] = a.tau[hq0 + tid] - a.offset_a;
+      teff_s[tid] = tau_in - a.offset_a;
     }
   }
   __syncthreads();
