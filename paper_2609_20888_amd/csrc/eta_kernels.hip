@@ -429,8 +429,22 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
   // the bias (or given threshold) and the predictor rows first, then this
   // tile's summaries: each is consumed in that order, so no wait for a later
   // load holds up an earlier step
+  const int64_t T = clamp_len(a.seq_lens, b, g.cap);
   float tau_in = 0.f;
   if (!BOUNDS_ONLY && tid < G) tau_in = a.predict ? a.bias[gh * G + tid] : a.tau[hq0 + tid];
+  // this wavefront's query elements: heads w, w + 4, ..., dimensions lane + 64 s
+  constexpr int QH = (G + 3) / 4, QI = D / 64;
+  uint32_t qraw[QH][QI];
+#pragma unroll
+  for (int r = 0; r < QH; ++r) {
+    const int h = w + 4 * r < G ? w + 4 * r : 0;
+#pragma unroll
+    for (int si = 0; si < QI; ++si) {
+      const int64_t idx = (hq0 + h) * D + lane + 64 * si;
+      qraw[r][si] = a.q_dtype == ETA_DT_F32 ? reinterpret_cast<const uint32_t*>(a.q)[idx]
+                                            : (uint32_t)reinterpret_cast<const uint16_t*>(a.q)[idx];
+    }
+  }
   const bool predict = !BOUNDS_ONLY && a.predict && a.W != nullptr;
   const int64_t Jq = (int64_t)g.Hq * D;
   PredRows<G> prow;
@@ -439,16 +453,22 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
   issue((int64_t)tile * kScreenTile, m0, sd0, M0);
 
   // the group's queries, their norms (one wavefront per head), thresholds
-  for (int h = w; h < G; h += 4) {
-    float ss = 0.f;
-    for (int i = lane; i < D; i += 64) {
-      const float x = load_q(a.q, a.q_dtype, (hq0 + h) * D + i);
-      q_s[i][h] = x;
-      q2_s[i][h] = x * x;
-      ss = fmaf(x, x, ss);
+#pragma unroll
+  for (int r = 0; r < QH; ++r) {
+    const int h = w + 4 * r;
+    if (h < G) {
+      float ss = 0.f;
+#pragma unroll
+      for (int si = 0; si < QI; ++si) {
+        const int i = lane + 64 * si;
+        const float x = pred_x(qraw[r][si], a.q_dtype);
+        q_s[i][h] = x;
+        q2_s[i][h] = x * x;
+        ss = fmaf(x, x, ss);
+      }
+      ss = wave_sum(ss);
+      if (lane == 0) qn_s[h] = sqrtf(ss);
     }
-    ss = wave_sum(ss);
-    if (lane == 0) qn_s[h] = sqrtf(ss);
   }
   if constexpr (!BOUNDS_ONLY) {
     if (a.predict) {
@@ -475,7 +495,6 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
   }
   __syncthreads();
 
-  const int64_t T = clamp_len(a.seq_lens, b, g.cap);
   const int64_t N = T / g.BS;
 
   // Bounds of blocks jb + lane from loads issued by `issue` (all four
@@ -955,31 +974,51 @@ __global__ __launch_bounds__(256) void split_kernel(SplitArgs a) {
   __shared__ int32_t item_j[kItemChunk];
   __shared__ uint8_t item_bits[kItemChunk];
 
-  const int64_t T = clamp_len(a.seq_lens, b, g.cap);
-  const int64_t N = T / BS;
-  const int ntail = (int)(T - N * BS);
   const int64_t hq0 = (int64_t)b * g.Hq + (int64_t)gh * G;
   const int64_t bg = (int64_t)b * g.Hkv + gh;
   const float scale = 1.0f / sqrtf((float)D);
-  if constexpr (BF) {
-    // chunk (quad, part, head r, c) = 8 bf16 of query head 4 quad + r, dims 8c..8c+7
-    uint16_t* qa16 = reinterpret_cast<uint16_t*>(qa_s);
-    for (int idx = tid; idx < NQ * 4 * D; idx += 256) {
+  // The independent loads go out together: length, the first 256 tile counts,
+  // thresholds and the query elements (as raw bits, converted afterwards, so
+  // that no conversion waits on its own load).
+  const int64_t T = clamp_len(a.seq_lens, b, g.cap);
+  const int32_t* tc = a.tile_cnt + bg * g.n_tiles;
+  const int tc0 = (!DENSE && tid < g.n_tiles) ? tc[tid] : 0;
+  const float tau_in = (!DENSE && tid < G) ? a.tau[hq0 + tid] : 0.f;
+  constexpr int QE = BF ? NQ * 4 * D : G * D;          // staged query elements
+  constexpr int QR = (QE + 255) / 256;
+  uint32_t qraw[QR];
+#pragma unroll
+  for (int r = 0; r < QR; ++r) {
+    const int idx = tid + 256 * r;
+    const int hh = idx / D, i = idx % D;
+    const int64_t src = (hq0 + ((idx < QE && hh < G) ? hh : 0)) * D + i;
+    qraw[r] = a.q_dtype == ETA_DT_F32 ? reinterpret_cast<const uint32_t*>(a.q)[src]
+                                      : (uint32_t)reinterpret_cast<const uint16_t*>(a.q)[src];
+  }
+  const int64_t N = T / BS;
+  const int ntail = (int)(T - N * BS);
+#pragma unroll
+  for (int r = 0; r < QR; ++r) {
+    const int idx = tid + 256 * r;
+    if (idx < QE) {
       const int hh = idx / D, i = idx % D;
-      const int quad = hh / 4, r = hh % 4;
-      const float x = hh < G ? load_q(a.q, a.q_dtype, (hq0 + hh) * D + i) : 0.f;
-      const uint16_t hi = to_bf16(x);
-      const uint16_t lo = to_bf16(x - bf16lo(hi));
-      qa16[(((quad * 2 + 0) * 4 + r) * DC) * 8 + i] = hi;
-      qa16[(((quad * 2 + 1) * 4 + r) * DC) * 8 + i] = lo;
-    }
-  } else {
-    for (int idx = tid; idx < G * D; idx += 256) {
-      const int h = idx / D, i = idx % D;
-      qf_s[i][h] = load_q(a.q, a.q_dtype, (hq0 + h) * D + i) * scale;
+      const float x = hh < G ? (a.q_dtype == ETA_DT_F32 ? __uint_as_float(qraw[r])
+                                                        : __uint_as_float(qraw[r] << 16))
+                             : 0.f;
+      if constexpr (BF) {
+        // chunk (quad, part, head r, c) = 8 bf16 of query head 4 quad + r, dims 8c..8c+7
+        uint16_t* qa16 = reinterpret_cast<uint16_t*>(qa_s);
+        const int quad = hh / 4, rr = hh % 4;
+        const uint16_t hi = to_bf16(x);
+        const uint16_t lo = to_bf16(x - bf16lo(hi));
+        qa16[(((quad * 2 + 0) * 4 + rr) * DC) * 8 + i] = hi;
+        qa16[(((quad * 2 + 1) * 4 + rr) * DC) * 8 + i] = lo;
+      } else {
+        qf_s[i][hh] = x * scale;
+      }
     }
   }
-  if (tid < G) teff_s[tid] = DENSE ? 0.f : a.tau[hq0 + tid] - a.offset_a;
+  if (tid < G) teff_s[tid] = DENSE ? 0.f : tau_in - a.offset_a;
   for (int idx = tid; idx < 4 * 64 * GQ; idx += 256) (&p_s[0][0])[idx] = 0.f;
 
   int64_t lo, hi;
@@ -988,11 +1027,10 @@ __global__ __launch_bounds__(256) void split_kernel(SplitArgs a) {
     hi = (N * (s + 1)) / S;
   } else {
     // exclusive prefix sum of the per-tile union counts, 256 tiles at a time
-    const int32_t* tc = a.tile_cnt + bg * g.n_tiles;
     int carry = 0;
     for (int base = 0; base < g.n_tiles; base += 256) {
       const int t = base + tid;
-      const int x = t < g.n_tiles ? tc[t] : 0;
+      const int x = base == 0 ? tc0 : (t < g.n_tiles ? tc[t] : 0);
       int incl = x;
 #pragma unroll
       for (int o = 1; o < 64; o <<= 1) {
