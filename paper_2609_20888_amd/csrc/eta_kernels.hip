@@ -136,13 +136,55 @@ __device__ __forceinline__ int64_t clamp_len(const int32_t* seq_lens, int b, int
 // ---------------------------------------------------------------- summaries
 //
 // One workgroup handles kSumBlocks consecutive full blocks of one (sequence,
-// kv head).  Each block is staged in LDS as fp32 (padded rows, conflict-free
-// column and row access); the row norms are reduced while staging; the mean
-// and the mean squared deviation are column sums over the staged copy.
-// Consecutive blocks of one workgroup fill the same cache lines of the
-// dimension-major output, so the scattered 4-byte stores merge in L2.
+// kv head); wavefront w takes blocks w, w + 4, ...  A block is read with
+// fully coalesced 16-byte loads: LPR lanes cover one row, so one load covers
+// R = 64 / LPR consecutive rows, and lane l keeps the EPL coordinates
+// EPL (l % LPR) .. + EPL - 1 of rows l / LPR, l / LPR + R, ...  The block
+// stays in registers for the two passes (mean, then mean squared deviation);
+// the row norms are summed over the LPR lanes of a row, and the per-lane
+// sums over the R row groups.  Results are staged in LDS and written as whole
+// rows of kSumBlocks consecutive blocks of the dimension-major output.
 
 constexpr int kSumBlocks = 32;
+
+// Sum over the aligned group of N lanes (N in 8, 16, 32) that holds one row;
+// every lane of the group ends with the same value.
+template <int N>
+__device__ __forceinline__ float lane_group_sum(float x) {
+  x += dpp_mov<0xB1>(x);
+  x += dpp_mov<0x4E>(x);
+  x += dpp_mov<0x141>(x);
+  if constexpr (N >= 16) x += dpp_mov<0x140>(x);
+  if constexpr (N >= 32) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+  return x;
+}
+
+// Combines lanes l, l ^ N, l ^ 2N, ... (the same coordinates of the other row
+// groups) with op; every lane ends with the combined value.
+template <int N, typename Op>
+__device__ __forceinline__ float row_group_reduce(float x, Op op) {
+  if constexpr (N <= 8) x = op(x, dpp_mov<0x128>(x));   // row_ror:8 = lane ^ 8 in a row
+  if constexpr (N <= 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = op(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  }
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return op(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+template <typename KVT>
+__device__ __forceinline__ void unpack16(const uint4& u, float (&f)[16 / sizeof(KVT)]) {
+  if constexpr (sizeof(KVT) == 2) {
+    f[0] = bf16lo(u.x); f[1] = bf16hi(u.x); f[2] = bf16lo(u.y); f[3] = bf16hi(u.y);
+    f[4] = bf16lo(u.z); f[5] = bf16hi(u.z); f[6] = bf16lo(u.w); f[7] = bf16hi(u.w);
+  } else {
+    f[0] = __uint_as_float(u.x); f[1] = __uint_as_float(u.y);
+    f[2] = __uint_as_float(u.z); f[3] = __uint_as_float(u.w);
+  }
+}
 
 template <int D, int BS, typename KVT>
 __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ k, Geom g,
@@ -150,85 +192,107 @@ __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ 
                                                         float* __restrict__ mu,
                                                         float* __restrict__ sigma,
                                                         float* __restrict__ mx) {
-  constexpr int LDR = D + 1;
-  constexpr int CPR = D / 8;        // 8-element chunks per row
-  constexpr int NCH = BS * CPR;
-  constexpr int P = 256 / D;        // partial column sums per coordinate
-  __shared__ float tile[BS * LDR];
-  __shared__ float red[256];
-  __shared__ float mean_s[D];
-  __shared__ float nmax_s[4];
+  constexpr int EPL = 16 / (int)sizeof(KVT);   // coordinates per lane and load
+  constexpr int LPR = D / EPL;                 // lanes per row
+  constexpr int R = 64 / LPR;                  // rows per load
+  constexpr int NI = BS / R;                   // loads per lane and block
+  constexpr int CH = NI * 4 <= 128 ? NI : 16;  // loads held at once (VGPR budget)
+  constexpr int NCH = NI / CH;
+  static_assert(LPR >= 8 && LPR <= 32 && NI % CH == 0, "unsupported summary shape");
+  __shared__ float mu_s[D][kSumBlocks + 1];
+  __shared__ float sg_s[D][kSumBlocks + 1];
+  __shared__ float mx_s[kSumBlocks];
 
   const int gh = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
+  const int rg = lane / LPR, cl = lane % LPR;
   const int64_t T = clamp_len(seq_lens, b, g.cap);
   const int64_t N = T / BS;
   const int64_t j0 = (int64_t)blockIdx.x * kSumBlocks;
+  if (j0 >= N) return;
   const KVT* kb = k + (int64_t)b * g.sb + (int64_t)gh * g.sh;
   const int64_t bg = (int64_t)b * g.Hkv + gh;
-  float* mub = mu + bg * D * g.ncap;
-  float* sgb = sigma + bg * D * g.ncap;
-  float* mxb = mx + bg * g.ncap;
+  constexpr float inv_bs = 1.0f / BS;
 
-  for (int jj = 0; jj < kSumBlocks; ++jj) {
+  for (int jj = w; jj < kSumBlocks; jj += 4) {
     const int64_t j = j0 + jj;
     if (j >= N) break;
-    float n2max = 0.f;
-    for (int c = tid; c < NCH; c += 256) {
-      const int r = c / CPR, cc = c % CPR;
-      float x[8];
-      Elem<KVT>::load8(kb + (j * BS + r) * g.st + cc * 8, x);
-      float n2 = 0.f;
+    const KVT* base = kb + (j * BS + rg) * g.st + cl * EPL;
+    uint4 x[CH];
+    // all of a chunk's loads are issued before any of them is used
+    auto load_chunk = [&](int c) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        tile[r * LDR + cc * 8 + e] = x[e];
-        n2 = fmaf(x[e], x[e], n2);
+      for (int i = 0; i < CH; ++i)
+        x[i] = *reinterpret_cast<const uint4*>(base + (int64_t)(R * (c * CH + i)) * g.st);
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    float s[EPL], v[EPL], n2max = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) { s[e] = 0.f; v[e] = 0.f; }
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      load_chunk(c);
+#pragma unroll
+      for (int i = 0; i < CH; ++i) {
+        float f[EPL];
+        unpack16<KVT>(x[i], f);
+        float n2 = 0.f;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) {
+          s[e] += f[e];
+          n2 = fmaf(f[e], f[e], n2);
+        }
+        n2max = fmaxf(n2max, lane_group_sum<LPR>(n2));
       }
-      // the CPR consecutive lanes holding row r reduce its squared norm
+    }
+    float mean[EPL];
 #pragma unroll
-      for (int o = CPR / 2; o > 0; o >>= 1) n2 += __shfl_xor(n2, o, 64);
-      n2max = fmaxf(n2max, n2);
-    }
-    n2max = wave_max(n2max);
-    if ((tid & 63) == 0) nmax_s[tid >> 6] = n2max;
-    __syncthreads();
-    {
-      const int i = tid % D, part = tid / D;
-      float s = 0.f;
-      for (int r = part; r < BS; r += P) s += tile[r * LDR + i];
-      red[tid] = s;
-    }
-    __syncthreads();
-    if (tid < D) {
-      float s = 0.f;
+    for (int e = 0; e < EPL; ++e)
+      mean[e] = row_group_reduce<LPR>(s[e], [](float a, float c) { return a + c; }) * inv_bs;
 #pragma unroll
-      for (int p = 0; p < P; ++p) s += red[p * D + tid];
-      mean_s[tid] = s * (1.0f / BS);
-    }
-    __syncthreads();
-    {
-      const int i = tid % D, part = tid / D;
-      const float m = mean_s[i];
-      float s = 0.f;
-      for (int r = part; r < BS; r += P) {
-        const float dv = tile[r * LDR + i] - m;
-        s = fmaf(dv, dv, s);
+    for (int c = 0; c < NCH; ++c) {
+      if constexpr (NCH > 1) {
+        load_chunk(c);
+      } else {
+        // unpack again rather than keep pass one's unpacked values alive
+#pragma unroll
+        for (int i = 0; i < CH; ++i) asm volatile("" : "+v"(x[i].x), "+v"(x[i].y), "+v"(x[i].z), "+v"(x[i].w));
       }
-      red[tid] = s;
-    }
-    __syncthreads();
-    if (tid < D) {
-      float s = 0.f;
 #pragma unroll
-      for (int p = 0; p < P; ++p) s += red[p * D + tid];
-      mub[(int64_t)tid * g.ncap + j] = mean_s[tid];
-      sgb[(int64_t)tid * g.ncap + j] = sqrtf(s * (1.0f / BS));
+      for (int i = 0; i < CH; ++i) {
+        float f[EPL];
+        unpack16<KVT>(x[i], f);
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) {
+          const float dv = f[e] - mean[e];
+          v[e] = fmaf(dv, dv, v[e]);
+        }
+      }
     }
-    if (tid == 0) {
-      const float a = fmaxf(fmaxf(nmax_s[0], nmax_s[1]), fmaxf(nmax_s[2], nmax_s[3]));
-      mxb[j] = sqrtf(a);
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+      const float var = row_group_reduce<LPR>(v[e], [](float a, float c) { return a + c; }) * inv_bs;
+      if (rg == 0) {
+        mu_s[cl * EPL + e][jj] = mean[e];
+        sg_s[cl * EPL + e][jj] = sqrtf(var);
+      }
     }
-    __syncthreads();
+    n2max = row_group_reduce<LPR>(n2max, [](float a, float c) { return fmaxf(a, c); });
+    if (lane == 0) mx_s[jj] = sqrtf(n2max);
   }
+  __syncthreads();
+  // whole rows of the dimension-major output (blocks j0 .. j0 + nv - 1)
+  const int nv = N - j0 < kSumBlocks ? (int)(N - j0) : kSumBlocks;
+  float* mub = mu + bg * D * g.ncap + j0;
+  float* sgb = sigma + bg * D * g.ncap + j0;
+  for (int idx = tid; idx < D * kSumBlocks; idx += 256) {
+    const int i = idx / kSumBlocks, jj = idx % kSumBlocks;
+    if (jj < nv) {
+      mub[(int64_t)i * g.ncap + jj] = mu_s[i][jj];
+      sgb[(int64_t)i * g.ncap + jj] = sg_s[i][jj];
+    }
+  }
+  if (tid < nv) mx[bg * g.ncap + j0 + tid] = mx_s[tid];
 }
 
 // ---------------------------------------------------------------- predictor

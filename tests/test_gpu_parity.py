@@ -36,6 +36,10 @@ SUMMARY_CASES = [
     (1, 3, 64, 128, [9000], torch.bfloat16),
     (2, 1, 64, 64, [5000, 63], torch.float32),
     (1, 2, 128, 128, [128 * 40 + 5], torch.float32),
+    (1, 2, 128, 128, [128 * 70 + 17], torch.bfloat16),
+    (2, 1, 64, 64, [64 * 33, 64 * 32], torch.bfloat16),
+    (1, 1, 128, 64, [64 * 50 + 1], torch.float32),
+    (1, 2, 64, 128, [128 * 31], torch.float32),
 ]
 
 
