@@ -113,6 +113,29 @@ def main():
     sum_bytes = B * Hkv * wl.seq_lens[0] * d * e + B * Hkv * (wl.seq_lens[0] // bs) * (2 * d * 4 + 4)
     log(f"[bench] summary build {sum_ms * 1e3:.1f} us ({sum_bytes / sum_ms / 1e6:.0f} GB/s)")
 
+    # ---- index variants: sub-block envelope build (16 sub-blocks per block, as the
+    # paper's b = 64 / b_sub = 4 layout) and the decode-time update when an appended
+    # token completes a block in every (sequence, kv head)
+    env_sub = bs // 16
+    env = eta.build_block_summaries(k, sl, bs, num_q_heads=Hq, sub_block=env_sub)
+    torch.cuda.synchronize()
+    s0.record()
+    for _ in range(reps):
+        eta.build_block_summaries(k, sl, bs, num_q_heads=Hq, sub_block=env_sub, out=env)
+    s1.record()
+    torch.cuda.synchronize()
+    env_ms = s0.elapsed_time(s1) / reps
+    prev = sl - 1
+    upd_reps = 50
+    s0.record()
+    for _ in range(upd_reps):
+        eta.update_block_summaries(k, prev, sl, env, bs, max_new_blocks=1, num_q_heads=Hq)
+    s1.record()
+    torch.cuda.synchronize()
+    upd_ms = s0.elapsed_time(s1) / upd_reps
+    del env
+    log(f"[bench] envelope build {env_ms * 1e3:.1f} us, per-step update {upd_ms * 1e3:.2f} us")
+
     # ---- thresholds: place the predictor bias from the GPU's own bounds
     bounds = eta.block_bounds(q, sl, summ, k, block_size=bs, z=wl.z).cpu().numpy()
     qW = eta.predict_threshold(q, W, torch.zeros(Hq, device=dev)).cpu().numpy().astype(np.float64)
@@ -311,6 +334,9 @@ def main():
         "speedup_vs_dense": round(dense_ms / gpu_ms, 3),
         "summary_build_us": round(sum_ms * 1e3, 1),
         "summary_build_GBps": round(sum_bytes / sum_ms / 1e6, 1),
+        "summary_envelope_build_us": round(env_ms * 1e3, 1),
+        "summary_envelope_sub_block": env_sub,
+        "summary_update_us_per_step": round(upd_ms * 1e3, 2),
         "roofline": {"bound": "hbm", "kernel": "split_decode", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "algorithmic_bytes_per_launch": kv_b,

@@ -129,6 +129,45 @@ eta_status_t eta_build_block_summaries(const eta_kv_desc_t* kv, const void* k,
                                        void* stream);
 
 /*
+ * eta_build_block_summaries_envelope -- as eta_build_block_summaries, with
+ * sigma replaced by the sub-block envelope (App. "Sub-Block Variance
+ * Envelope", Eq. subblock_envelope_appx): per coordinate i, the largest over
+ * the block's contiguous sub-blocks B_m of sub_block tokens of
+ *   sqrt( (1/sub_block) * sum_{k in B_m} (k_i - mu_i)^2 ),
+ * mu the centroid of the whole block.  The decode path uses it where it uses
+ * sigma (the paper's b = 64 configuration).
+ *   sub_block  a power of two in [1, block_size]; 0 gives the flat sigma
+ *              (sub_block = block_size gives the same values as the flat sigma)
+ */
+eta_status_t eta_build_block_summaries_envelope(const eta_kv_desc_t* kv, const void* k,
+                                                const int32_t* seq_lens, int32_t sub_block,
+                                                const eta_summary_t* out, void* stream);
+
+/*
+ * eta_update_block_summaries -- incremental decode-time index update (App.
+ * "End-to-End Systems Accounting": the metadata update that follows each
+ * appended token).  Writes the records of the blocks that became full since
+ * an earlier state of the cache: for each sequence b, blocks
+ *   prev_lens[b] / block_size  ..  min(seq_lens[b] / block_size,
+ *                                      prev_lens[b] / block_size + max_new_blocks) - 1
+ * with exactly the values eta_build_block_summaries(_envelope) writes for them;
+ * every other entry is left as it is.  The tail is never summarised (it is
+ * always attended), so a block's record is emitted once, when it fills.
+ *   prev_lens       device int32 [batch], the lengths the index was built for
+ *   seq_lens        device int32 [batch], the current lengths
+ *   max_new_blocks  >= 0, upper bound on blocks completed per sequence since
+ *                   prev_lens (1 for one appended token per step); it sizes the
+ *                   grid without reading the lengths on the host
+ *   sub_block       0 (flat sigma) or the envelope's sub-block, as above
+ * Lengths are clamped to [0, capacity_tokens]; prev_lens[b] > seq_lens[b]
+ * writes nothing for b.
+ */
+eta_status_t eta_update_block_summaries(const eta_kv_desc_t* kv, const void* k,
+                                        const int32_t* prev_lens, const int32_t* seq_lens,
+                                        int32_t max_new_blocks, int32_t sub_block,
+                                        const eta_summary_t* out, void* stream);
+
+/*
  * eta_predict_threshold -- Eq. (tau_pred): tau[b][h] = sum_j qbar[b][j] W[j][h] + bias[h],
  * qbar[b] the concatenation of the num_q_heads query heads of sequence b
  * (post-RoPE queries).  W == NULL gives frozen per-head constants tau[b][h] =

@@ -233,18 +233,46 @@ const char* eta_last_error_string(void) { return g_err.c_str(); }
 
 int32_t eta_abi_version(void) { return 1; }
 
-eta_status_t eta_build_block_summaries(const eta_kv_desc_t* kv, const void* k,
-                                       const int32_t* seq_lens, const eta_summary_t* out,
-                                       void* stream) {
+static eta_status_t summaries_impl(const eta_kv_desc_t* kv, const void* k,
+                                   const int32_t* prev_lens, const int32_t* seq_lens,
+                                   int32_t max_new_blocks, int32_t sub_block,
+                                   const eta_summary_t* out, void* stream) {
   Geom g;
   eta_status_t st = check_kv(kv, &g);
   if (st) return st;
   if (!k || !seq_lens) return fail(ETA_ERR_INVALID_ARG, "k and seq_lens must be non-NULL");
-  if (!aligned16(k) || !aligned16(seq_lens)) return fail(ETA_ERR_INVALID_ARG, "k / seq_lens must be 16-byte aligned");
+  if (!aligned16(k) || !aligned16(seq_lens) || (prev_lens && !aligned16(prev_lens)))
+    return fail(ETA_ERR_INVALID_ARG, "k / seq_lens / prev_lens must be 16-byte aligned");
+  if (sub_block < 0 || sub_block > g.BS || (sub_block & (sub_block - 1)) != 0)
+    return fail(ETA_ERR_INVALID_ARG, "sub_block must be 0 or a power of two in [1, block_size = %d]", g.BS);
   if ((st = check_summary(out, &g))) return st;
-  hipError_t e = launch_summaries(g, k, seq_lens, *out, (hipStream_t)stream, active_hook());
+  hipError_t e = launch_summaries(g, k, seq_lens, prev_lens, max_new_blocks, sub_block, *out,
+                                  (hipStream_t)stream, active_hook());
   if (e != hipSuccess) return fail(ETA_ERR_HIP, "summaries launch failed: %s", hipGetErrorString(e));
   return ok();
+}
+
+eta_status_t eta_build_block_summaries(const eta_kv_desc_t* kv, const void* k,
+                                       const int32_t* seq_lens, const eta_summary_t* out,
+                                       void* stream) {
+  return summaries_impl(kv, k, nullptr, seq_lens, 0, 0, out, stream);
+}
+
+eta_status_t eta_build_block_summaries_envelope(const eta_kv_desc_t* kv, const void* k,
+                                                const int32_t* seq_lens, int32_t sub_block,
+                                                const eta_summary_t* out, void* stream) {
+  return summaries_impl(kv, k, nullptr, seq_lens, 0, sub_block, out, stream);
+}
+
+eta_status_t eta_update_block_summaries(const eta_kv_desc_t* kv, const void* k,
+                                        const int32_t* prev_lens, const int32_t* seq_lens,
+                                        int32_t max_new_blocks, int32_t sub_block,
+                                        const eta_summary_t* out, void* stream) {
+  if (!prev_lens) return fail(ETA_ERR_INVALID_ARG, "prev_lens must be non-NULL");
+  if (max_new_blocks < 0) return fail(ETA_ERR_INVALID_ARG, "max_new_blocks must be >= 0");
+  if (kv && kv->block_size > 0 && max_new_blocks > kv->capacity_tokens / kv->block_size)
+    max_new_blocks = (int32_t)(kv->capacity_tokens / kv->block_size);
+  return summaries_impl(kv, k, prev_lens, seq_lens, max_new_blocks, sub_block, out, stream);
 }
 
 eta_status_t eta_predict_threshold(int32_t batch, int32_t num_q_heads, int32_t head_dim,

@@ -55,7 +55,11 @@ struct DecodeCfg {
 // `kind_cb` brackets each launch for the optional kernel timer.
 using LaunchHook = void (*)(int kind, hipStream_t stream, bool after);
 
+// prev_lens == nullptr: every full block; else the blocks completed since
+// prev_lens (at most max_new_blocks per sequence).  sub_block > 0 (a power of
+// two dividing the block size): sigma is the sub-block envelope.
 hipError_t launch_summaries(const Geom& g, const void* k, const int32_t* seq_lens,
+                            const int32_t* prev_lens, int max_new_blocks, int sub_block,
                             const eta_summary_t& s, hipStream_t stream, LaunchHook hook);
 
 hipError_t launch_predict(int B, int Hq, int D, int q_dtype, const void* q, const float* W,

@@ -144,6 +144,12 @@ __device__ __forceinline__ int64_t clamp_len(const int32_t* seq_lens, int b, int
 // the row norms are summed over the LPR lanes of a row, and the per-lane
 // sums over the R row groups.  Results are staged in LDS and written as whole
 // rows of kSumBlocks consecutive blocks of the dimension-major output.
+//
+// Variants: ENV replaces sigma by the sub-block envelope (per coordinate, the
+// largest root mean squared deviation from the block mean over contiguous
+// sub-blocks of 2^sub_log2 tokens); with prev_lens, the blocks start at
+// prev_lens[b] / BS (the blocks completed since then) and at most max_new
+// blocks per sequence are written.
 
 constexpr int kSumBlocks = 32;
 
@@ -175,6 +181,30 @@ __device__ __forceinline__ float row_group_reduce(float x, Op op) {
   return op(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
+// Sum over ng (1, 2, 4 or 8) consecutive row groups of N lanes each.
+template <int N>
+__device__ __forceinline__ float partial_group_sum(float x, int ng) {
+  auto swap_sum16 = [](float y) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  };
+  auto swap_sum32 = [](float y) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  };
+  if constexpr (N == 8) {
+    if (ng >= 2) x += dpp_mov<0x128>(x);
+    if (ng >= 4) x = swap_sum16(x);
+    if (ng >= 8) x = swap_sum32(x);
+  } else if constexpr (N == 16) {
+    if (ng >= 2) x = swap_sum16(x);
+    if (ng >= 4) x = swap_sum32(x);
+  } else {
+    if (ng >= 2) x = swap_sum32(x);
+  }
+  return x;
+}
+
 template <typename KVT>
 __device__ __forceinline__ void unpack16(const uint4& u, float (&f)[16 / sizeof(KVT)]) {
   if constexpr (sizeof(KVT) == 2) {
@@ -186,9 +216,11 @@ __device__ __forceinline__ void unpack16(const uint4& u, float (&f)[16 / sizeof(
   }
 }
 
-template <int D, int BS, typename KVT>
+template <int D, int BS, typename KVT, bool ENV>
 __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ k, Geom g,
                                                         const int32_t* __restrict__ seq_lens,
+                                                        const int32_t* __restrict__ prev_lens,
+                                                        int max_new, int sub_log2,
                                                         float* __restrict__ mu,
                                                         float* __restrict__ sigma,
                                                         float* __restrict__ mx) {
@@ -207,8 +239,13 @@ __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ 
   const int lane = tid & 63, w = tid >> 6;
   const int rg = lane / LPR, cl = lane % LPR;
   const int64_t T = clamp_len(seq_lens, b, g.cap);
-  const int64_t N = T / BS;
-  const int64_t j0 = (int64_t)blockIdx.x * kSumBlocks;
+  int64_t N = T / BS;
+  int64_t j0 = (int64_t)blockIdx.x * kSumBlocks;
+  if (prev_lens != nullptr) {
+    const int64_t first = clamp_len(prev_lens, b, g.cap) / BS;
+    j0 += first;
+    if (N > first + max_new) N = first + max_new;
+  }
   if (j0 >= N) return;
   const KVT* kb = k + (int64_t)b * g.sb + (int64_t)gh * g.sh;
   const int64_t bg = (int64_t)b * g.Hkv + gh;
@@ -247,8 +284,10 @@ __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ 
     }
     float mean[EPL];
 #pragma unroll
-    for (int e = 0; e < EPL; ++e)
+    for (int e = 0; e < EPL; ++e) {
       mean[e] = row_group_reduce<LPR>(s[e], [](float a, float c) { return a + c; }) * inv_bs;
+      s[e] = 0.f;   // pass two keeps the envelope here
+    }
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
       if constexpr (NCH > 1) {
@@ -267,14 +306,32 @@ __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ 
           const float dv = f[e] - mean[e];
           v[e] = fmaf(dv, dv, v[e]);
         }
+        if constexpr (ENV) {
+          // a sub-block is ng row groups of kl consecutive loads
+          const int sub = 1 << sub_log2;
+          const int ng = sub < R ? sub : R, kl = sub > R ? sub / R : 1;
+          if (((c * CH + i + 1) & (kl - 1)) == 0) {
+            const float inv_sub = 1.0f / (float)sub;
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) {
+              const float t = partial_group_sum<LPR>(v[e], ng);
+              s[e] = fmaxf(s[e], sqrtf(t * inv_sub));
+              v[e] = 0.f;
+            }
+          }
+        }
       }
     }
 #pragma unroll
     for (int e = 0; e < EPL; ++e) {
-      const float var = row_group_reduce<LPR>(v[e], [](float a, float c) { return a + c; }) * inv_bs;
+      float sd;
+      if constexpr (ENV)
+        sd = row_group_reduce<LPR>(s[e], [](float a, float c) { return fmaxf(a, c); });
+      else
+        sd = sqrtf(row_group_reduce<LPR>(v[e], [](float a, float c) { return a + c; }) * inv_bs);
       if (rg == 0) {
         mu_s[cl * EPL + e][jj] = mean[e];
-        sg_s[cl * EPL + e][jj] = sqrtf(var);
+        sg_s[cl * EPL + e][jj] = sd;
       }
     }
     n2max = row_group_reduce<LPR>(n2max, [](float a, float c) { return fmaxf(a, c); });
@@ -1335,15 +1392,26 @@ hipError_t with_hook(LaunchHook hook, int kind, hipStream_t st, F&& f) {
 // ---------------------------------------------------------------- launchers
 
 hipError_t launch_summaries(const Geom& g, const void* k, const int32_t* seq_lens,
+                            const int32_t* prev_lens, int max_new_blocks, int sub_block,
                             const eta_summary_t& s, hipStream_t stream, LaunchHook hook) {
-  const int64_t nblk = g.cap / g.BS;
+  const int64_t nblk = prev_lens != nullptr ? max_new_blocks : g.cap / g.BS;
   if (nblk <= 0) return hipSuccess;
   dim3 grid((unsigned)((nblk + kSumBlocks - 1) / kSumBlocks), g.Hkv, g.B);
+  int sub_log2 = 0;
+  while (sub_block > 0 && (1 << sub_log2) < sub_block) ++sub_log2;
+  const int max_new = prev_lens != nullptr ? max_new_blocks : 0;
   return with_hook(hook, ETA_KERNEL_SUMMARIES, stream, [&] {
 #define ETA_SUM(D_, BS_, T_)                                                                    \
-  if (g.D == D_ && g.BS == BS_)                                                                 \
-    hipLaunchKernelGGL((summaries_kernel<D_, BS_, T_>), grid, dim3(256), 0, stream,             \
-                       reinterpret_cast<const T_*>(k), g, seq_lens, s.mu, s.sigma, s.max_norm);
+  if (g.D == D_ && g.BS == BS_) {                                                               \
+    if (sub_block > 0)                                                                          \
+      hipLaunchKernelGGL((summaries_kernel<D_, BS_, T_, true>), grid, dim3(256), 0, stream,     \
+                         reinterpret_cast<const T_*>(k), g, seq_lens, prev_lens, max_new,       \
+                         sub_log2, s.mu, s.sigma, s.max_norm);                                  \
+    else                                                                                        \
+      hipLaunchKernelGGL((summaries_kernel<D_, BS_, T_, false>), grid, dim3(256), 0, stream,    \
+                         reinterpret_cast<const T_*>(k), g, seq_lens, prev_lens, max_new,       \
+                         sub_log2, s.mu, s.sigma, s.max_norm);                                  \
+  }
     if (g.kv_dtype == ETA_DT_F32) {
       ETA_SUM(64, 64, float) ETA_SUM(64, 128, float) ETA_SUM(128, 64, float) ETA_SUM(128, 128, float)
     } else {

@@ -50,7 +50,8 @@ class KernelTime(ctypes.Structure):
 
 
 # Symbols include/eta.h declares (the CPU test checks the library exports each).
-EXPORTS = ("eta_build_block_summaries", "eta_predict_threshold", "eta_decode_workspace_size",
+EXPORTS = ("eta_build_block_summaries", "eta_build_block_summaries_envelope",
+           "eta_update_block_summaries", "eta_predict_threshold", "eta_decode_workspace_size",
            "eta_decode", "eta_decode_predicted", "eta_block_bounds", "eta_dense_workspace_size", "eta_dense_decode",
            "eta_last_error_string", "eta_abi_version", "eta_profile_begin", "eta_profile_end")
 
@@ -79,6 +80,8 @@ def load_library(path: Optional[str] = None):
     sz = ctypes.c_size_t
     sigs = {
         "eta_build_block_summaries": [P(KvDesc), _vp, _vp, P(SummaryDesc), _vp],
+        "eta_build_block_summaries_envelope": [P(KvDesc), _vp, _vp, i32, P(SummaryDesc), _vp],
+        "eta_update_block_summaries": [P(KvDesc), _vp, _vp, _vp, i32, i32, P(SummaryDesc), _vp],
         "eta_predict_threshold": [i32, i32, i32, i32, _vp, _vp, _vp, _vp, _vp],
         "eta_decode_workspace_size": [P(KvDesc), P(DecodeParams), P(sz)],
         "eta_decode": [P(KvDesc), i32, _vp, _vp, _vp, _vp, P(SummaryDesc), _vp, P(DecodeParams),
@@ -171,16 +174,35 @@ def decode_params(*, beta=4.0, z=1.0, offset_a=0.0, rescue_window=128, lwb=0,
 
 def build_block_summaries(k: torch.Tensor, seq_lens: torch.Tensor, block_size: int, *,
                           num_q_heads: Optional[int] = None, out: Optional[Summaries] = None,
-                          stream=None) -> Summaries:
-    """eta_build_block_summaries: mu, sigma, M of every full block of K."""
+                          sub_block: int = 0, stream=None) -> Summaries:
+    """eta_build_block_summaries: mu, sigma, M of every full block of K
+    (sub_block > 0: eta_build_block_summaries_envelope, sigma = sub-block envelope)."""
     B, Hkv, T_cap, d = k.shape
     desc = kv_desc(k, num_q_heads or Hkv, block_size)
     if out is None:
         out = Summaries.empty(B, Hkv, d, T_cap // block_size, k.device)
     sd = out.desc()
-    _check(load_library().eta_build_block_summaries(ctypes.byref(desc), _ptr(k), _ptr(seq_lens),
-                                                    ctypes.byref(sd), _stream(stream)))
+    lib = load_library()
+    if sub_block:
+        _check(lib.eta_build_block_summaries_envelope(ctypes.byref(desc), _ptr(k), _ptr(seq_lens),
+                                                      sub_block, ctypes.byref(sd), _stream(stream)))
+    else:
+        _check(lib.eta_build_block_summaries(ctypes.byref(desc), _ptr(k), _ptr(seq_lens),
+                                             ctypes.byref(sd), _stream(stream)))
     return out
+
+
+def update_block_summaries(k: torch.Tensor, prev_lens: torch.Tensor, seq_lens: torch.Tensor,
+                           summ: Summaries, block_size: int, *, max_new_blocks: int = 1,
+                           num_q_heads: Optional[int] = None, sub_block: int = 0,
+                           stream=None) -> Summaries:
+    """eta_update_block_summaries: records of the blocks completed since prev_lens."""
+    desc = kv_desc(k, num_q_heads or k.shape[1], block_size)
+    sd = summ.desc()
+    _check(load_library().eta_update_block_summaries(ctypes.byref(desc), _ptr(k), _ptr(prev_lens),
+                                                     _ptr(seq_lens), max_new_blocks, sub_block,
+                                                     ctypes.byref(sd), _stream(stream)))
+    return summ
 
 
 def predict_threshold(q: torch.Tensor, W: Optional[torch.Tensor], bias: torch.Tensor, *,

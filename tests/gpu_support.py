@@ -69,11 +69,11 @@ def calibrate_bias(wl: Workload, np_inputs=None) -> None:
 
 def run_gpu(wl: Workload, *, num_splits: int = 0, screen_all: bool = False,
             self_ungated: bool = False, tau: Optional[torch.Tensor] = None,
-            rescue_window: Optional[int] = None) -> GpuRun:
+            rescue_window: Optional[int] = None, sub_block: int = 0) -> GpuRun:
     dev = torch.device("cuda")
     q, k, v = wl.q.to(dev), wl.k.to(dev), wl.v.to(dev)
     sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
-    summ = eta.build_block_summaries(k, sl, wl.block, num_q_heads=wl.Hq)
+    summ = eta.build_block_summaries(k, sl, wl.block, num_q_heads=wl.Hq, sub_block=sub_block)
     if tau is None:
         W = None if wl.W is None else wl.W.to(dev)
         tau = eta.predict_threshold(q, W, wl.bias.to(dev))
@@ -86,9 +86,24 @@ def run_gpu(wl: Workload, *, num_splits: int = 0, screen_all: bool = False,
     return GpuRun(out=r.out, mask=r.mask, counts=r.counts, tau=tau, summ=summ)
 
 
+def oracle_summaries(wl: Workload, k: np.ndarray, sub_block: int = 0):
+    """The oracle's (mu, sigma, M) arrays for every (sequence, kv head), laid out as
+    oracle.decode takes them; sub_block > 0 puts the sub-block envelope in sigma."""
+    B, Hkv, Ncap, d = wl.B, wl.Hkv, wl.n_blk_cap, wl.d
+    mu = np.zeros((B, Hkv, Ncap, d)); sg = np.zeros((B, Hkv, Ncap, d)); mx = np.zeros((B, Hkv, Ncap))
+    for b in range(B):
+        N = wl.seq_lens[b] // wl.block
+        for g in range(Hkv):
+            m, s, x = oracle.summaries(k[b, g, :wl.seq_lens[b]], wl.block)
+            if sub_block:
+                s = oracle.envelope(k[b, g, :wl.seq_lens[b]], wl.block, sub_block, m)
+            mu[b, g, :N], sg[b, g, :N], mx[b, g, :N] = m, s, x
+    return mu, sg, mx
+
+
 def run_oracle(wl: Workload, np_inputs=None, rows: Optional[Sequence[int]] = None,
                screen_all: bool = False, self_ungated: bool = False, tau=None,
-               rescue_window: Optional[int] = None):
+               rescue_window: Optional[int] = None, summaries=None):
     q, k, v = np_inputs or oracle_inputs(wl)
     if tau is None:
         W = None if wl.W is None else as_numpy(wl.W)
@@ -97,7 +112,7 @@ def run_oracle(wl: Workload, np_inputs=None, rows: Optional[Sequence[int]] = Non
                          a=wl.a,
                          rescue_window=wl.rescue_window if rescue_window is None else rescue_window,
                          lwb=wl.lwb, self_ungated=self_ungated, screen_all=screen_all, rows=rows,
-                         n_threads=0), tau
+                         summaries=summaries, n_threads=0), tau
 
 
 def _f64(t: torch.Tensor) -> np.ndarray:

@@ -143,3 +143,21 @@ def test_profile_roundtrip_without_launches(lib):
     arr = (eta.KernelTime * len(eta.KERNEL_KINDS))()
     assert lib.eta_profile_end(arr) == eta.ETA_OK
     assert all(arr[i].launches == 0 for i in range(len(eta.KERNEL_KINDS)))
+
+
+def test_summary_variants_reject(lib):
+    d = good_desc()                                  # block_size 64
+    s = eta.SummaryDesc(mu=FAKE, sigma=FAKE, max_norm=FAKE, n_blk_cap=64)
+    env = lib.eta_build_block_summaries_envelope
+    for bad in (-1, 3, 48, 128):                     # not a power of two in [1, 64]
+        assert env(ctypes.byref(d), FAKE, FAKE, bad, ctypes.byref(s), None) == eta.ETA_ERR_INVALID_ARG
+    assert "sub_block" in lib.eta_last_error_string().decode()
+    upd = lib.eta_update_block_summaries
+    assert upd(ctypes.byref(d), FAKE, None, FAKE, 1, 0, ctypes.byref(s), None) == eta.ETA_ERR_INVALID_ARG
+    assert upd(ctypes.byref(d), FAKE, FAKE, FAKE, -1, 0, ctypes.byref(s), None) == eta.ETA_ERR_INVALID_ARG
+    assert upd(ctypes.byref(d), FAKE, FAKE + 4, FAKE, 1, 0, ctypes.byref(s), None) == eta.ETA_ERR_INVALID_ARG
+    assert upd(ctypes.byref(d), FAKE, FAKE, FAKE, 1, 5, ctypes.byref(s), None) == eta.ETA_ERR_INVALID_ARG
+    small = eta.SummaryDesc(mu=FAKE, sigma=FAKE, max_norm=FAKE, n_blk_cap=63)
+    assert upd(ctypes.byref(d), FAKE, FAKE, FAKE, 1, 0, ctypes.byref(small), None) == eta.ETA_ERR_INVALID_ARG
+    # no block can have completed: nothing is launched
+    assert upd(ctypes.byref(d), FAKE, FAKE, FAKE, 0, 4, ctypes.byref(s), None) == eta.ETA_OK
