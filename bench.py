@@ -281,6 +281,32 @@ def main():
         if is_primary:
             primary = (ms, gpu_ms, kt, kv_b, step_b, ub, dh, du, steps, warm, cold_ms)
 
+    # ---- the same steps screening on half-precision records (fp16 mu / sigma, as the
+    # paper's compact record); the headline keeps the fp32 index
+    summ16 = eta.build_block_summaries(k, sl, bs, num_q_heads=Hq, stat_dtype=torch.float16)
+    prep16 = eta.DecodeStep(q, k, v, sl, summ16, W, bias_buf, block_size=bs, params=params)
+    index_f16 = {}
+    for s in (SWEEP if not args.only_primary else (PRIMARY_SURVIVAL,)):
+        set_point(biases[s])
+        for _ in range(5):
+            prep16.run()
+        torch.cuda.synchronize()
+        n16 = max(20, args.steps // 4)
+        t0 = time.perf_counter()
+        for _ in range(n16):
+            prep16.run()
+        torch.cuda.synchronize()
+        index_f16[f"{int(round(s * 100))}%"] = round((time.perf_counter() - t0) * 1e6 / n16, 2)
+    set_point(biases[PRIMARY_SURVIVAL])
+    eta.profile_begin()
+    for _ in range(50):
+        prep16.run()
+    torch.cuda.synchronize()
+    kt16 = eta.profile_end()
+    index_f16["screen_avg_us_20%"] = round(kt16["screen"][0] / max(kt16["screen"][1], 1) * 1e3, 2)
+    log(f"[bench] fp16 index: {index_f16}")
+    del prep16, summ16
+
     ms, gpu_ms, kt, kv_b, step_b, ub, dh, du, steps, warm, cold_ms = primary
     split_ms, split_n = kt["split_decode"]
     split_avg_ms = split_ms / max(split_n, 1)
@@ -337,6 +363,7 @@ def main():
         "summary_envelope_build_us": round(env_ms * 1e3, 1),
         "summary_envelope_sub_block": env_sub,
         "summary_update_us_per_step": round(upd_ms * 1e3, 2),
+        "index_f16_us_per_step": index_f16,
         "roofline": {"bound": "hbm", "kernel": "split_decode", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "algorithmic_bytes_per_launch": kv_b,

@@ -58,7 +58,9 @@ typedef enum {
   ETA_ERR_HIP = 4            /* a HIP runtime call or kernel launch failed */
 } eta_status_t;
 
-typedef enum { ETA_DT_F32 = 0, ETA_DT_BF16 = 1 } eta_dtype_t;
+/* Element types.  q, K and V are ETA_DT_F32 or ETA_DT_BF16; block-index
+ * records (mu, sigma) are ETA_DT_F32 or ETA_DT_F16. */
+typedef enum { ETA_DT_F32 = 0, ETA_DT_BF16 = 1, ETA_DT_F16 = 2 } eta_dtype_t;
 
 /*
  * KV cache geometry.  K and V share it.  Element (b, h, t, i) of K lives at
@@ -82,22 +84,28 @@ typedef struct {
 
 /*
  * Block index (the "Dual Probabilistic-Geometric Block Index" of Sec.
- * "Block-Based Scanning via Dual Metadata Caching"), fp32, dimension-major so
- * that a wavefront reading coordinate i of 64 consecutive blocks issues one
+ * "Block-Based Scanning via Dual Metadata Caching"), dimension-major so that a
+ * wavefront reading coordinate i of 64 consecutive blocks issues one
  * coalesced load:
  *   mu[((b*num_kv_heads + h)*head_dim + i)*n_blk_cap + j]     centroid
  *   sigma[((b*num_kv_heads + h)*head_dim + i)*n_blk_cap + j]  coordinate std (population)
- *   max_norm[(b*num_kv_heads + h)*n_blk_cap + j]              largest key L2 norm
- * The standard deviation (not the variance) is stored, as the paper does
- * (App. "GQA-Grouped Execution and Compact Metadata Layout").
+ *   max_norm[(b*num_kv_heads + h)*n_blk_cap + j]              largest key L2 norm, fp32
+ * mu and sigma are stat_dtype: fp32, or fp16 as in the paper's compact record
+ * (App. "GQA-Grouped Execution and Compact Metadata Layout": half-precision
+ * centroid and standard deviation, fp32 maximum norm).  The statistics are
+ * computed in fp32 and rounded to nearest-even when stored as fp16; the bound
+ * is evaluated in fp32 either way.  The standard deviation (not the variance)
+ * is stored, as the paper does, so small spreads do not underflow in fp16.
  * n_blk_cap >= capacity_tokens / block_size, n_blk_cap < 2^24 and
  * n_blk_cap <= 131072 (2048 screening tiles of 64 blocks).
  */
 typedef struct {
-  float* mu;
-  float* sigma;
+  void* mu;
+  void* sigma;
   float* max_norm;
   int64_t n_blk_cap;
+  int32_t stat_dtype;          /* ETA_DT_F32 (0) or ETA_DT_F16 */
+  int32_t reserved;            /* 0 */
 } eta_summary_t;
 
 /* Decode hyper-parameters (Alg. "Hardware-Aligned Block-Sparse Decoding (Inference)"). */

@@ -65,6 +65,10 @@ def _load():
     lib.eta_oracle_envelope.restype = None
     lib.eta_oracle_envelope.argtypes = [_vp, ctypes.c_int, ctypes.c_int64, ctypes.c_int64,
                                         ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp]
+    lib.eta_oracle_round_f16.restype = ctypes.c_double
+    lib.eta_oracle_round_f16.argtypes = [ctypes.c_double]
+    lib.eta_oracle_round_f16_array.restype = None
+    lib.eta_oracle_round_f16_array.argtypes = [_vp, _vp, ctypes.c_int64]
     lib.eta_oracle_bound.restype = ctypes.c_double
     lib.eta_oracle_bound.argtypes = [_vp, _vp, _vp, ctypes.c_double, ctypes.c_int, ctypes.c_double]
     lib.eta_oracle_predict.restype = None
@@ -122,6 +126,15 @@ def summaries(k: np.ndarray, b: int):
     mu = np.zeros((max(N, 1), d)); sg = np.zeros((max(N, 1), d)); mx = np.zeros(max(N, 1))
     _load().eta_oracle_summaries(_ptr(k), _dtype_code(k), d, T, d, b, _ptr(mu), _ptr(sg), _ptr(mx))
     return mu[:N], sg[:N], mx[:N]
+
+
+def round_f16(x) -> np.ndarray:
+    """Nearest binary16 values (ties to even) as float64: the fp16 index records of
+    App. "GQA-Grouped Execution and Compact Metadata Layout"."""
+    a = np.ascontiguousarray(np.asarray(x, np.float64))
+    out = np.empty_like(a)
+    _load().eta_oracle_round_f16_array(_ptr(a), _ptr(out), a.size)
+    return out
 
 
 def envelope(k: np.ndarray, b: int, b_sub: int, mu: np.ndarray) -> np.ndarray:

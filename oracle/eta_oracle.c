@@ -24,6 +24,10 @@
  *       Kernel Validation"; slack tau_eff = tau - a for screening and gate
  *       (same algorithm); pinning of the most recent blocks
  *       (App. sub-block envelope paragraph, "lwb").
+ *   - half-precision index records: the fp16 centroid / standard deviation
+ *       of App. "GQA-Grouped Execution and Compact Metadata Layout",
+ *       modelled by rounding the fp64 statistics to the nearest IEEE 754
+ *       binary16 value (ties to even) before the bound uses them.
  *   - softmax over the attended set: the plain definition (Sec.
  *       "Elastic Threshold Attention", dense attention output), which the
  *       chunked two-stage reduction of the paper reaches exactly.
@@ -112,6 +116,33 @@ void eta_oracle_summaries(const void* k, int dt, int64_t row_stride, int64_t T, 
  * sub-blocks of b_sub tokens of sqrt(mean over the sub-block of (k_i - mu_i)^2),
  * with mu the full-block centroid.  Same layout as eta_oracle_summaries.
  */
+/*
+ * Nearest IEEE 754 binary16 value to x, ties to even, returned as a double:
+ * 11 significant bits, binades 2^-14 .. 2^15, fixed spacing 2^-24 below 2^-14
+ * (subnormals), largest finite 65504; magnitudes of 65520 and above round to
+ * infinity.  NaN, infinities and zeros pass through.
+ */
+double eta_oracle_round_f16(double x) {
+  if (isnan(x) || isinf(x) || x == 0.0) return x;
+  const double a = fabs(x);
+  double r;
+  if (a >= 65520.0) {
+    r = INFINITY;
+  } else {
+    int e;
+    frexp(a, &e);              /* a in [2^(e-1), 2^e) */
+    int ex = e - 1;
+    if (ex < -14) ex = -14;    /* subnormal range: the spacing of the lowest binade */
+    const double ulp = ldexp(1.0, ex - 10);
+    r = nearbyint(a / ulp) * ulp;   /* a / ulp is exact; default mode rounds half to even */
+  }
+  return copysign(r, x);
+}
+
+void eta_oracle_round_f16_array(const double* in, double* out, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) out[i] = eta_oracle_round_f16(in[i]);
+}
+
 void eta_oracle_envelope(const void* k, int dt, int64_t row_stride, int64_t T, int d, int b,
                          int b_sub, const double* mu, double* env) {
   int64_t N = T / b;

@@ -83,6 +83,7 @@ eta_status_t check_kv(const eta_kv_desc_t* kv, Geom* g) {
   g->BS = kv->block_size;
   g->G = G;
   g->kv_dtype = kv->kv_dtype;
+  g->stat_dtype = ETA_DT_F32;
   g->cap = kv->capacity_tokens;
   g->sb = kv->stride_b;
   g->sh = kv->stride_h;
@@ -99,6 +100,9 @@ eta_status_t check_summary(const eta_summary_t* s, Geom* g) {
     return fail(ETA_ERR_INVALID_ARG, "summary buffers must be non-NULL");
   if (!aligned16(s->mu) || !aligned16(s->sigma) || !aligned16(s->max_norm))
     return fail(ETA_ERR_INVALID_ARG, "summary buffers must be 16-byte aligned");
+  if (s->stat_dtype != ETA_DT_F32 && s->stat_dtype != ETA_DT_F16)
+    return fail(ETA_ERR_INVALID_ARG, "stat_dtype %d: summaries are ETA_DT_F32 or ETA_DT_F16", s->stat_dtype);
+  g->stat_dtype = s->stat_dtype;
   if (s->n_blk_cap < g->cap / g->BS)
     return fail(ETA_ERR_INVALID_ARG, "n_blk_cap (%lld) < capacity_tokens / block_size (%lld)",
                 (long long)s->n_blk_cap, (long long)(g->cap / g->BS));
@@ -231,7 +235,7 @@ extern "C" {
 
 const char* eta_last_error_string(void) { return g_err.c_str(); }
 
-int32_t eta_abi_version(void) { return 1; }
+int32_t eta_abi_version(void) { return 2; }
 
 static eta_status_t summaries_impl(const eta_kv_desc_t* kv, const void* k,
                                    const int32_t* prev_lens, const int32_t* seq_lens,

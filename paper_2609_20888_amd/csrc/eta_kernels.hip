@@ -221,8 +221,8 @@ __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ 
                                                         const int32_t* __restrict__ seq_lens,
                                                         const int32_t* __restrict__ prev_lens,
                                                         int max_new, int sub_log2,
-                                                        float* __restrict__ mu,
-                                                        float* __restrict__ sigma,
+                                                        void* __restrict__ mu,
+                                                        void* __restrict__ sigma,
                                                         float* __restrict__ mx) {
   constexpr int EPL = 16 / (int)sizeof(KVT);   // coordinates per lane and load
   constexpr int LPR = D / EPL;                 // lanes per row
@@ -340,13 +340,19 @@ __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ 
   __syncthreads();
   // whole rows of the dimension-major output (blocks j0 .. j0 + nv - 1)
   const int nv = N - j0 < kSumBlocks ? (int)(N - j0) : kSumBlocks;
-  float* mub = mu + bg * D * g.ncap + j0;
-  float* sgb = sigma + bg * D * g.ncap + j0;
+  const int64_t ob = bg * D * g.ncap + j0;
+  const bool f16 = g.stat_dtype == ETA_DT_F16;
   for (int idx = tid; idx < D * kSumBlocks; idx += 256) {
     const int i = idx / kSumBlocks, jj = idx % kSumBlocks;
     if (jj < nv) {
-      mub[(int64_t)i * g.ncap + jj] = mu_s[i][jj];
-      sgb[(int64_t)i * g.ncap + jj] = sg_s[i][jj];
+      const int64_t o = ob + (int64_t)i * g.ncap + jj;
+      if (f16) {   // round to nearest even
+        reinterpret_cast<_Float16*>(mu)[o] = (_Float16)mu_s[i][jj];
+        reinterpret_cast<_Float16*>(sigma)[o] = (_Float16)sg_s[i][jj];
+      } else {
+        reinterpret_cast<float*>(mu)[o] = mu_s[i][jj];
+        reinterpret_cast<float*>(sigma)[o] = sg_s[i][jj];
+      }
     }
   }
   if (tid < nv) mx[bg * g.ncap + j0 + tid] = mx_s[tid];
@@ -497,8 +503,8 @@ struct ScreenArgs {
   const float* bias;
   float* tau_store;          // predicted thresholds for the decode kernel (tile 0 writes)
   float* tau_out;            // optional copy for the caller
-  const float* mu;
-  const float* sigma;
+  const void* mu;             // stat type ST
+  const void* sigma;
   const float* mx;
   uint8_t* mask;
   int32_t* ids;
@@ -515,7 +521,7 @@ struct ScreenArgs {
 constexpr int kScreenThreads = 256;
 constexpr uint32_t kIdMask = 0x00ffffffu;   // union id: block index | head bits << 24
 
-template <int D, int G, bool BOUNDS_ONLY>
+template <int D, int G, bool BOUNDS_ONLY, typename ST>
 __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
   constexpr int DQ = D / 4;            // dimensions per quarter
   const Geom& g = a.g;
@@ -538,12 +544,12 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
   auto issue = [&](int64_t jb, float (&m)[DQ], float (&sd)[DQ], float& M) {
     int64_t jc = jb + lane;
     jc = jc < g.ncap ? jc : g.ncap - 1;
-    const float* mup = a.mu + (bg * D + w * DQ) * g.ncap + jc;
-    const float* sgp = a.sigma + (bg * D + w * DQ) * g.ncap + jc;
+    const ST* mup = reinterpret_cast<const ST*>(a.mu) + (bg * D + w * DQ) * g.ncap + jc;
+    const ST* sgp = reinterpret_cast<const ST*>(a.sigma) + (bg * D + w * DQ) * g.ncap + jc;
 #pragma unroll
     for (int i = 0; i < DQ; ++i) {
-      m[i] = mup[(int64_t)i * g.ncap];
-      sd[i] = sgp[(int64_t)i * g.ncap];
+      m[i] = (float)mup[(int64_t)i * g.ncap];
+      sd[i] = (float)sgp[(int64_t)i * g.ncap];
     }
     M = a.mx[bg * g.ncap + jc];
   };
@@ -1436,8 +1442,14 @@ template <bool BOUNDS_ONLY>
 void launch_screen_impl(const Geom& g, const ScreenArgs& sa, hipStream_t stream) {
   dim3 grid(g.n_tiles, g.Hkv, g.B);
 #define ETA_SCR(D_, G_)                                                                         \
-  if (g.D == D_ && g.G == G_)                                                                   \
-    hipLaunchKernelGGL((screen_kernel<D_, G_, BOUNDS_ONLY>), grid, dim3(kScreenThreads), 0, stream, sa);
+  if (g.D == D_ && g.G == G_) {                                                                 \
+    if (g.stat_dtype == ETA_DT_F16)                                                             \
+      hipLaunchKernelGGL((screen_kernel<D_, G_, BOUNDS_ONLY, _Float16>), grid,                  \
+                         dim3(kScreenThreads), 0, stream, sa);                                  \
+    else                                                                                        \
+      hipLaunchKernelGGL((screen_kernel<D_, G_, BOUNDS_ONLY, float>), grid,                     \
+                         dim3(kScreenThreads), 0, stream, sa);                                  \
+  }
   ETA_SCR(64, 1) ETA_SCR(64, 2) ETA_SCR(64, 4) ETA_SCR(64, 8)
   ETA_SCR(128, 1) ETA_SCR(128, 2) ETA_SCR(128, 4) ETA_SCR(128, 8)
 #undef ETA_SCR

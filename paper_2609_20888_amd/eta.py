@@ -18,7 +18,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libeta.so")
 
 ETA_OK, ETA_ERR_INVALID_ARG, ETA_ERR_UNSUPPORTED, ETA_ERR_WORKSPACE, ETA_ERR_HIP = range(5)
-ETA_DT_F32, ETA_DT_BF16 = 0, 1
+ETA_DT_F32, ETA_DT_BF16, ETA_DT_F16 = 0, 1, 2
 KERNEL_KINDS = ("summaries", "predict", "screen", "split_decode", "combine", "dense_split",
                 "dense_combine", "bounds")
 
@@ -35,7 +35,8 @@ class KvDesc(ctypes.Structure):
 
 
 class SummaryDesc(ctypes.Structure):
-    _fields_ = [("mu", _vp), ("sigma", _vp), ("max_norm", _vp), ("n_blk_cap", ctypes.c_int64)]
+    _fields_ = [("mu", _vp), ("sigma", _vp), ("max_norm", _vp), ("n_blk_cap", ctypes.c_int64),
+                ("stat_dtype", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class DecodeParams(ctypes.Structure):
@@ -152,14 +153,17 @@ class Summaries:
         return self.mu.shape[-1]
 
     def desc(self) -> SummaryDesc:
+        st = {torch.float32: ETA_DT_F32, torch.float16: ETA_DT_F16}[self.mu.dtype]
         return SummaryDesc(mu=_ptr(self.mu), sigma=_ptr(self.sigma), max_norm=_ptr(self.max_norm),
-                           n_blk_cap=self.n_blk_cap)
+                           n_blk_cap=self.n_blk_cap, stat_dtype=st)
 
     @staticmethod
-    def empty(B: int, Hkv: int, d: int, n_blk_cap: int, device) -> "Summaries":
+    def empty(B: int, Hkv: int, d: int, n_blk_cap: int, device,
+              stat_dtype: torch.dtype = torch.float32) -> "Summaries":
+        """stat_dtype: torch.float32 or torch.float16 (mu and sigma records)."""
         n = max(int(n_blk_cap), 1)
-        return Summaries(mu=torch.zeros(B, Hkv, d, n, device=device, dtype=torch.float32),
-                         sigma=torch.zeros(B, Hkv, d, n, device=device, dtype=torch.float32),
+        return Summaries(mu=torch.zeros(B, Hkv, d, n, device=device, dtype=stat_dtype),
+                         sigma=torch.zeros(B, Hkv, d, n, device=device, dtype=stat_dtype),
                          max_norm=torch.zeros(B, Hkv, n, device=device, dtype=torch.float32))
 
 
@@ -174,13 +178,15 @@ def decode_params(*, beta=4.0, z=1.0, offset_a=0.0, rescue_window=128, lwb=0,
 
 def build_block_summaries(k: torch.Tensor, seq_lens: torch.Tensor, block_size: int, *,
                           num_q_heads: Optional[int] = None, out: Optional[Summaries] = None,
-                          sub_block: int = 0, stream=None) -> Summaries:
+                          sub_block: int = 0, stat_dtype: torch.dtype = torch.float32,
+                          stream=None) -> Summaries:
     """eta_build_block_summaries: mu, sigma, M of every full block of K
-    (sub_block > 0: eta_build_block_summaries_envelope, sigma = sub-block envelope)."""
+    (sub_block > 0: eta_build_block_summaries_envelope, sigma = sub-block envelope;
+    stat_dtype torch.float16: half-precision mu / sigma records)."""
     B, Hkv, T_cap, d = k.shape
     desc = kv_desc(k, num_q_heads or Hkv, block_size)
     if out is None:
-        out = Summaries.empty(B, Hkv, d, T_cap // block_size, k.device)
+        out = Summaries.empty(B, Hkv, d, T_cap // block_size, k.device, stat_dtype)
     sd = out.desc()
     lib = load_library()
     if sub_block:

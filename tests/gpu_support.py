@@ -69,11 +69,13 @@ def calibrate_bias(wl: Workload, np_inputs=None) -> None:
 
 def run_gpu(wl: Workload, *, num_splits: int = 0, screen_all: bool = False,
             self_ungated: bool = False, tau: Optional[torch.Tensor] = None,
-            rescue_window: Optional[int] = None, sub_block: int = 0) -> GpuRun:
+            rescue_window: Optional[int] = None, sub_block: int = 0,
+            stat_dtype: torch.dtype = torch.float32) -> GpuRun:
     dev = torch.device("cuda")
     q, k, v = wl.q.to(dev), wl.k.to(dev), wl.v.to(dev)
     sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
-    summ = eta.build_block_summaries(k, sl, wl.block, num_q_heads=wl.Hq, sub_block=sub_block)
+    summ = eta.build_block_summaries(k, sl, wl.block, num_q_heads=wl.Hq, sub_block=sub_block,
+                                     stat_dtype=stat_dtype)
     if tau is None:
         W = None if wl.W is None else wl.W.to(dev)
         tau = eta.predict_threshold(q, W, wl.bias.to(dev))
@@ -130,10 +132,72 @@ def _band_variants(om: np.ndarray, band_idx: np.ndarray):
         yield m
 
 
+U32 = 2.0 ** -24   # fp32 unit roundoff
+
+
+def f16_record_ranges(wl: Workload, k: np.ndarray, mu: np.ndarray, sg: np.ndarray,
+                      sub_block: int = 0):
+    """For each fp16 record value, the interval [lo, hi] of values the GPU may store.
+
+    The GPU rounds (nearest even) fp32 statistics that lie within the classical
+    summation error bound of the exact ones:
+      |mu32 - mu|       <= dmu = (b - 1) u mean_t |k_ti|
+      |sigma32 - sigma| <= (b + 8) u sigma + min(dmu, dmu^2 / (2 sigma))
+    (u = 2^-24; the last term is what the mean's error does to the spread: zero
+    to first order, never more than dmu; for the sub-block envelope, whose
+    sub-blocks are not centred on the block mean, dmu itself).  Rounding is
+    monotone, so the stored
+    value lies between the roundings of the interval's ends.  mu, sg: the
+    oracle's fp64 statistics [B][Hkv][Ncap][d].  Returns (mu_lo, mu_hi, sg_lo, sg_hi).
+    """
+    mabs = np.zeros_like(mu)
+    for b in range(wl.B):
+        N = wl.seq_lens[b] // wl.block
+        if N == 0:
+            continue
+        x = _q64(k[b, :, :N * wl.block]).reshape(wl.Hkv, N, wl.block, wl.d)
+        mabs[b, :, :N] = np.abs(x).mean(axis=2)
+    bs = wl.block
+    dmu = (bs - 1) * U32 * mabs
+    if sub_block:
+        dsg = (bs + 8) * U32 * sg + dmu
+    else:
+        dsg = (bs + 8) * U32 * sg + np.minimum(dmu, dmu ** 2 / (2.0 * np.maximum(sg, 1e-300)))
+    return (oracle.round_f16(mu - dmu), oracle.round_f16(mu + dmu),
+            oracle.round_f16(sg - dsg), oracle.round_f16(sg + dsg))
+
+
+def f16_band(wl: Workload, q: np.ndarray, mu16: np.ndarray, sg16: np.ndarray, ranges) -> np.ndarray:
+    """Largest change [B][Hq][Ncap] of each block bound when every record value
+    moves anywhere within its admissible fp16 interval (f16_record_ranges):
+    s (sum_i |q_i| e_i + z sqrt(sum_i q_i^2 f_i^2)) with e, f the largest
+    distances from the oracle's own fp16 values, by the triangle inequality."""
+    mlo, mhi, slo, shi = ranges
+    emu = np.maximum(np.abs(mhi - mu16), np.abs(mlo - mu16))
+    esg = np.maximum(np.abs(shi - sg16), np.abs(slo - sg16))
+    qd = _q64(q)
+    B, Hkv, Ncap, d = mu16.shape
+    G = wl.Hq // Hkv
+    out = np.zeros((B, wl.Hq, Ncap))
+    for b in range(B):
+        for h in range(wl.Hq):
+            g = h // G
+            qa = np.abs(qd[b, h])
+            out[b, h] = (emu[b, g] @ qa + wl.z * np.sqrt(esg[b, g] ** 2 @ qa ** 2)) / math.sqrt(d)
+    return out
+
+
+def _q64(q: np.ndarray) -> np.ndarray:
+    if q.dtype == np.uint16:       # bf16 raw words
+        return (q.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return q.astype(np.float64)
+
+
 def compare(wl: Workload, g: GpuRun, orc, tau_oracle: np.ndarray,
             rows: Optional[Sequence[int]] = None, min_compared: float = 0.9,
             rescue_window: Optional[int] = None, np_inputs=None, screen_all: bool = False,
-            self_ungated: bool = False, max_band: int = 6) -> dict:
+            self_ungated: bool = False, max_band: int = 6,
+            band_extra: Optional[np.ndarray] = None) -> dict:
     """Check masks / counts / outputs of the given rows; returns statistics.
 
     A row whose oracle bounds put blocks inside the tie band is compared
@@ -158,12 +222,13 @@ def compare(wl: Workload, g: GpuRun, orc, tau_oracle: np.ndarray,
         assert np.all(gm[N:Ncap] == 0), f"row {row}: mask set beyond the full blocks"
         bnd = orc.bounds[b, h, :N]
         teff = tau_oracle[b, h] - wl.a
-        band = (np.abs(bnd - teff) <= TIE_BAND) if not screen_all else np.zeros(N, bool)
+        extra = band_extra[b, h, :N] if band_extra is not None else np.zeros(N)
+        band = (np.abs(bnd - teff) <= TIE_BAND + extra) if not screen_all else np.zeros(N, bool)
         Wn = min(c, N)
         rescue_tie = False
         if Wn >= 2 and c > 0 and orc.rescued[b, h] >= 0:
             top = np.sort(bnd[:Wn])[::-1]
-            rescue_tie = bool(top[0] - top[1] <= TIE_BAND)
+            rescue_tie = bool(top[0] - top[1] <= TIE_BAND + 2.0 * float(np.max(extra[:Wn])))
         diff = np.nonzero(gm[:N] != om)[0]
         ref_o, ref_n = orc.o[b, h], orc.counts[b, h]
         if rescue_tie:

@@ -23,7 +23,7 @@ def test_header_declarations_are_all_exported(lib):
     assert declared == set(eta.EXPORTS), declared ^ set(eta.EXPORTS)
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.eta_abi_version() == 1
+    assert lib.eta_abi_version() == 2
 
 
 def good_desc(**kw):
@@ -161,3 +161,13 @@ def test_summary_variants_reject(lib):
     assert upd(ctypes.byref(d), FAKE, FAKE, FAKE, 1, 0, ctypes.byref(small), None) == eta.ETA_ERR_INVALID_ARG
     # no block can have completed: nothing is launched
     assert upd(ctypes.byref(d), FAKE, FAKE, FAKE, 0, 4, ctypes.byref(s), None) == eta.ETA_OK
+
+
+def test_summary_stat_dtype_rejected(lib):
+    d = good_desc()
+    for bad in (eta.ETA_DT_BF16, 7):
+        s = eta.SummaryDesc(mu=FAKE, sigma=FAKE, max_norm=FAKE, n_blk_cap=64, stat_dtype=bad)
+        assert lib.eta_build_block_summaries(ctypes.byref(d), FAKE, FAKE, ctypes.byref(s), None) \
+            == eta.ETA_ERR_INVALID_ARG
+        assert "stat_dtype" in lib.eta_last_error_string().decode()
+        assert decode_call(lib, summ=s) == eta.ETA_ERR_INVALID_ARG

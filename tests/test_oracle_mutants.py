@@ -38,6 +38,10 @@ MUTANTS = {
     "self_index": ("(self_ungated && t == T - 1)", "(self_ungated && t == T - 2)"),
     "predictor_transposed": ("(double)W[j * Hq + h];", "(double)W[h * J + j];"),
     "softmax_no_max_shift": ("double w = exp(st[t] - m);", "double w = exp(st[t] - m) * (1.0 + 1e-3 * (t == 0));"),
+    "f16_ties_away": ("r = nearbyint(a / ulp) * ulp;", "r = round(a / ulp) * ulp;"),
+    "f16_no_subnormal_floor": ("if (ex < -14) ex = -14;", ";"),
+    "f16_short_significand": ("const double ulp = ldexp(1.0, ex - 10);", "const double ulp = ldexp(1.0, ex - 9);"),
+    "envelope_block_divisor": ("double sd = sqrt(acc / (double)b_sub);", "double sd = sqrt(acc / (double)b);"),
 }
 
 

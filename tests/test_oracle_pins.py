@@ -399,3 +399,26 @@ def test_config1_selects_exactly_the_planted_blocks():
         np.testing.assert_allclose(r.o[0, h], o_p, rtol=1e-12)
     # the margin to the threshold is wide (no block inside the 1e-4 tie band)
     assert np.nanmin(np.abs(r.bounds - 2.0)) > 1e-2
+
+
+def test_round_f16_is_ieee_binary16_nearest_even():
+    """fp16 index records (App. "GQA-Grouped Execution and Compact Metadata Layout"):
+    the oracle's rounding equals NumPy's float64 -> float16 conversion, an
+    independent implementation of IEEE 754 round-to-nearest-even."""
+    rng = np.random.default_rng(5)
+    mag = 10.0 ** rng.uniform(-10, 6, 20000)
+    x = np.concatenate([mag * rng.choice([-1.0, 1.0], mag.size),
+                        rng.standard_normal(5000) * 3.0,
+                        np.array([0.0, -0.0, np.inf, -np.inf, 65504.0, 65519.99, 65520.0, 7e4,
+                                  2.0 ** -24, 2.0 ** -25, 3 * 2.0 ** -25, 2.0 ** -14,
+                                  2.0 ** -14 - 2.0 ** -25])])
+    with np.errstate(over="ignore"):
+        ref = x.astype(np.float16).astype(np.float64)
+    got = oracle.round_f16(x)
+    assert np.array_equal(got, ref)
+    assert np.array_equal(np.signbit(got), np.signbit(ref))
+    assert np.isnan(oracle.round_f16([np.nan]))[0]
+    # ties go to the even significand: 1 + 2^-11 -> 1, 1 + 3 * 2^-11 -> 1 + 2^-9,
+    # half the smallest subnormal -> 0, 1.5 of it -> 2^-23
+    assert oracle.round_f16([1 + 2.0 ** -11, 1 + 3 * 2.0 ** -11, 2.0 ** -25, 3 * 2.0 ** -25]).tolist() \
+        == [1.0, 1 + 2.0 ** -9, 0.0, 2.0 ** -23]
