@@ -65,6 +65,17 @@ def _load():
     lib.eta_oracle_envelope.restype = None
     lib.eta_oracle_envelope.argtypes = [_vp, ctypes.c_int, ctypes.c_int64, ctypes.c_int64,
                                         ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp]
+    lib.eta_oracle_calib_hist.restype = None
+    lib.eta_oracle_calib_hist.argtypes = [_vp, _vp, ctypes.c_int, _vp, ctypes.c_int, ctypes.c_int,
+                                          ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_double,
+                                          ctypes.c_double, ctypes.c_double, ctypes.c_int,
+                                          ctypes.c_double, ctypes.c_double, _vp, _vp, _vp, _vp, _vp]
+    lib.eta_oracle_calib_g.restype = ctypes.c_double
+    lib.eta_oracle_calib_g.argtypes = [_vp, ctypes.c_int, ctypes.c_double, ctypes.c_double,
+                                       ctypes.c_double, ctypes.c_double]
+    lib.eta_oracle_calib_solve.restype = ctypes.c_double
+    lib.eta_oracle_calib_solve.argtypes = [_vp, ctypes.c_int, ctypes.c_double, ctypes.c_double,
+                                           ctypes.c_double, ctypes.c_double]
     lib.eta_oracle_round_f16.restype = ctypes.c_double
     lib.eta_oracle_round_f16.argtypes = [ctypes.c_double]
     lib.eta_oracle_round_f16_array.restype = None
@@ -301,3 +312,50 @@ def gate_vec(S: np.ndarray, tau: float, beta: float) -> np.ndarray:
     lib = _load()
     return np.array([lib.eta_oracle_gate(float(s), float(tau), float(beta)) for s in np.ravel(S)]
                     ).reshape(np.shape(S))
+
+
+@dataclass
+class CalibResult:
+    hist: np.ndarray      # [Hq][nb] 1/t-weighted counts (not normalised)
+    dens: np.ndarray      # [Hq] sum of gate * weight
+    total: np.ndarray     # [Hq] sum of weights (= sequences x T)
+    hist_lo: Optional[np.ndarray] = None
+    hist_hi: Optional[np.ndarray] = None
+
+    @property
+    def target(self) -> np.ndarray:
+        """Target density of the dynamic thresholds per head."""
+        return self.dens / self.total
+
+
+def calib_hist(q: np.ndarray, k: np.ndarray, tau: np.ndarray, *, beta: float, lo: float, hi: float,
+               nb: int, gamma: float = 0.0, eps_abs: float = 0.0, brackets: bool = False) -> CalibResult:
+    """Accumulation of Alg. "Density-Matched Offline Threshold Calibration" for every head:
+    q [N][Hq][T][d], k [N][Hkv][T][d] (fp32, or bf16 as raw uint16), tau [N][Hq][T]."""
+    q, k = _c(q), _c(k)
+    N, Hq, T, d = q.shape
+    Hkv = k.shape[1]
+    assert k.shape == (N, Hkv, T, d) and Hq % Hkv == 0 and _dtype_code(q) == _dtype_code(k)
+    tau = np.ascontiguousarray(np.asarray(tau, np.float64))
+    assert tau.shape == (N, Hq, T)
+    r = CalibResult(hist=np.zeros((Hq, nb)), dens=np.zeros(Hq), total=np.zeros(Hq))
+    if brackets:
+        r.hist_lo, r.hist_hi = np.zeros((Hq, nb)), np.zeros((Hq, nb))
+    _load().eta_oracle_calib_hist(_ptr(q), _ptr(k), _dtype_code(q), _ptr(tau), N, Hq, Hkv, T, d,
+                                  float(beta), float(lo), float(hi), int(nb), float(gamma),
+                                  float(eps_abs), _ptr(r.hist), _ptr(r.hist_lo), _ptr(r.hist_hi),
+                                  _ptr(r.dens), _ptr(r.total))
+    return r
+
+
+def calib_g(hist: np.ndarray, lo: float, hi: float, beta: float, c: float) -> float:
+    """g(c) = sum_b H_b sigmoid(beta (s_b - c)) over one head's normalised histogram."""
+    h = np.ascontiguousarray(np.asarray(hist, np.float64))
+    return _load().eta_oracle_calib_g(_ptr(h), h.size, float(lo), float(hi), float(beta), float(c))
+
+
+def calib_solve(hist: np.ndarray, lo: float, hi: float, beta: float, target: float) -> float:
+    """Static threshold c of one head: g(c) = target by bisection."""
+    h = np.ascontiguousarray(np.asarray(hist, np.float64))
+    return _load().eta_oracle_calib_solve(_ptr(h), h.size, float(lo), float(hi), float(beta),
+                                          float(target))

@@ -28,6 +28,11 @@
  *       of App. "GQA-Grouped Execution and Compact Metadata Layout",
  *       modelled by rounding the fp64 statistics to the nearest IEEE 754
  *       binary16 value (ties to even) before the bound uses them.
+ *   - offline density-matched calibration of static thresholds: App.
+ *       "Offline Threshold Calibration via 1/t-Weighted Histograms" and Alg.
+ *       "Density-Matched Offline Threshold Calibration": 1/t-weighted score
+ *       histogram, target density of the dynamic gates, bisection of the
+ *       histogram's density function.
  *   - softmax over the attended set: the plain definition (Sec.
  *       "Elastic Threshold Attention", dense attention output), which the
  *       chunked two-stage reduction of the paper reaches exactly.
@@ -402,4 +407,105 @@ int eta_oracle_decode(const eta_oracle_problem* P) {
   free(own_mx);
   free(need);
   return 0;
+}
+
+/*
+ * Offline calibration, accumulation (App. "Offline Threshold Calibration via
+ * 1/t-Weighted Histograms"; Alg. "Density-Matched Offline Threshold
+ * Calibration").  Every calibration sequence x has T steps; at step t
+ * (0-based) the query q_t of head h sees the t + 1 causal keys k_0..k_t of kv
+ * head h / G, and each causal pair weighs 1 / (t + 1) (the paper's 1/t with
+ * steps counted from one).  For each pair:
+ *   S   = <q_t, k_s> / sqrt(d)                       raw score
+ *   bin = floor((S - lo) / w), w = (hi - lo) / nb     clamped to [0, nb)
+ *   hist[h][bin] += 1 / (t + 1);  dens[h] += sigmoid(beta (S - tau[x][h][t])) / (t + 1)
+ * and total[h] sums the weights (N T).  hist_lo / hist_hi (may be NULL) bin
+ * the same pairs at S - delta and S + delta, delta = gamma * sum_i |q_ti k_si|
+ * / sqrt(d) + eps_abs: the interval any computation of S within that error
+ * bound falls into.  Layouts: q [N][Hq][T][d], k [N][Hkv][T][d] (fp32 or bf16
+ * words), tau [N][Hq][T]; outputs [Hq][nb] and [Hq].
+ */
+static int calib_bin(double S, double lo, double w, int nb) {
+  double f = floor((S - lo) / w);
+  if (!(f >= 0.0)) return 0;            /* also NaN */
+  if (f >= (double)nb) return nb - 1;
+  return (int)f;
+}
+
+void eta_oracle_calib_hist(const void* q, const void* k, int dt, const double* tau, int N, int Hq,
+                           int Hkv, int T, int d, double beta, double lo, double hi, int nb,
+                           double gamma, double eps_abs, double* hist, double* hist_lo,
+                           double* hist_hi, double* dens, double* total) {
+  const int G = Hq / Hkv;
+  const double w = (hi - lo) / (double)nb;
+  const double scale = 1.0 / sqrt((double)d);
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int h = 0; h < Hq; ++h) {
+    double* H = hist + (int64_t)h * nb;
+    double* HL = hist_lo ? hist_lo + (int64_t)h * nb : NULL;
+    double* HH = hist_hi ? hist_hi + (int64_t)h * nb : NULL;
+    for (int b = 0; b < nb; ++b) {
+      H[b] = 0.0;
+      if (HL) HL[b] = 0.0;
+      if (HH) HH[b] = 0.0;
+    }
+    double dsum = 0.0, wsum = 0.0;
+    for (int x = 0; x < N; ++x) {
+      const int64_t qb = (((int64_t)x * Hq + h) * T) * d;
+      const int64_t kb = (((int64_t)x * Hkv + h / G) * T) * d;
+      for (int t = 0; t < T; ++t) {
+        const double wt = 1.0 / (double)(t + 1);
+        const double tau_t = tau[((int64_t)x * Hq + h) * T + t];
+        for (int s2 = 0; s2 <= t; ++s2) {
+          double dot = 0.0, mag = 0.0;
+          for (int i = 0; i < d; ++i) {
+            const double a = ld(q, dt, qb + (int64_t)t * d + i);
+            const double c = ld(k, dt, kb + (int64_t)s2 * d + i);
+            dot += a * c;
+            mag += fabs(a * c);
+          }
+          const double S = dot * scale;
+          H[calib_bin(S, lo, w, nb)] += wt;
+          if (HL || HH) {
+            const double delta = gamma * mag * scale + eps_abs;
+            if (HL) HL[calib_bin(S - delta, lo, w, nb)] += wt;
+            if (HH) HH[calib_bin(S + delta, lo, w, nb)] += wt;
+          }
+          dsum += sigmoid(beta * (S - tau_t)) * wt;
+          wsum += wt;
+        }
+      }
+    }
+    dens[h] = dsum;
+    total[h] = wsum;
+  }
+}
+
+/*
+ * The histogram's density function g(c) = sum_b H_b sigmoid(beta (s_b - c)),
+ * H normalised to sum one, s_b = lo + (b + 1/2) w the bin centres.
+ */
+double eta_oracle_calib_g(const double* hist, int nb, double lo, double hi, double beta, double c) {
+  const double w = (hi - lo) / (double)nb;
+  double tot = 0.0, g = 0.0;
+  for (int b = 0; b < nb; ++b) tot += hist[b];
+  for (int b = 0; b < nb; ++b) g += hist[b] * sigmoid(beta * (lo + ((double)b + 0.5) * w - c));
+  return g / tot;
+}
+
+/*
+ * Static threshold c with g(c) = target by bisection (g falls strictly from
+ * one to zero, beta > 0).  Bracket [lo - 60 / beta, hi + 60 / beta]; halves
+ * until the midpoint equals an end; a target outside g's range on the bracket
+ * gives the nearer end.
+ */
+double eta_oracle_calib_solve(const double* hist, int nb, double lo, double hi, double beta,
+                              double target) {
+  double a = lo - 60.0 / beta, b = hi + 60.0 / beta;
+  for (int it = 0; it < 4096; ++it) {
+    const double m = 0.5 * (a + b);
+    if (m <= a || m >= b) break;
+    if (eta_oracle_calib_g(hist, nb, lo, hi, beta, m) > target) a = m; else b = m;
+  }
+  return 0.5 * (a + b);
 }

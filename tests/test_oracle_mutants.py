@@ -42,6 +42,11 @@ MUTANTS = {
     "f16_no_subnormal_floor": ("if (ex < -14) ex = -14;", ";"),
     "f16_short_significand": ("const double ulp = ldexp(1.0, ex - 10);", "const double ulp = ldexp(1.0, ex - 9);"),
     "envelope_block_divisor": ("double sd = sqrt(acc / (double)b_sub);", "double sd = sqrt(acc / (double)b);"),
+    "calib_unweighted": ("const double wt = 1.0 / (double)(t + 1);", "const double wt = 1.0;"),
+    "calib_weight_off_by_one": ("const double wt = 1.0 / (double)(t + 1);", "const double wt = 1.0 / (double)(t + 2);"),
+    "calib_not_causal_diag": ("for (int s2 = 0; s2 <= t; ++s2) {", "for (int s2 = 0; s2 < t || s2 == 0; ++s2) {"),
+    "calib_bin_left_edge": ("g += hist[b] * sigmoid(beta * (lo + ((double)b + 0.5) * w - c));", "g += hist[b] * sigmoid(beta * (lo + (double)b * w - c));"),
+    "calib_bisect_direction": ("if (eta_oracle_calib_g(hist, nb, lo, hi, beta, m) > target) a = m; else b = m;", "if (eta_oracle_calib_g(hist, nb, lo, hi, beta, m) < target) a = m; else b = m;"),
 }
 
 

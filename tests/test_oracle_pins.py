@@ -422,3 +422,87 @@ def test_round_f16_is_ieee_binary16_nearest_even():
     # half the smallest subnormal -> 0, 1.5 of it -> 2^-23
     assert oracle.round_f16([1 + 2.0 ** -11, 1 + 3 * 2.0 ** -11, 2.0 ** -25, 3 * 2.0 ** -25]).tolist() \
         == [1.0, 1 + 2.0 ** -9, 0.0, 2.0 ** -23]
+
+
+# ------------------------------------------------------------- offline calibration
+# App. "Offline Threshold Calibration via 1/t-Weighted Histograms",
+# Alg. "Density-Matched Offline Threshold Calibration".
+
+def _calib_inputs(seed, N=2, Hq=4, Hkv=2, T=40, d=8):
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal((N, Hq, T, d)).astype(np.float32)
+    k = rng.standard_normal((N, Hkv, T, d)).astype(np.float32)
+    return q, k
+
+
+def test_calib_weights_sum_to_steps_and_brackets_order():
+    q, k = _calib_inputs(1)
+    N, Hq, T = q.shape[0], q.shape[1], q.shape[2]
+    tau = np.random.default_rng(2).normal(0.5, 0.3, (N, Hq, T))
+    r = oracle.calib_hist(q, k, tau, beta=4.0, lo=-3.0, hi=3.0, nb=64, gamma=1e-3, brackets=True)
+    # sum over causal pairs of 1 / (steps seen) is one per step: N T per head
+    np.testing.assert_allclose(r.total, N * T, rtol=1e-12)
+    for H in (r.hist, r.hist_lo, r.hist_hi):
+        np.testing.assert_allclose(H.sum(axis=1), N * T, rtol=1e-12)
+    # binning at S - delta moves mass left, at S + delta right: cumulative sums bracket
+    c, cl, ch = (np.cumsum(H, axis=1) for H in (r.hist, r.hist_lo, r.hist_hi))
+    assert np.all(cl >= c - 1e-9) and np.all(c >= ch - 1e-9)
+    assert np.all((r.target > 0) & (r.target < 1))
+
+
+def test_calib_matches_brute_force_definition():
+    """Tiny case, pure-Python loops over the definition of the weighted histogram
+    and of the target density (causal pairs s <= t, weight 1/(t+1))."""
+    q, k = _calib_inputs(3, N=2, Hq=2, Hkv=1, T=6, d=4)
+    tau = np.random.default_rng(4).normal(0.0, 0.5, (2, 2, 6))
+    lo, hi, nb, beta = -2.0, 2.0, 8, 3.0
+    r = oracle.calib_hist(q, k, tau, beta=beta, lo=lo, hi=hi, nb=nb)
+    w = (hi - lo) / nb
+    for h in range(2):
+        H = [0.0] * nb
+        dens = 0.0
+        for x in range(2):
+            for t in range(6):
+                for s in range(t + 1):
+                    S = sum(float(q[x, h, t, i]) * float(k[x, 0, s, i]) for i in range(4)) / 2.0
+                    b = min(max(int(math.floor((S - lo) / w)), 0), nb - 1)
+                    H[b] += 1.0 / (t + 1)
+                    dens += 1.0 / (1.0 + math.exp(-beta * (S - tau[x, h, t]))) / (t + 1)
+        np.testing.assert_allclose(r.hist[h], H, rtol=1e-12, atol=1e-14)
+        assert abs(r.dens[h] - dens) < 1e-12
+
+
+def test_calib_constant_scores_closed_form():
+    """q = 0 makes every score 0: all weight in the bin holding 0, whose centre is
+    s0; with a constant dynamic threshold tau0 the target is sigmoid(-beta tau0),
+    so g(c) = sigmoid(beta (s0 - c)) = target gives c = s0 + tau0 exactly."""
+    q, k = _calib_inputs(5, N=1, Hq=2, Hkv=2, T=10, d=8)
+    q[:] = 0.0
+    lo, hi, nb = -1.0, 1.0, 10           # 0 lies in bin 5, centre 0.1
+    for beta, tau0 in ((4.0, 0.3), (1.5, -0.8), (8.0, 2.0)):
+        tau = np.full((1, 2, 10), tau0)
+        r = oracle.calib_hist(q, k, tau, beta=beta, lo=lo, hi=hi, nb=nb)
+        assert np.all(r.hist[:, 5] == r.total) and np.all(np.delete(r.hist, 5, axis=1) == 0)
+        np.testing.assert_allclose(r.target, 1.0 / (1.0 + math.exp(beta * tau0)), rtol=1e-12)
+        c = oracle.calib_solve(r.hist[0], lo, hi, beta, r.target[0])
+        assert abs(c - (0.1 + tau0)) < 1e-12
+
+
+def test_calib_g_monotone_and_constant_threshold_recovered():
+    """g falls from 1 to 0; calibrating the densities a constant dynamic threshold
+    realises returns that constant to within the bin width; the bisection residual
+    is at rounding level (the paper's < 2e-16)."""
+    q, k = _calib_inputs(6, N=2, Hq=4, Hkv=2, T=48, d=16)
+    lo, hi, nb = -6.0, 6.0, 600
+    for beta, tau0 in ((4.0, 0.7), (2.0, -0.5), (6.0, 1.6)):
+        tau = np.full((2, 4, 48), tau0)
+        r = oracle.calib_hist(q, k, tau, beta=beta, lo=lo, hi=hi, nb=nb)
+        for h in range(4):
+            cs = np.linspace(lo - 10, hi + 10, 200)
+            g = np.array([oracle.calib_g(r.hist[h], lo, hi, beta, c) for c in cs])
+            inner = (g[:-1] > 1e-12) & (g[:-1] < 1 - 1e-12)
+            assert np.all(np.diff(g) <= 0) and np.all(np.diff(g)[inner] < 0)
+            assert g[0] > 1 - 1e-9 and g[-1] < 1e-9
+            c = oracle.calib_solve(r.hist[h], lo, hi, beta, r.target[h])
+            assert abs(c - tau0) <= (hi - lo) / nb, (beta, tau0, h, c)
+            assert abs(oracle.calib_g(r.hist[h], lo, hi, beta, c) - r.target[h]) < 1e-15
