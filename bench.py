@@ -58,6 +58,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline")
+    ap.add_argument("--no-calibration", action="store_true",
+                    help="skip the offline threshold calibration measurement")
     ap.add_argument("--only-primary", action="store_true",
                     help="time only the 20%% survival point (profiling runs)")
     ap.add_argument("--splits", type=int, default=0,
@@ -307,6 +309,36 @@ def main():
     log(f"[bench] fp16 index: {index_f16}")
     del prep16, summ16
 
+    # ---- offline threshold calibration: 16 calibration sequences of 4096 steps at the
+    # ragged workload's head shape (32 query / 8 kv heads, d = 128), 1024 bins
+    calib = None
+    if not args.no_calibration:
+        from synth import calib_stream
+        cN, cHq, cHkv, cT, cd, cnb = 16, 32, 8, 4096, 128, 1024
+        cs = calib_stream(N=cN, Hq=cHq, Hkv=cHkv, T=cT, d=cd, seed=9, device=dev)
+        cal = eta.Calibrator(cHq, cHkv, cd, beta=4.0, lo=-8.0, hi=24.0, num_bins=cnb, device=dev)
+        cal.accumulate(cs.q, cs.k, cs.tau)        # warm-up
+        torch.cuda.synchronize()
+        cal.hist.zero_(); cal.density.zero_()
+        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        e0.record()
+        cal.accumulate(cs.q, cs.k, cs.tau)
+        e1.record()
+        cal.solve()
+        e2.record()
+        torch.cuda.synchronize()
+        acc_ms, solve_ms = e0.elapsed_time(e1), e1.elapsed_time(e2)
+        pairs = cN * cHq * cT * (cT + 1) // 2
+        flops = 2.0 * pairs * cd
+        calib = {"workload": f"{cN} sequences x {cT} steps, {cHq}/{cHkv} heads, d={cd}, bf16, "
+                             f"{cnb} bins",
+                 "accumulate_ms": round(acc_ms, 3), "solve_us": round(solve_ms * 1e3, 1),
+                 "causal_pairs_per_s": round(pairs / acc_ms * 1e3, 1),
+                 "score_tflops": round(flops / acc_ms / 1e9, 1),
+                 "score_frac_of_bf16_mfma_peak": round(flops / acc_ms / 1e9 / 2500.0, 4)}
+        log(f"[bench] calibration: {calib}")
+        del cs, cal
+
     ms, gpu_ms, kt, kv_b, step_b, ub, dh, du, steps, warm, cold_ms = primary
     split_ms, split_n = kt["split_decode"]
     split_avg_ms = split_ms / max(split_n, 1)
@@ -364,6 +396,7 @@ def main():
         "summary_envelope_sub_block": env_sub,
         "summary_update_us_per_step": round(upd_ms * 1e3, 2),
         "index_f16_us_per_step": index_f16,
+        "calibration": calib,
         "roofline": {"bound": "hbm", "kernel": "split_decode", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "algorithmic_bytes_per_launch": kv_b,

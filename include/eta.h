@@ -248,6 +248,64 @@ eta_status_t eta_decode_predicted(const eta_kv_desc_t* kv, int32_t q_dtype, cons
                                   size_t workspace_bytes, void* stream);
 
 /*
+ * Offline density-matched calibration of static per-head thresholds (App.
+ * "Offline Threshold Calibration via 1/t-Weighted Histograms"; Alg.
+ * "Density-Matched Offline Threshold Calibration"): the frozen constants that
+ * replace the predictor (eta_predict_threshold with W = NULL) for a stationary
+ * deployment.  Over calibration sequences of T steps, step t (0-based) of head
+ * h sees the t + 1 causal keys of kv head h / G, and each causal pair (t, s <= t)
+ * weighs 1 / (t + 1).  eta_calib_accumulate adds, per head,
+ *   hist[h][bin(S)]  += 1 / (t + 1),   S = <q_t, k_s> / sqrt(head_dim),
+ *                      bin(S) = floor((S - lo) / w), w = (hi - lo) / num_bins,
+ *                      clamped to [0, num_bins)
+ *   density[h]       += sigmoid(beta (S - tau[x][h][t])) / (t + 1)
+ * in fixed point (units of 2^-40, integer adds, so the sums do not depend on
+ * the order of the adds); eta_calib_solve then finds, per head, the c with
+ *   sum_b H_b sigmoid(beta (s_b - c)) = density / total      (bisection, fp64)
+ * H the normalised histogram, s_b = lo + (b + 1/2) w, total the sum of the
+ * weights (sequences x T).  Scores are computed on the matrix cores from bf16
+ * q and K with fp32 accumulation.
+ */
+typedef struct {
+  int32_t num_seqs;            /* N sequences in this call's q, k, tau */
+  int32_t num_q_heads;
+  int32_t num_kv_heads;        /* num_q_heads / num_kv_heads in {1, 2, 4, 8} */
+  int32_t head_dim;            /* 64 or 128 */
+  int32_t seq_len;             /* T >= 1 steps (= keys) per sequence */
+  int32_t dtype;               /* q and K element type: ETA_DT_BF16 */
+  float beta;                  /* gate inverse temperature, finite, > 0 */
+  float lo, hi;                /* histogram range of raw scores, finite, lo < hi */
+  int32_t num_bins;            /* 1 .. 4096 */
+} eta_calib_desc_t;
+
+/* Accumulators, device memory owned by the caller, zeroed before the first
+ * eta_calib_accumulate; sequences x T per head must stay below 2^23. */
+typedef struct {
+  uint64_t* hist;              /* [num_q_heads][num_bins] */
+  uint64_t* density;           /* [num_q_heads] */
+} eta_calib_state_t;
+
+/*
+ * eta_calib_accumulate -- add N calibration sequences to the accumulators.
+ *   q    bf16 [num_seqs][num_q_heads][seq_len][head_dim] (the query of every step)
+ *   k    bf16 [num_seqs][num_kv_heads][seq_len][head_dim]
+ *   tau  fp32 [num_seqs][num_q_heads][seq_len]  the dynamic thresholds of the steps
+ *        (e.g. eta_predict_threshold over the steps' concatenated queries)
+ * All pointers 16-byte aligned; tensors contiguous.
+ */
+eta_status_t eta_calib_accumulate(const eta_calib_desc_t* cd, const void* q, const void* k,
+                                  const float* tau, const eta_calib_state_t* st, void* stream);
+
+/*
+ * eta_calib_solve -- the static threshold of every head.
+ *   c_out       fp32 [num_q_heads]
+ *   target_out  fp64 [num_q_heads] or NULL: the target density density / total
+ * A head with nothing accumulated gets NaN.
+ */
+eta_status_t eta_calib_solve(const eta_calib_desc_t* cd, const eta_calib_state_t* st,
+                             float* c_out, double* target_out, void* stream);
+
+/*
  * eta_block_bounds -- the screening bound of Eq. (dual_bound_eq) for every
  * full block and query head, as eta_decode computes it, without selecting or
  * attending.  For threshold calibration and diagnostics.
@@ -294,7 +352,9 @@ typedef enum {
   ETA_KERNEL_DENSE_SPLIT = 5,
   ETA_KERNEL_DENSE_COMBINE = 6,
   ETA_KERNEL_BOUNDS = 7,
-  ETA_KERNEL_KINDS = 8
+  ETA_KERNEL_CALIB_ACCUMULATE = 8,
+  ETA_KERNEL_CALIB_SOLVE = 9,
+  ETA_KERNEL_KINDS = 10
 } eta_kernel_kind_t;
 
 typedef struct {

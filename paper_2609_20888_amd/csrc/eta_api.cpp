@@ -367,6 +367,58 @@ eta_status_t eta_decode_predicted(const eta_kv_desc_t* kv, int32_t q_dtype, cons
                      block_mask, head_token_counts, workspace, workspace_bytes, stream);
 }
 
+static eta_status_t check_calib(const eta_calib_desc_t* cd, const eta_calib_state_t* st) {
+  if (!cd || !st) return fail(ETA_ERR_INVALID_ARG, "calibration descriptor or state is NULL");
+  if (cd->num_seqs < 1 || cd->num_seqs > 65535 || cd->seq_len < 1)
+    return fail(ETA_ERR_INVALID_ARG, "num_seqs must be in [1, 65535] and seq_len >= 1");
+  if (cd->num_q_heads < 1 || cd->num_kv_heads < 1 || cd->num_q_heads % cd->num_kv_heads != 0)
+    return fail(ETA_ERR_INVALID_ARG, "num_q_heads must be a positive multiple of num_kv_heads");
+  const int G = cd->num_q_heads / cd->num_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return fail(ETA_ERR_UNSUPPORTED, "GQA group size %d unsupported (1, 2, 4 or 8)", G);
+  if (cd->num_q_heads > 256) return fail(ETA_ERR_UNSUPPORTED, "num_q_heads > 256 unsupported");
+  if (cd->head_dim != 64 && cd->head_dim != 128)
+    return fail(ETA_ERR_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", cd->head_dim);
+  if (cd->dtype != ETA_DT_BF16)
+    return fail(ETA_ERR_UNSUPPORTED, "calibration takes bf16 q and K (dtype %d)", cd->dtype);
+  if (!std::isfinite(cd->beta) || cd->beta <= 0.f)
+    return fail(ETA_ERR_INVALID_ARG, "beta must be finite and > 0");
+  if (!std::isfinite(cd->lo) || !std::isfinite(cd->hi) || !(cd->lo < cd->hi))
+    return fail(ETA_ERR_INVALID_ARG, "histogram range must be finite with lo < hi");
+  if (cd->num_bins < 1 || cd->num_bins > kCalibBinsMax)
+    return fail(ETA_ERR_INVALID_ARG, "num_bins must be in [1, %d]", kCalibBinsMax);
+  if ((int64_t)cd->num_seqs * cd->seq_len >= (int64_t(1) << 23))
+    return fail(ETA_ERR_INVALID_ARG, "num_seqs x seq_len must stay below 2^23 (fixed-point range)");
+  if (!st->hist || !st->density) return fail(ETA_ERR_INVALID_ARG, "accumulators must be non-NULL");
+  if ((reinterpret_cast<uintptr_t>(st->hist) | reinterpret_cast<uintptr_t>(st->density)) & 7u)
+    return fail(ETA_ERR_INVALID_ARG, "accumulators must be 8-byte aligned");
+  return ETA_OK;
+}
+
+eta_status_t eta_calib_accumulate(const eta_calib_desc_t* cd, const void* q, const void* k,
+                                  const float* tau, const eta_calib_state_t* st, void* stream) {
+  eta_status_t s = check_calib(cd, st);
+  if (s) return s;
+  if (!q || !k || !tau) return fail(ETA_ERR_INVALID_ARG, "q, k and tau must be non-NULL");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(tau))
+    return fail(ETA_ERR_INVALID_ARG, "q, k and tau must be 16-byte aligned");
+  hipError_t e = launch_calib(*cd, q, k, tau, *st, (hipStream_t)stream, active_hook());
+  if (e != hipSuccess) return fail(ETA_ERR_HIP, "calibration launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+eta_status_t eta_calib_solve(const eta_calib_desc_t* cd, const eta_calib_state_t* st, float* c_out,
+                             double* target_out, void* stream) {
+  eta_status_t s = check_calib(cd, st);
+  if (s) return s;
+  if (!c_out) return fail(ETA_ERR_INVALID_ARG, "c_out must be non-NULL");
+  if ((reinterpret_cast<uintptr_t>(c_out) & 3u) || (reinterpret_cast<uintptr_t>(target_out) & 7u))
+    return fail(ETA_ERR_INVALID_ARG, "c_out / target_out misaligned");
+  hipError_t e = launch_calib_solve(*cd, *st, c_out, target_out, (hipStream_t)stream, active_hook());
+  if (e != hipSuccess) return fail(ETA_ERR_HIP, "calibration solve launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 eta_status_t eta_block_bounds(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q,
                               const int32_t* seq_lens, const eta_summary_t* summ, float z,
                               float* bounds, void* stream) {

@@ -1284,6 +1284,163 @@ __global__ __launch_bounds__(256) void split_kernel(SplitArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- calibration
+//
+// Offline density-matched calibration.  calib_kernel: one workgroup per
+// (query head, sequence); wavefront w takes the 16-query groups w, w + 4, ...
+// and, for each, the 16-key blocks 0 .. group (the causal triangle).  Scores
+// come from v_mfma_f32_16x16x32_bf16 in the standard layout: A = 16 query rows
+// x 32 dims, B = 32 dims x 16 keys, so lane l gets the scores of queries
+// 4 (l >> 4) + i of the group and key l & 15 of the block.  Each causal score
+// adds its step's weight round(2^40 / (t + 1)) to an LDS histogram with a
+// 64-bit integer atomic; the lane's gate sum sigmoid(beta (S - tau_t)) / (t + 1)
+// accumulates in fp64 in a fixed order and is added once, rounded to the same
+// fixed point.  Integer sums make the result independent of the adds' order.
+// calib_solve_kernel: one workgroup per head, fp64 bisection of the
+// histogram's density function with fixed-order block reductions.
+
+constexpr int kCalibMaxBins = 4096;
+constexpr double kCalibUnit = 1099511627776.0;   // 2^40
+
+struct CalibArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const float* tau;
+  unsigned long long* hist;
+  unsigned long long* dens;
+  int Hq, Hkv, T, nb;
+  float beta, lo, inv_w;
+};
+
+template <int D>
+__global__ __launch_bounds__(256) void calib_kernel(CalibArgs a) {
+  constexpr int KC = D / 32;                      // 32-dim chunks
+  __shared__ unsigned long long hist_s[kCalibMaxBins];
+  const int h = blockIdx.x, x = blockIdx.y, tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
+  const int G = a.Hq / a.Hkv;
+  for (int b = tid; b < a.nb; b += 256) hist_s[b] = 0ull;
+  __syncthreads();
+  const uint16_t* qh = a.q + (((int64_t)x * a.Hq + h) * a.T) * D;
+  const uint16_t* kh = a.k + (((int64_t)x * a.Hkv + h / G) * a.T) * D;
+  const float* tauh = a.tau + ((int64_t)x * a.Hq + h) * a.T;
+  const float scale = 1.0f / sqrtf((float)D);
+  const int ngroups = (a.T + 15) / 16;
+  const int r16 = lane & 15, g4 = lane >> 4;
+  double dens = 0.0;
+  for (int qg = w; qg < ngroups; qg += 4) {
+    // A: query row 16 qg + r16, dims 32 kc + 8 g4 .. + 7 (rows past T read row T - 1)
+    const int qr = min(16 * qg + r16, a.T - 1);
+    bf16x8 qa[KC];
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc)
+      qa[kc] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(qh + (int64_t)qr * D + 32 * kc + 8 * g4));
+    // this lane's output rows: steps t_i = 16 qg + 4 g4 + i
+    int t_i[4];
+    float tau_i[4], invt_i[4];
+    unsigned long long wt_i[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      t_i[i] = 16 * qg + 4 * g4 + i;
+      const int tc = min(t_i[i], a.T - 1);
+      tau_i[i] = tauh[tc];
+      invt_i[i] = 1.0f / (float)(t_i[i] + 1);
+      wt_i[i] = (unsigned long long)llrint(kCalibUnit / (double)(t_i[i] + 1));
+    }
+    for (int kb = 0; kb <= qg; ++kb) {
+      const int kr = min(16 * kb + r16, a.T - 1);
+      bf16x8 kk[KC];
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc)
+        kk[kc] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kh + (int64_t)kr * D + 32 * kc + 8 * g4));
+      f32x4 c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc) c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kc], kk[kc], c, 0, 0, 0);
+      const int s_idx = 16 * kb + r16;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (s_idx <= t_i[i] && t_i[i] < a.T) {
+          const float S = c[i] * scale;
+          float f = floorf((S - a.lo) * a.inv_w);
+          f = f >= 0.f ? f : 0.f;        // also NaN
+          const int bin = f < (float)a.nb ? (int)f : a.nb - 1;
+          atomicAdd(&hist_s[bin], wt_i[i]);
+          const float gate = 1.0f / (1.0f + __expf(-a.beta * (S - tau_i[i])));
+          dens += (double)(gate * invt_i[i]);
+        }
+      }
+    }
+  }
+  // the lane's gate sum in fixed point; integer wavefront sum; one global add
+  unsigned long long dv = (unsigned long long)llrint(dens * kCalibUnit);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) dv += __shfl_xor(dv, o, 64);
+  if (lane == 0) atomicAdd(&a.dens[h], dv);
+  __syncthreads();
+  for (int b = tid; b < a.nb; b += 256) {
+    const unsigned long long v = hist_s[b];
+    if (v != 0ull) atomicAdd(&a.hist[(int64_t)h * a.nb + b], v);
+  }
+}
+
+__device__ __forceinline__ double sigmoid_f64(double x) {
+  if (x >= 0.0) return 1.0 / (1.0 + exp(-x));
+  const double e = exp(x);
+  return e / (1.0 + e);
+}
+
+__device__ __forceinline__ double block_sum_f64(double x, double* red) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  if (lane == 0) red[w] = x;
+  __syncthreads();
+  const double r = ((red[0] + red[1]) + red[2]) + red[3];
+  __syncthreads();
+  return r;
+}
+
+struct CalibSolveArgs {
+  const unsigned long long* hist;
+  const unsigned long long* dens;
+  float* c_out;
+  double* target_out;
+  int nb;
+  double beta, lo, hi;
+};
+
+__global__ __launch_bounds__(256) void calib_solve_kernel(CalibSolveArgs a) {
+  constexpr int PER = kCalibMaxBins / 256;
+  __shared__ double red[4];
+  const int h = blockIdx.x, tid = threadIdx.x;
+  const double w = (a.hi - a.lo) / (double)a.nb;
+  double hb[PER], sb[PER];
+  double tot = 0.0;
+#pragma unroll
+  for (int r = 0; r < PER; ++r) {
+    const int b = tid + 256 * r;
+    hb[r] = b < a.nb ? (double)a.hist[(int64_t)h * a.nb + b] : 0.0;
+    sb[r] = a.lo + ((double)b + 0.5) * w;
+    tot += hb[r];
+  }
+  tot = block_sum_f64(tot, red);
+  const double target = (double)a.dens[h] / tot;
+  double lo = a.lo - 60.0 / a.beta, hi = a.hi + 60.0 / a.beta;
+  for (int it = 0; it < 2048; ++it) {
+    const double m = 0.5 * (lo + hi);
+    if (m <= lo || m >= hi) break;
+    double g = 0.0;
+#pragma unroll
+    for (int r = 0; r < PER; ++r) g += hb[r] * sigmoid_f64(a.beta * (sb[r] - m));
+    g = block_sum_f64(g, red) / tot;
+    if (g > target) lo = m; else hi = m;
+  }
+  if (tid == 0) {
+    a.c_out[h] = tot > 0.0 ? (float)(0.5 * (lo + hi)) : __builtin_nanf("");
+    if (a.target_out != nullptr) a.target_out[h] = tot > 0.0 ? target : __builtin_nan("");
+  }
+}
+
 // ---------------------------------------------------------------- combine
 
 struct CombineArgs {
@@ -1512,6 +1669,30 @@ hipError_t launch_bounds(const Geom& g, int q_dtype, const void* q, const int32_
                 0, 0, 0};
   return with_hook(hook, ETA_KERNEL_BOUNDS, stream,
                    [&] { launch_screen_impl<true>(g, sa, stream); });
+}
+
+hipError_t launch_calib(const eta_calib_desc_t& cd, const void* q, const void* k, const float* tau,
+                        const eta_calib_state_t& st, hipStream_t stream, LaunchHook hook) {
+  CalibArgs ca{reinterpret_cast<const uint16_t*>(q), reinterpret_cast<const uint16_t*>(k), tau,
+               reinterpret_cast<unsigned long long*>(st.hist),
+               reinterpret_cast<unsigned long long*>(st.density), cd.num_q_heads, cd.num_kv_heads,
+               cd.seq_len, cd.num_bins, cd.beta, cd.lo,
+               (float)((double)cd.num_bins / ((double)cd.hi - (double)cd.lo))};
+  dim3 grid(cd.num_q_heads, cd.num_seqs);
+  return with_hook(hook, ETA_KERNEL_CALIB_ACCUMULATE, stream, [&] {
+    if (cd.head_dim == 64) hipLaunchKernelGGL(calib_kernel<64>, grid, dim3(256), 0, stream, ca);
+    if (cd.head_dim == 128) hipLaunchKernelGGL(calib_kernel<128>, grid, dim3(256), 0, stream, ca);
+  });
+}
+
+hipError_t launch_calib_solve(const eta_calib_desc_t& cd, const eta_calib_state_t& st, float* c_out,
+                              double* target_out, hipStream_t stream, LaunchHook hook) {
+  CalibSolveArgs sa{reinterpret_cast<const unsigned long long*>(st.hist),
+                    reinterpret_cast<const unsigned long long*>(st.density), c_out, target_out,
+                    cd.num_bins, (double)cd.beta, (double)cd.lo, (double)cd.hi};
+  return with_hook(hook, ETA_KERNEL_CALIB_SOLVE, stream, [&] {
+    hipLaunchKernelGGL(calib_solve_kernel, dim3(cd.num_q_heads), dim3(256), 0, stream, sa);
+  });
 }
 
 hipError_t launch_dense(const Geom& g, int S, int q_dtype, const void* q, const void* k,

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libeta.so")
 ETA_OK, ETA_ERR_INVALID_ARG, ETA_ERR_UNSUPPORTED, ETA_ERR_WORKSPACE, ETA_ERR_HIP = range(5)
 ETA_DT_F32, ETA_DT_BF16, ETA_DT_F16 = 0, 1, 2
 KERNEL_KINDS = ("summaries", "predict", "screen", "split_decode", "combine", "dense_split",
-                "dense_combine", "bounds")
+                "dense_combine", "bounds", "calib_accumulate", "calib_solve")
 
 _vp = ctypes.c_void_p
 
@@ -39,6 +39,17 @@ class SummaryDesc(ctypes.Structure):
                 ("stat_dtype", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
+class CalibDesc(ctypes.Structure):
+    _fields_ = [("num_seqs", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("seq_len", ctypes.c_int32), ("dtype", ctypes.c_int32), ("beta", ctypes.c_float),
+                ("lo", ctypes.c_float), ("hi", ctypes.c_float), ("num_bins", ctypes.c_int32)]
+
+
+class CalibState(ctypes.Structure):
+    _fields_ = [("hist", _vp), ("density", _vp)]
+
+
 class DecodeParams(ctypes.Structure):
     _fields_ = [("beta", ctypes.c_float), ("z", ctypes.c_float), ("offset_a", ctypes.c_float),
                 ("rescue_window_blocks", ctypes.c_int32), ("pin_recent_blocks", ctypes.c_int32),
@@ -54,6 +65,7 @@ class KernelTime(ctypes.Structure):
 EXPORTS = ("eta_build_block_summaries", "eta_build_block_summaries_envelope",
            "eta_update_block_summaries", "eta_predict_threshold", "eta_decode_workspace_size",
            "eta_decode", "eta_decode_predicted", "eta_block_bounds", "eta_dense_workspace_size", "eta_dense_decode",
+           "eta_calib_accumulate", "eta_calib_solve",
            "eta_last_error_string", "eta_abi_version", "eta_profile_begin", "eta_profile_end")
 
 
@@ -81,6 +93,8 @@ def load_library(path: Optional[str] = None):
     sz = ctypes.c_size_t
     sigs = {
         "eta_build_block_summaries": [P(KvDesc), _vp, _vp, P(SummaryDesc), _vp],
+        "eta_calib_accumulate": [P(CalibDesc), _vp, _vp, _vp, P(CalibState), _vp],
+        "eta_calib_solve": [P(CalibDesc), P(CalibState), _vp, _vp, _vp],
         "eta_build_block_summaries_envelope": [P(KvDesc), _vp, _vp, i32, P(SummaryDesc), _vp],
         "eta_update_block_summaries": [P(KvDesc), _vp, _vp, _vp, i32, i32, P(SummaryDesc), _vp],
         "eta_predict_threshold": [i32, i32, i32, i32, _vp, _vp, _vp, _vp, _vp],
@@ -373,3 +387,48 @@ def profile_end() -> dict:
     arr = (KernelTime * len(KERNEL_KINDS))()
     _check(load_library().eta_profile_end(arr))
     return {name: (arr[i].ms_total, arr[i].launches) for i, name in enumerate(KERNEL_KINDS)}
+
+
+CALIB_UNIT = float(2 ** 40)   # fixed-point unit of the calibration accumulators
+
+
+class Calibrator:
+    """Offline density-matched calibration of static per-head thresholds
+    (eta_calib_accumulate / eta_calib_solve).  The accumulators live on the
+    device; ``accumulate`` may be called for any number of batches of
+    calibration sequences, ``solve`` returns the constants (usable as the
+    ``bias`` of a predictor-free decode, W = None)."""
+
+    def __init__(self, num_q_heads: int, num_kv_heads: int, head_dim: int, *, beta: float,
+                 lo: float, hi: float, num_bins: int, device):
+        self.Hq, self.Hkv, self.d = num_q_heads, num_kv_heads, head_dim
+        self.beta, self.lo, self.hi, self.nb = float(beta), float(lo), float(hi), int(num_bins)
+        self.hist = torch.zeros(num_q_heads, num_bins, dtype=torch.int64, device=device)
+        self.density = torch.zeros(num_q_heads, dtype=torch.int64, device=device)
+
+    def _desc(self, N: int, T: int) -> CalibDesc:
+        return CalibDesc(num_seqs=N, num_q_heads=self.Hq, num_kv_heads=self.Hkv, head_dim=self.d,
+                         seq_len=T, dtype=ETA_DT_BF16, beta=self.beta, lo=self.lo, hi=self.hi,
+                         num_bins=self.nb)
+
+    def _state(self) -> CalibState:
+        return CalibState(hist=_ptr(self.hist), density=_ptr(self.density))
+
+    def accumulate(self, q: torch.Tensor, k: torch.Tensor, tau: torch.Tensor, stream=None):
+        """q bf16 [N][Hq][T][d], k bf16 [N][Hkv][T][d], tau fp32 [N][Hq][T] (contiguous)."""
+        N, Hq, T, d = q.shape
+        assert (Hq, d) == (self.Hq, self.d) and k.shape == (N, self.Hkv, T, d)
+        assert tau.shape == (N, Hq, T) and tau.dtype == torch.float32
+        assert q.is_contiguous() and k.is_contiguous() and tau.is_contiguous()
+        desc, st = self._desc(N, T), self._state()
+        _check(load_library().eta_calib_accumulate(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(tau),
+                                                   ctypes.byref(st), _stream(stream)))
+
+    def solve(self, stream=None):
+        """(c fp32 [Hq], target density fp64 [Hq])."""
+        c = torch.empty(self.Hq, dtype=torch.float32, device=self.hist.device)
+        target = torch.empty(self.Hq, dtype=torch.float64, device=self.hist.device)
+        desc, st = self._desc(1, 1), self._state()
+        _check(load_library().eta_calib_solve(ctypes.byref(desc), ctypes.byref(st), _ptr(c),
+                                              _ptr(target), _stream(stream)))
+        return c, target

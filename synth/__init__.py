@@ -257,3 +257,40 @@ def as_numpy(t: torch.Tensor) -> np.ndarray:
     if t.dtype == torch.float32:
         return t.numpy()
     raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+@dataclass
+class CalibStream:
+    """Calibration split for the offline threshold calibration: N sequences of T
+    steps, the query of every step, the keys, and the dynamic thresholds the
+    deployed predictor produced at each step."""
+    q: torch.Tensor      # bf16 [N][Hq][T][d]
+    k: torch.Tensor      # bf16 [N][Hkv][T][d]
+    tau: torch.Tensor    # fp32 [N][Hq][T]
+
+
+def calib_stream(*, N: int, Hq: int, Hkv: int, T: int, d: int, seed: int = 0,
+                 tau_mean=(0.5, 2.0), tau_std: float = 0.3, planted_frac: float = 0.05,
+                 tau_const: Optional[Sequence[float]] = None, device="cpu") -> CalibStream:
+    """q, k ~ N(0, 1) in fp32 rounded to bf16; a fraction of keys planted along the
+    group's mean query direction (3 sqrt(d) u + N(0, 1)) so the score stream has a
+    right tail; per-head dynamic thresholds N(mu_h, tau_std) per step with mu_h
+    spread over tau_mean, or exactly tau_const[h] at every step."""
+    # large streams are drawn on the device (its own seeded generator)
+    gdev = torch.device(device) if N * Hq * T * d > (1 << 26) else torch.device("cpu")
+    gen = torch.Generator(device=gdev).manual_seed(seed)
+    q = torch.randn(N, Hq, T, d, generator=gen, device=gdev)
+    k = torch.randn(N, Hkv, T, d, generator=gen, device=gdev)
+    G = Hq // Hkv
+    u = q.view(N, Hkv, G, T, d).sum(dim=(2, 3))
+    u = u / u.norm(dim=-1, keepdim=True)
+    plant = torch.rand(N, Hkv, T, generator=gen, device=gdev) < planted_frac
+    k = torch.where(plant[..., None], 3.0 * math.sqrt(d) * u[:, :, None, :] + k, k)
+    if tau_const is not None:
+        tau = torch.tensor(list(tau_const), dtype=torch.float32,
+                           device=gdev)[None, :, None].expand(N, Hq, T)
+    else:
+        mu = torch.linspace(tau_mean[0], tau_mean[1], Hq, device=gdev)
+        tau = mu[None, :, None] + tau_std * torch.randn(N, Hq, T, generator=gen, device=gdev)
+    return CalibStream(q=q.to(torch.bfloat16).to(device), k=k.to(torch.bfloat16).to(device),
+                       tau=tau.to(torch.float32).contiguous().to(device))

@@ -171,3 +171,29 @@ def test_summary_stat_dtype_rejected(lib):
             == eta.ETA_ERR_INVALID_ARG
         assert "stat_dtype" in lib.eta_last_error_string().decode()
         assert decode_call(lib, summ=s) == eta.ETA_ERR_INVALID_ARG
+
+
+def test_calibration_rejects(lib):
+    def desc(**kw):
+        d = dict(num_seqs=2, num_q_heads=8, num_kv_heads=2, head_dim=128, seq_len=256,
+                 dtype=eta.ETA_DT_BF16, beta=4.0, lo=-4.0, hi=4.0, num_bins=512)
+        d.update(kw)
+        return eta.CalibDesc(**d)
+    st = eta.CalibState(hist=FAKE, density=FAKE)
+    acc = lambda cd, s=st, q=FAKE, k=FAKE, t=FAKE: lib.eta_calib_accumulate(
+        ctypes.byref(cd), q, k, t, ctypes.byref(s), None)
+    bad = [(dict(num_seqs=0), eta.ETA_ERR_INVALID_ARG), (dict(seq_len=0), eta.ETA_ERR_INVALID_ARG),
+           (dict(num_kv_heads=3), eta.ETA_ERR_INVALID_ARG), (dict(num_kv_heads=1, num_q_heads=16), eta.ETA_ERR_UNSUPPORTED),
+           (dict(head_dim=96), eta.ETA_ERR_UNSUPPORTED), (dict(dtype=eta.ETA_DT_F32), eta.ETA_ERR_UNSUPPORTED),
+           (dict(beta=0.0), eta.ETA_ERR_INVALID_ARG), (dict(beta=float("nan")), eta.ETA_ERR_INVALID_ARG),
+           (dict(lo=1.0, hi=1.0), eta.ETA_ERR_INVALID_ARG), (dict(hi=float("inf")), eta.ETA_ERR_INVALID_ARG),
+           (dict(num_bins=0), eta.ETA_ERR_INVALID_ARG), (dict(num_bins=4097), eta.ETA_ERR_INVALID_ARG),
+           (dict(num_seqs=64, seq_len=1 << 17), eta.ETA_ERR_INVALID_ARG)]
+    for kw, code in bad:
+        assert acc(desc(**kw)) == code, kw
+    assert acc(desc(), q=None) == eta.ETA_ERR_INVALID_ARG
+    assert acc(desc(), t=FAKE + 4) == eta.ETA_ERR_INVALID_ARG
+    assert acc(desc(), s=eta.CalibState(hist=None, density=FAKE)) == eta.ETA_ERR_INVALID_ARG
+    assert acc(desc(), s=eta.CalibState(hist=FAKE + 4, density=FAKE)) == eta.ETA_ERR_INVALID_ARG
+    assert lib.eta_calib_solve(ctypes.byref(desc()), ctypes.byref(st), None, None, None) \
+        == eta.ETA_ERR_INVALID_ARG
