@@ -76,6 +76,10 @@ def _load():
     lib.eta_oracle_calib_solve.restype = ctypes.c_double
     lib.eta_oracle_calib_solve.argtypes = [_vp, ctypes.c_int, ctypes.c_double, ctypes.c_double,
                                            ctypes.c_double, ctypes.c_double]
+    lib.eta_oracle_prefill.restype = None
+    lib.eta_oracle_prefill.argtypes = [_vp, _vp, _vp, ctypes.c_int, _vp, _vp, ctypes.c_int,
+                                       ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                       ctypes.c_double, ctypes.c_int, ctypes.c_double, _vp, _vp, _vp]
     lib.eta_oracle_round_f16.restype = ctypes.c_double
     lib.eta_oracle_round_f16.argtypes = [ctypes.c_double]
     lib.eta_oracle_round_f16_array.restype = None
@@ -359,3 +363,29 @@ def calib_solve(hist: np.ndarray, lo: float, hi: float, beta: float, target: flo
     h = np.ascontiguousarray(np.asarray(hist, np.float64))
     return _load().eta_oracle_calib_solve(_ptr(h), h.size, float(lo), float(hi), float(beta),
                                           float(target))
+
+
+@dataclass
+class PrefillResult:
+    o: np.ndarray     # [B][Hq][T][d]
+    r: np.ndarray     # [B][Hq][T]  sum of the gates over the causal keys
+    lse: np.ndarray   # [B][Hq][T]  log-sum-exp of the gated scores
+
+
+def prefill(q: np.ndarray, k: np.ndarray, v: np.ndarray, tau: np.ndarray, seq_lens: Sequence[int],
+            *, beta: float, additive: bool = False, C: float = 0.0) -> PrefillResult:
+    """Gated prefill / training forward of App. "Hardware-Aligned Forward Kernel":
+    q [B][Hq][T][d], k, v [B][Hkv][T][d] (fp32, or bf16 as raw uint16), tau [B][Hq][T]."""
+    q, k, v = _c(q), _c(k), _c(v)
+    B, Hq, T, d = q.shape
+    Hkv = k.shape[1]
+    assert k.shape == (B, Hkv, T, d) and v.shape == k.shape and Hq % Hkv == 0
+    assert _dtype_code(q) == _dtype_code(k) == _dtype_code(v)
+    tau = np.ascontiguousarray(np.asarray(tau, np.float64))
+    assert tau.shape == (B, Hq, T)
+    sl = np.ascontiguousarray(np.asarray(seq_lens, np.int32))
+    r = PrefillResult(o=np.zeros((B, Hq, T, d)), r=np.zeros((B, Hq, T)), lse=np.zeros((B, Hq, T)))
+    _load().eta_oracle_prefill(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), _ptr(tau), _ptr(sl), B, Hq,
+                               Hkv, T, d, float(beta), int(bool(additive)), float(C), _ptr(r.o),
+                               _ptr(r.r), _ptr(r.lse))
+    return r

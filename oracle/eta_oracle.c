@@ -33,6 +33,11 @@
  *       "Density-Matched Offline Threshold Calibration": 1/t-weighted score
  *       histogram, target density of the dynamic gates, bisection of the
  *       histogram's density function.
+ *   - gated prefill / training forward: App. "Hardware-Aligned Forward
+ *       Kernel" (Alg. fwd_kernel) -- causal scores, gates sigmoid(beta (S -
+ *       tau_i)) and their row sums R_i, multiplicative (S sigma) or additive
+ *       (S + C sigma - C) masking with the diagonal ungated, softmax output
+ *       and log-sum-exp, from the definitions (no blocking).
  *   - softmax over the attended set: the plain definition (Sec.
  *       "Elastic Threshold Attention", dense attention output), which the
  *       chunked two-stage reduction of the paper reaches exactly.
@@ -508,4 +513,65 @@ double eta_oracle_calib_solve(const double* hist, int nb, double lo, double hi, 
     if (eta_oracle_calib_g(hist, nb, lo, hi, beta, m) > target) a = m; else b = m;
   }
   return 0.5 * (a + b);
+}
+
+/*
+ * Gated prefill / training forward (App. "Hardware-Aligned Forward Kernel"):
+ * for every sequence b, query head h (kv head h / G) and position i < T_b,
+ * over the causal keys j <= i:
+ *   S_ij     = s <q_i, k_j>,  s = 1 / sqrt(d)
+ *   sigma_ij = sigmoid(beta (S_ij - tau_i)),     R_i = sum_{j <= i} sigma_ij
+ *   S~_ij    = S_ij sigma_ij (multiplicative) or S_ij + C sigma_ij - C
+ *              (additive); S~_ii = S_ii (the diagonal is never gated)
+ *   O_i      = sum_j exp(S~_ij - L_i) v_j,  L_i = log sum_j exp(S~_ij)
+ * Layouts q, O [B][Hq][T][d], k, v [B][Hkv][T][d] (fp32 or bf16 words),
+ * tau, R, L [B][Hq][T].  Rows i >= T_b: O = 0, R = 0, L = -inf.
+ */
+void eta_oracle_prefill(const void* q, const void* k, const void* v, int dt, const double* tau,
+                        const int32_t* seq_lens, int B, int Hq, int Hkv, int T, int d, double beta,
+                        int additive, double C, double* O, double* R, double* L) {
+  const int G = Hq / Hkv;
+  const double scale = 1.0 / sqrt((double)d);
+#pragma omp parallel for collapse(2) schedule(dynamic, 1)
+  for (int b = 0; b < B; ++b) {
+    for (int h = 0; h < Hq; ++h) {
+      const int Tb = seq_lens[b] < 0 ? 0 : (seq_lens[b] > T ? T : seq_lens[b]);
+      const int64_t qb = (((int64_t)b * Hq + h) * T) * d;
+      const int64_t kb = (((int64_t)b * Hkv + h / G) * T) * d;
+      double* st = (double*)malloc(sizeof(double) * (size_t)(T > 0 ? T : 1));
+      for (int i = 0; i < T; ++i) {
+        const int64_t row = ((int64_t)b * Hq + h) * T + i;
+        double* o = O + row * d;
+        for (int c = 0; c < d; ++c) o[c] = 0.0;
+        if (i >= Tb) {
+          R[row] = 0.0;
+          L[row] = -INFINITY;
+          continue;
+        }
+        double rsum = 0.0, m = -INFINITY;
+        for (int j = 0; j <= i; ++j) {
+          double dot = 0.0;
+          for (int c = 0; c < d; ++c)
+            dot += ld(q, dt, qb + (int64_t)i * d + c) * ld(k, dt, kb + (int64_t)j * d + c);
+          const double S = dot * scale;
+          const double g = sigmoid(beta * (S - tau[row]));
+          rsum += g;
+          double Sg = additive ? S + C * g - C : S * g;
+          if (j == i) Sg = S;
+          st[j] = Sg;
+          if (Sg > m) m = Sg;
+        }
+        double l = 0.0;
+        for (int j = 0; j <= i; ++j) {
+          const double w = exp(st[j] - m);
+          l += w;
+          for (int c = 0; c < d; ++c) o[c] += w * ld(v, dt, kb + (int64_t)j * d + c);
+        }
+        for (int c = 0; c < d; ++c) o[c] /= l;
+        R[row] = rsum;
+        L[row] = m + log(l);
+      }
+      free(st);
+    }
+  }
 }

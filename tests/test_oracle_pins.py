@@ -506,3 +506,100 @@ def test_calib_g_monotone_and_constant_threshold_recovered():
             c = oracle.calib_solve(r.hist[h], lo, hi, beta, r.target[h])
             assert abs(c - tau0) <= (hi - lo) / nb, (beta, tau0, h, c)
             assert abs(oracle.calib_g(r.hist[h], lo, hi, beta, c) - r.target[h]) < 1e-15
+
+
+# ------------------------------------------------------------- gated prefill forward
+# App. "Hardware-Aligned Forward Kernel" (Alg. fwd_kernel).
+
+def _prefill_inputs(seed, B=2, Hq=4, Hkv=2, T=24, d=16):
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal((B, Hq, T, d)).astype(np.float32)
+    k = rng.standard_normal((B, Hkv, T, d)).astype(np.float32)
+    v = rng.standard_normal((B, Hkv, T, d)).astype(np.float32)
+    return q, k, v
+
+
+def _expand_kv(x, G):
+    return np.repeat(x, G, axis=1)
+
+
+def test_prefill_ungated_is_causal_softmax_attention():
+    """tau = -inf: every gate is 1, so O is causal softmax attention (torch SDPA in
+    fp64), L its log-sum-exp, R_i = i + 1; rows past a sequence's length are empty."""
+    q, k, v = _prefill_inputs(11)
+    B, Hq, T, d = q.shape
+    G = Hq // k.shape[1]
+    r = oracle.prefill(q, k, v, np.full((B, Hq, T), -np.inf), [T, 17], beta=4.0)
+    qt = torch.tensor(q, dtype=torch.float64)
+    kt = torch.tensor(_expand_kv(k, G), dtype=torch.float64)
+    vt = torch.tensor(_expand_kv(v, G), dtype=torch.float64)
+    ref = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, is_causal=True).numpy()
+    S = (qt @ kt.transpose(-1, -2)) / math.sqrt(d)
+    S = S.masked_fill(torch.triu(torch.ones(T, T, dtype=torch.bool), 1), float("-inf"))
+    lse = torch.logsumexp(S, dim=-1).numpy()
+    np.testing.assert_allclose(r.o[0], ref[0], atol=1e-12)
+    np.testing.assert_allclose(r.lse[0], lse[0], atol=1e-12)
+    np.testing.assert_allclose(r.o[1, :, :17], ref[1, :, :17], atol=1e-12)
+    np.testing.assert_array_equal(r.r[0], np.broadcast_to(np.arange(1, T + 1), (Hq, T)))
+    assert np.all(r.o[1, :, 17:] == 0) and np.all(np.isneginf(r.lse[1, :, 17:]))
+    assert np.all(r.r[1, :, 17:] == 0)
+
+
+def test_prefill_closed_gates_leave_only_the_diagonal():
+    """tau = +inf: every gate is 0.  Multiplicative: S~ = 0 off the diagonal and S_ii on
+    it, so O_i = (sum_{j<i} v_j + e^{S_ii} v_i) / (i + e^{S_ii}).  Additive with C:
+    S~ = S - C off the diagonal.  R = 0."""
+    q, k, v = _prefill_inputs(12, B=1, Hq=2, Hkv=1, T=12, d=8)
+    T, d = 12, 8
+    tau = np.full((1, 2, T), np.inf)
+    r = oracle.prefill(q, k, v, tau, [T], beta=3.0)
+    ra = oracle.prefill(q, k, v, tau, [T], beta=3.0, additive=True, C=2.5)
+    kv, vv = k[0, 0].astype(np.float64), v[0, 0].astype(np.float64)
+    for h in range(2):
+        qq = q[0, h].astype(np.float64)
+        for i in range(T):
+            sii = float(qq[i] @ kv[i]) / math.sqrt(d)
+            e = math.exp(sii)
+            want = (vv[:i].sum(axis=0) + e * vv[i]) / (i + e)
+            np.testing.assert_allclose(r.o[0, h, i], want, atol=1e-12)
+            s = np.array([float(qq[i] @ kv[j]) / math.sqrt(d) - 2.5 for j in range(i)] + [sii])
+            w = np.exp(s - s.max())
+            np.testing.assert_allclose(ra.o[0, h, i], (w[:, None] * vv[:i + 1]).sum(0) / w.sum(),
+                                       atol=1e-12)
+    assert np.all(r.r == 0)
+
+
+def test_prefill_last_row_is_dense_gated_decode():
+    """The prefill's last row is the decode step at the same position over every
+    key with the gate (screen_all) and the diagonal bypass (self_ungated): two
+    independently written routines of the oracle."""
+    q, k, v = _prefill_inputs(13, B=2, Hq=4, Hkv=2, T=64, d=16)
+    tau = np.random.default_rng(14).normal(0.3, 0.5, (2, 4, 64))
+    r = oracle.prefill(q, k, v, tau, [64, 64], beta=4.0)
+    dec = oracle.decode(np.ascontiguousarray(q[:, :, -1]), k, v, [64, 64], tau[:, :, -1],
+                        block_size=16, beta=4.0, z=1.0, rescue_window=0, screen_all=True,
+                        self_ungated=True)
+    np.testing.assert_allclose(r.o[:, :, -1], dec.o, atol=1e-12)
+    np.testing.assert_allclose(r.lse[:, :, -1], dec.lse, atol=1e-12)
+
+
+def test_prefill_matches_brute_force_definition():
+    q, k, v = _prefill_inputs(15, B=1, Hq=2, Hkv=1, T=7, d=4)
+    tau = np.random.default_rng(16).normal(0.0, 0.7, (1, 2, 7))
+    beta, C = 2.5, 1.7
+    for additive in (False, True):
+        r = oracle.prefill(q, k, v, tau, [7], beta=beta, additive=additive, C=C)
+        for h in range(2):
+            for i in range(7):
+                sc, gs = [], 0.0
+                for j in range(i + 1):
+                    S = sum(float(q[0, h, i, c]) * float(k[0, 0, j, c]) for c in range(4)) / 2.0
+                    g = 1.0 / (1.0 + math.exp(-beta * (S - tau[0, h, i])))
+                    gs += g
+                    sc.append(S if j == i else (S + C * g - C if additive else S * g))
+                mx = max(sc)
+                w = [math.exp(x - mx) for x in sc]
+                o = [sum(w[j] * float(v[0, 0, j, c]) for j in range(i + 1)) / sum(w) for c in range(4)]
+                np.testing.assert_allclose(r.o[0, h, i], o, atol=1e-12)
+                assert abs(r.r[0, h, i] - gs) < 1e-12
+                assert abs(r.lse[0, h, i] - (mx + math.log(sum(w)))) < 1e-12
