@@ -58,6 +58,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline")
+    ap.add_argument("--no-prefill", action="store_true",
+                    help="skip the gated prefill forward measurement")
     ap.add_argument("--no-calibration", action="store_true",
                     help="skip the offline threshold calibration measurement")
     ap.add_argument("--only-primary", action="store_true",
@@ -339,6 +341,34 @@ def main():
         log(f"[bench] calibration: {calib}")
         del cs, cal
 
+    # ---- gated prefill / training forward: one 16K-token sequence at the ragged
+    # workload's head shape (32 query / 8 kv heads, d = 128), bf16
+    prefill = None
+    if not args.no_prefill:
+        pB, pHq, pHkv, pT, pd = 1, 32, 8, 16384, 128
+        g = torch.Generator(device=dev).manual_seed(10)
+        pq = torch.randn(pB, pHq, pT, pd, generator=g, device=dev).to(torch.bfloat16)
+        pk = torch.randn(pB, pHkv, pT, pd, generator=g, device=dev).to(torch.bfloat16)
+        pv = torch.randn(pB, pHkv, pT, pd, generator=g, device=dev).to(torch.bfloat16)
+        ptau = 0.5 + 0.5 * torch.randn(pB, pHq, pT, generator=g, device=dev)
+        psl = torch.full((pB,), pT, dtype=torch.int32, device=dev)
+        pout, pR, pL = eta.gated_prefill(pq, pk, pv, ptau, psl, beta=4.0)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        reps = 5
+        e0.record()
+        for _ in range(reps):
+            eta.gated_prefill(pq, pk, pv, ptau, psl, beta=4.0, out=pout, R=pR, L=pL)
+        e1.record()
+        torch.cuda.synchronize()
+        pms = e0.elapsed_time(e1) / reps
+        pflops = 4.0 * pd * pHq * pT * (pT + 1) / 2      # QK^T and p.V over the causal pairs
+        prefill = {"workload": f"B={pB}, {pT} tokens, {pHq}/{pHkv} heads, d={pd}, bf16, causal",
+                   "ms": round(pms, 3), "tflops": round(pflops / pms / 1e9, 1),
+                   "frac_of_bf16_mfma_peak": round(pflops / pms / 1e9 / 2500.0, 4)}
+        log(f"[bench] gated prefill: {prefill}")
+        del pq, pk, pv, ptau, pout, pR, pL
+
     ms, gpu_ms, kt, kv_b, step_b, ub, dh, du, steps, warm, cold_ms = primary
     split_ms, split_n = kt["split_decode"]
     split_avg_ms = split_ms / max(split_n, 1)
@@ -397,6 +427,7 @@ def main():
         "summary_update_us_per_step": round(upd_ms * 1e3, 2),
         "index_f16_us_per_step": index_f16,
         "calibration": calib,
+        "gated_prefill": prefill,
         "roofline": {"bound": "hbm", "kernel": "split_decode", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "algorithmic_bytes_per_launch": kv_b,

@@ -306,6 +306,38 @@ eta_status_t eta_calib_solve(const eta_calib_desc_t* cd, const eta_calib_state_t
                              float* c_out, double* target_out, void* stream);
 
 /*
+ * Gated prefill / training forward (App. "Hardware-Aligned Forward Kernel"):
+ * for every sequence b, query head h (kv head h / G) and row i < seq_lens[b],
+ * over the causal keys j <= i:
+ *   S_ij = <q_i, k_j> / sqrt(head_dim),  sigma_ij = sigmoid(beta (S_ij - tau_i))
+ *   S~_ij = S_ij sigma_ij, or S_ij + C sigma_ij - C when additive; S~_ii = S_ii
+ *   out_i = sum_j softmax_j(S~_ij) v_j,  R_i = sum_j sigma_ij,  L_i = log sum_j exp(S~_ij)
+ * Rows i >= seq_lens[b] (up to capacity_tokens): out 0, R 0, L -inf.  Scores
+ * and p.V on the matrix cores (bf16 operands, fp32 accumulation; the softmax
+ * weights are rounded to bf16 for p.V), everything else fp32.
+ *   q, out   bf16 [batch][num_q_heads][capacity_tokens][head_dim]
+ *   k, v     bf16 [batch][num_kv_heads][capacity_tokens][head_dim]
+ *   tau      fp32 [batch][num_q_heads][capacity_tokens]  per-row thresholds
+ *   R, L     fp32 [batch][num_q_heads][capacity_tokens]
+ *   seq_lens device int32 [batch]
+ */
+typedef struct {
+  int32_t batch;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;        /* num_q_heads / num_kv_heads in {1, 2, 4, 8} */
+  int32_t head_dim;            /* 64 or 128 */
+  int32_t capacity_tokens;     /* rows per (sequence, head) in every tensor, >= 1 */
+  int32_t dtype;               /* q, k, v, out: ETA_DT_BF16 */
+  float beta;                  /* finite, >= 0 */
+  int32_t additive;            /* 0: multiplicative gate S sigma; 1: S + C sigma - C */
+  float C;                     /* additive mask depth, finite (ignored when multiplicative) */
+} eta_prefill_desc_t;
+
+eta_status_t eta_gated_prefill(const eta_prefill_desc_t* pd, const void* q, const void* k,
+                               const void* v, const float* tau, const int32_t* seq_lens,
+                               void* out, float* R, float* L, void* stream);
+
+/*
  * eta_block_bounds -- the screening bound of Eq. (dual_bound_eq) for every
  * full block and query head, as eta_decode computes it, without selecting or
  * attending.  For threshold calibration and diagnostics.
@@ -354,7 +386,8 @@ typedef enum {
   ETA_KERNEL_BOUNDS = 7,
   ETA_KERNEL_CALIB_ACCUMULATE = 8,
   ETA_KERNEL_CALIB_SOLVE = 9,
-  ETA_KERNEL_KINDS = 10
+  ETA_KERNEL_PREFILL = 10,
+  ETA_KERNEL_KINDS = 11
 } eta_kernel_kind_t;
 
 typedef struct {

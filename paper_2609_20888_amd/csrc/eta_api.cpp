@@ -419,6 +419,37 @@ eta_status_t eta_calib_solve(const eta_calib_desc_t* cd, const eta_calib_state_t
   return ok();
 }
 
+eta_status_t eta_gated_prefill(const eta_prefill_desc_t* pd, const void* q, const void* k,
+                               const void* v, const float* tau, const int32_t* seq_lens,
+                               void* out, float* R, float* L, void* stream) {
+  if (!pd) return fail(ETA_ERR_INVALID_ARG, "prefill descriptor is NULL");
+  if (pd->batch < 1 || pd->batch > 65535 || pd->capacity_tokens < 1)
+    return fail(ETA_ERR_INVALID_ARG, "batch must be in [1, 65535] and capacity_tokens >= 1");
+  if (pd->num_q_heads < 1 || pd->num_kv_heads < 1 || pd->num_q_heads % pd->num_kv_heads != 0)
+    return fail(ETA_ERR_INVALID_ARG, "num_q_heads must be a positive multiple of num_kv_heads");
+  const int G = pd->num_q_heads / pd->num_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return fail(ETA_ERR_UNSUPPORTED, "GQA group size %d unsupported (1, 2, 4 or 8)", G);
+  if (pd->num_q_heads > 256) return fail(ETA_ERR_UNSUPPORTED, "num_q_heads > 256 unsupported");
+  if (pd->head_dim != 64 && pd->head_dim != 128)
+    return fail(ETA_ERR_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", pd->head_dim);
+  if (pd->dtype != ETA_DT_BF16) return fail(ETA_ERR_UNSUPPORTED, "prefill takes bf16 q, k, v");
+  if (!std::isfinite(pd->beta) || pd->beta < 0.f)
+    return fail(ETA_ERR_INVALID_ARG, "beta must be finite and >= 0");
+  if (pd->additive != 0 && pd->additive != 1) return fail(ETA_ERR_INVALID_ARG, "additive must be 0 or 1");
+  if (pd->additive && !std::isfinite(pd->C)) return fail(ETA_ERR_INVALID_ARG, "C must be finite");
+  if (!q || !k || !v || !tau || !seq_lens || !out || !R || !L)
+    return fail(ETA_ERR_INVALID_ARG, "q, k, v, tau, seq_lens, out, R and L must be non-NULL");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) ||
+      (reinterpret_cast<uintptr_t>(tau) | reinterpret_cast<uintptr_t>(R) |
+       reinterpret_cast<uintptr_t>(L) | reinterpret_cast<uintptr_t>(seq_lens)) & 3u)
+    return fail(ETA_ERR_INVALID_ARG, "q, k, v, out must be 16-byte and tau, R, L, seq_lens 4-byte aligned");
+  hipError_t e = launch_prefill(*pd, q, k, v, tau, seq_lens, out, R, L, (hipStream_t)stream,
+                                active_hook());
+  if (e != hipSuccess) return fail(ETA_ERR_HIP, "prefill launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 eta_status_t eta_block_bounds(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q,
                               const int32_t* seq_lens, const eta_summary_t* summ, float z,
                               float* bounds, void* stream) {

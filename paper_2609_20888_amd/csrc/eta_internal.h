@@ -83,6 +83,9 @@ hipError_t launch_calib(const eta_calib_desc_t& cd, const void* q, const void* k
 hipError_t launch_calib_solve(const eta_calib_desc_t& cd, const eta_calib_state_t& st, float* c_out,
                               double* target_out, hipStream_t stream, LaunchHook hook);
 constexpr int kCalibBinsMax = 4096;
+hipError_t launch_prefill(const eta_prefill_desc_t& pd, const void* q, const void* k, const void* v,
+                          const float* tau, const int32_t* seq_lens, void* out, float* R, float* L,
+                          hipStream_t stream, LaunchHook hook);
 
 hipError_t launch_dense(const Geom& g, int S, int q_dtype, const void* q, const void* k,
                         const void* v, const int32_t* seq_lens, void* out, const DecodeWs& ws,

@@ -1441,6 +1441,222 @@ __global__ __launch_bounds__(256) void calib_solve_kernel(CalibSolveArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- gated prefill forward
+//
+// The training / prefill forward (App. "Hardware-Aligned Forward Kernel"):
+// causal attention over gated scores S~ = S sigma(beta (S - tau_i)) (or the
+// additive S + C sigma - C), diagonal ungated, with the gate row sums R and the
+// log-sum-exp L.  One workgroup per (64-query block, query head, sequence),
+// longest blocks first; wavefront w owns query rows 16 w .. 16 w + 15 of the
+// block.  Per 64-key block: the workgroup stages K row-major and V transposed
+// in LDS (the next block is loaded into registers meanwhile); scores on
+// v_mfma_f32_16x16x32_bf16 (A = 16 query rows x 32 dims from registers, B =
+// 32 dims x 16 keys from LDS), so lane l holds rows 4 (l >> 4) + i and key
+// l & 15 of each 16-key quarter; gate, mask and online softmax per row with
+// 16-lane DPP reductions; P goes through the wavefront's LDS slice into the
+// A layout and p.V runs on the MFMAs with B = V^T from LDS; fp32 accumulators.
+
+constexpr int kPfQ = 64;     // query rows per workgroup
+constexpr int kPfK = 64;     // keys per block
+constexpr int kPfPad = 8;    // bf16 padding of LDS rows
+
+struct PrefillArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const float* tau;
+  const int32_t* seq_lens;
+  uint16_t* out;
+  float* R;
+  float* L;
+  int Hq, Hkv, T;
+  float beta, C;
+  int additive;
+};
+
+// 16-lane group reductions (rows of the MFMA result); all lanes of the group
+// end with the value
+__device__ __forceinline__ float row16_max(float x) {
+  x = fmaxf(x, dpp_mov<0xB1>(x));
+  x = fmaxf(x, dpp_mov<0x4E>(x));
+  x = fmaxf(x, dpp_mov<0x141>(x));
+  return fmaxf(x, dpp_mov<0x140>(x));
+}
+__device__ __forceinline__ float row16_sum(float x) {
+  x += dpp_mov<0xB1>(x);
+  x += dpp_mov<0x4E>(x);
+  x += dpp_mov<0x141>(x);
+  return x + dpp_mov<0x140>(x);
+}
+
+// Native vector (a value, not a struct: register staging never goes through memory).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// This thread's share of a 64-key block of K and V (rows past the cache read its last row).
+template <int D, int LPT>
+__device__ __forceinline__ void prefill_load_kv(const uint16_t* __restrict__ kh,
+                                                const uint16_t* __restrict__ vh, int kb, int T,
+                                                int tid, u32x4 (&kr)[LPT], u32x4 (&vr)[LPT]) {
+  constexpr int CPR = D / 8;
+#pragma unroll
+  for (int u = 0; u < LPT; ++u) {
+    const int c = tid + 256 * u;
+    const int row = min(kb * kPfK + c / CPR, T - 1);
+    kr[u] = *reinterpret_cast<const u32x4*>(kh + (int64_t)row * D + 8 * (c % CPR));
+    vr[u] = *reinterpret_cast<const u32x4*>(vh + (int64_t)row * D + 8 * (c % CPR));
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
+  constexpr int KC = D / 32;             // 32-dim chunks (QK^T contraction)
+  constexpr int DB = D / 16;             // 16-dim output blocks
+  constexpr int KLD = D + kPfPad;        // K row stride in LDS (bf16)
+  constexpr int VLD = kPfK + kPfPad;     // V^T row stride in LDS (bf16)
+  constexpr int PLD = kPfK + kPfPad;     // P row stride
+  constexpr int CPR = D / 8;             // 16-byte chunks per K / V row
+  constexpr int LPT = kPfK * CPR / 256;  // chunks per thread per block
+  __shared__ __attribute__((aligned(16))) uint16_t k_s[kPfK * KLD];
+  __shared__ __attribute__((aligned(16))) uint16_t vt_s[D * VLD];
+  __shared__ __attribute__((aligned(16))) uint16_t p_s[4][16 * PLD];
+
+  const int nqb = (a.T + kPfQ - 1) / kPfQ;
+  const int qblk = nqb - 1 - (int)blockIdx.x;        // longest causal ranges first
+  const int h = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
+  const int r16 = lane & 15, g4 = lane >> 4;
+  const int G = a.Hq / a.Hkv;
+  const int Tb = (int)clamp_len(a.seq_lens, b, a.T);
+  const int64_t qrow0 = ((int64_t)b * a.Hq + h) * a.T;
+  const uint16_t* kh = a.k + (((int64_t)b * a.Hkv + h / G) * a.T) * D;
+  const uint16_t* vh = a.v + (((int64_t)b * a.Hkv + h / G) * a.T) * D;
+  const float scale = 1.0f / sqrtf((float)D);
+
+  // this wavefront's query rows as the A operand (rows past the cache read its last row)
+  const int qa_row = min(qblk * kPfQ + 16 * w + r16, a.T - 1);
+  uint4 qa[KC];
+#pragma unroll
+  for (int kc = 0; kc < KC; ++kc)
+    qa[kc] = *reinterpret_cast<const uint4*>(a.q + (qrow0 + qa_row) * D + 32 * kc + 8 * g4);
+  int t_i[4];
+  float tau_i[4], m_i[4], l_i[4], r_i[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    t_i[i] = qblk * kPfQ + 16 * w + 4 * g4 + i;
+    tau_i[i] = a.tau[qrow0 + min(t_i[i], a.T - 1)];
+    m_i[i] = kNegInf;
+    l_i[i] = 0.f;
+    r_i[i] = 0.f;
+  }
+  f32x4 acc[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // key blocks 0 .. last: up to the block's last query row and the sequence's length
+  const int last_row = min(qblk * kPfQ + kPfQ, Tb) - 1;
+  const int nkb = last_row >= 0 ? last_row / kPfK + 1 : 0;
+  u32x4 kr[LPT], vr[LPT];
+  if (nkb > 0) prefill_load_kv<D, LPT>(kh, vh, 0, a.T, tid, kr, vr);
+  for (int kb = 0; kb < nkb; ++kb) {
+    __syncthreads();                       // every wavefront is done with the previous block
+#pragma unroll
+    for (int u = 0; u < LPT; ++u) {
+      const int c = tid + 256 * u;
+      const int key = c / CPR, d0 = 8 * (c % CPR);
+      *reinterpret_cast<u32x4*>(&k_s[key * KLD + d0]) = kr[u];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        vt_s[(d0 + 2 * e) * VLD + key] = (uint16_t)(vr[u][e] & 0xffffu);
+        vt_s[(d0 + 2 * e + 1) * VLD + key] = (uint16_t)(vr[u][e] >> 16);
+      }
+    }
+    __syncthreads();
+    // the next block's loads are in flight during this block's arithmetic (the last
+    // iteration reloads its own block: an unconditional load keeps one copy of kr, vr)
+    prefill_load_kv<D, LPT>(kh, vh, kb + 1 < nkb ? kb + 1 : kb, a.T, tid, kr, vr);
+
+    // scores of the wavefront's 16 rows against the 64 keys
+    f32x4 c[4];
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) {
+      c[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc) {
+        const bf16x8 bk = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const uint4*>(&k_s[(16 * nb + r16) * KLD + 32 * kc + 8 * g4]));
+        c[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, qa[kc]), bk, c[nb], 0, 0, 0);
+      }
+    }
+    // gate, mask, online softmax; P to the wavefront's LDS slice
+    float alpha[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = t_i[i];
+      float sg[4], mx = kNegInf;
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        const int s = kb * kPfK + 16 * nb + r16;
+        const bool valid = s <= t && t < Tb;
+        const float S = c[nb][i] * scale;
+        const float gate = 1.0f / (1.0f + __expf(-a.beta * (S - tau_i[i])));
+        r_i[i] += valid ? gate : 0.f;
+        float x = a.additive ? S + a.C * gate - a.C : S * gate;
+        if (s == t) x = S;
+        sg[nb] = valid ? x : kNegInf;
+        mx = fmaxf(mx, sg[nb]);
+      }
+      mx = row16_max(mx);
+      const float mn = fmaxf(m_i[i], mx);
+      alpha[i] = mn == kNegInf ? 1.f : __expf(m_i[i] - mn);
+      float ps = 0.f;
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        const float p = mn == kNegInf ? 0.f : __expf(sg[nb] - mn);
+        ps += p;
+        p_s[w][(4 * g4 + i) * PLD + 16 * nb + r16] = to_bf16(p);
+      }
+      l_i[i] = l_i[i] * alpha[i] + row16_sum(ps);
+      m_i[i] = mn;
+    }
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[db][i] *= alpha[i];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // acc += P V: A = P rows (16 x 32 keys), B = V^T (32 keys x 16 dims)
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const bf16x8 pa = __builtin_bit_cast(
+          bf16x8, *reinterpret_cast<const uint4*>(&p_s[w][r16 * PLD + 32 * kk + 8 * g4]));
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const bf16x8 bv = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const uint4*>(&vt_s[(16 * db + r16) * VLD + 32 * kk + 8 * g4]));
+        acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, bv, acc[db], 0, 0, 0);
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+  // outputs: rows 4 g4 + i of the wavefront, dims 16 db + r16
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int t = t_i[i];
+    const float rs = row16_sum(r_i[i]);
+    if (t < a.T) {
+      const float inv = l_i[i] > 0.f ? 1.0f / l_i[i] : 0.f;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+        a.out[(qrow0 + t) * D + 16 * db + r16] = to_bf16(acc[db][i] * inv);
+      if (r16 == 0) {
+        a.R[qrow0 + t] = t < Tb ? rs : 0.f;
+        a.L[qrow0 + t] = l_i[i] > 0.f ? m_i[i] + logf(l_i[i]) : kNegInf;
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------- combine
 
 struct CombineArgs {
@@ -1692,6 +1908,20 @@ hipError_t launch_calib_solve(const eta_calib_desc_t& cd, const eta_calib_state_
                     cd.num_bins, (double)cd.beta, (double)cd.lo, (double)cd.hi};
   return with_hook(hook, ETA_KERNEL_CALIB_SOLVE, stream, [&] {
     hipLaunchKernelGGL(calib_solve_kernel, dim3(cd.num_q_heads), dim3(256), 0, stream, sa);
+  });
+}
+
+hipError_t launch_prefill(const eta_prefill_desc_t& pd, const void* q, const void* k, const void* v,
+                          const float* tau, const int32_t* seq_lens, void* out, float* R, float* L,
+                          hipStream_t stream, LaunchHook hook) {
+  PrefillArgs pa{reinterpret_cast<const uint16_t*>(q), reinterpret_cast<const uint16_t*>(k),
+                 reinterpret_cast<const uint16_t*>(v), tau, seq_lens,
+                 reinterpret_cast<uint16_t*>(out), R, L, pd.num_q_heads, pd.num_kv_heads,
+                 pd.capacity_tokens, pd.beta, pd.C, pd.additive};
+  dim3 grid((pd.capacity_tokens + kPfQ - 1) / kPfQ, pd.num_q_heads, pd.batch);
+  return with_hook(hook, ETA_KERNEL_PREFILL, stream, [&] {
+    if (pd.head_dim == 64) hipLaunchKernelGGL(prefill_kernel<64>, grid, dim3(256), 0, stream, pa);
+    if (pd.head_dim == 128) hipLaunchKernelGGL(prefill_kernel<128>, grid, dim3(256), 0, stream, pa);
   });
 }
 

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libeta.so")
 ETA_OK, ETA_ERR_INVALID_ARG, ETA_ERR_UNSUPPORTED, ETA_ERR_WORKSPACE, ETA_ERR_HIP = range(5)
 ETA_DT_F32, ETA_DT_BF16, ETA_DT_F16 = 0, 1, 2
 KERNEL_KINDS = ("summaries", "predict", "screen", "split_decode", "combine", "dense_split",
-                "dense_combine", "bounds", "calib_accumulate", "calib_solve")
+                "dense_combine", "bounds", "calib_accumulate", "calib_solve", "prefill")
 
 _vp = ctypes.c_void_p
 
@@ -50,6 +50,13 @@ class CalibState(ctypes.Structure):
     _fields_ = [("hist", _vp), ("density", _vp)]
 
 
+class PrefillDesc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("capacity_tokens", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("beta", ctypes.c_float), ("additive", ctypes.c_int32), ("C", ctypes.c_float)]
+
+
 class DecodeParams(ctypes.Structure):
     _fields_ = [("beta", ctypes.c_float), ("z", ctypes.c_float), ("offset_a", ctypes.c_float),
                 ("rescue_window_blocks", ctypes.c_int32), ("pin_recent_blocks", ctypes.c_int32),
@@ -65,7 +72,7 @@ class KernelTime(ctypes.Structure):
 EXPORTS = ("eta_build_block_summaries", "eta_build_block_summaries_envelope",
            "eta_update_block_summaries", "eta_predict_threshold", "eta_decode_workspace_size",
            "eta_decode", "eta_decode_predicted", "eta_block_bounds", "eta_dense_workspace_size", "eta_dense_decode",
-           "eta_calib_accumulate", "eta_calib_solve",
+           "eta_calib_accumulate", "eta_calib_solve", "eta_gated_prefill",
            "eta_last_error_string", "eta_abi_version", "eta_profile_begin", "eta_profile_end")
 
 
@@ -95,6 +102,7 @@ def load_library(path: Optional[str] = None):
         "eta_build_block_summaries": [P(KvDesc), _vp, _vp, P(SummaryDesc), _vp],
         "eta_calib_accumulate": [P(CalibDesc), _vp, _vp, _vp, P(CalibState), _vp],
         "eta_calib_solve": [P(CalibDesc), P(CalibState), _vp, _vp, _vp],
+        "eta_gated_prefill": [P(PrefillDesc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp],
         "eta_build_block_summaries_envelope": [P(KvDesc), _vp, _vp, i32, P(SummaryDesc), _vp],
         "eta_update_block_summaries": [P(KvDesc), _vp, _vp, _vp, i32, i32, P(SummaryDesc), _vp],
         "eta_predict_threshold": [i32, i32, i32, i32, _vp, _vp, _vp, _vp, _vp],
@@ -432,3 +440,29 @@ class Calibrator:
         _check(load_library().eta_calib_solve(ctypes.byref(desc), ctypes.byref(st), _ptr(c),
                                               _ptr(target), _stream(stream)))
         return c, target
+
+
+def gated_prefill(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, tau: torch.Tensor,
+                  seq_lens: torch.Tensor, *, beta: float, additive: bool = False, C: float = 0.0,
+                  out: Optional[torch.Tensor] = None, R: Optional[torch.Tensor] = None,
+                  L: Optional[torch.Tensor] = None, stream=None):
+    """eta_gated_prefill: gated causal attention forward with the gate row sums R and
+    the log-sum-exp L.  q bf16 [B][Hq][T][d], k, v bf16 [B][Hkv][T][d], tau fp32
+    [B][Hq][T], seq_lens int32 [B]; returns (out bf16 [B][Hq][T][d], R, L fp32 [B][Hq][T])."""
+    B, Hq, T, d = q.shape
+    Hkv = k.shape[1]
+    assert k.shape == (B, Hkv, T, d) and v.shape == k.shape and tau.shape == (B, Hq, T)
+    assert q.dtype == k.dtype == v.dtype == torch.bfloat16 and tau.dtype == torch.float32
+    assert q.is_contiguous() and k.is_contiguous() and v.is_contiguous() and tau.is_contiguous()
+    if out is None:
+        out = torch.empty_like(q)
+    if R is None:
+        R = torch.empty(B, Hq, T, dtype=torch.float32, device=q.device)
+    if L is None:
+        L = torch.empty(B, Hq, T, dtype=torch.float32, device=q.device)
+    desc = PrefillDesc(batch=B, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=d, capacity_tokens=T,
+                       dtype=ETA_DT_BF16, beta=beta, additive=int(bool(additive)), C=C)
+    _check(load_library().eta_gated_prefill(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v),
+                                            _ptr(tau), _ptr(seq_lens), _ptr(out), _ptr(R), _ptr(L),
+                                            _stream(stream)))
+    return out, R, L

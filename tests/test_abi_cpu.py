@@ -197,3 +197,23 @@ def test_calibration_rejects(lib):
     assert acc(desc(), s=eta.CalibState(hist=FAKE + 4, density=FAKE)) == eta.ETA_ERR_INVALID_ARG
     assert lib.eta_calib_solve(ctypes.byref(desc()), ctypes.byref(st), None, None, None) \
         == eta.ETA_ERR_INVALID_ARG
+
+
+def test_prefill_rejects(lib):
+    def desc(**kw):
+        d = dict(batch=1, num_q_heads=8, num_kv_heads=2, head_dim=128, capacity_tokens=256,
+                 dtype=eta.ETA_DT_BF16, beta=4.0, additive=0, C=0.0)
+        d.update(kw)
+        return eta.PrefillDesc(**d)
+    call = lambda pd, **p: lib.eta_gated_prefill(
+        ctypes.byref(pd), p.get("q", FAKE), FAKE, FAKE, p.get("tau", FAKE), FAKE, p.get("out", FAKE),
+        FAKE, FAKE, None)
+    for kw, code in [(dict(batch=0), eta.ETA_ERR_INVALID_ARG), (dict(capacity_tokens=0), eta.ETA_ERR_INVALID_ARG),
+                     (dict(num_kv_heads=3), eta.ETA_ERR_INVALID_ARG), (dict(head_dim=80), eta.ETA_ERR_UNSUPPORTED),
+                     (dict(num_kv_heads=1, num_q_heads=16), eta.ETA_ERR_UNSUPPORTED),
+                     (dict(dtype=eta.ETA_DT_F32), eta.ETA_ERR_UNSUPPORTED), (dict(beta=-1.0), eta.ETA_ERR_INVALID_ARG),
+                     (dict(additive=2), eta.ETA_ERR_INVALID_ARG), (dict(additive=1, C=float("inf")), eta.ETA_ERR_INVALID_ARG)]:
+        assert call(desc(**kw)) == code, kw
+    assert call(desc(), q=None) == eta.ETA_ERR_INVALID_ARG
+    assert call(desc(), out=FAKE + 8) == eta.ETA_ERR_INVALID_ARG
+    assert call(desc(), tau=FAKE + 2) == eta.ETA_ERR_INVALID_ARG
