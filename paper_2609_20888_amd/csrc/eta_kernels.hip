@@ -1447,14 +1447,17 @@ __global__ __launch_bounds__(256) void calib_solve_kernel(CalibSolveArgs a) {
 // causal attention over gated scores S~ = S sigma(beta (S - tau_i)) (or the
 // additive S + C sigma - C), diagonal ungated, with the gate row sums R and the
 // log-sum-exp L.  One workgroup per (64-query block, query head, sequence),
-// longest blocks first; wavefront w owns query rows 16 w .. 16 w + 15 of the
-// block.  Per 64-key block: the workgroup stages K row-major and V transposed
-// in LDS (the next block is loaded into registers meanwhile); scores on
-// v_mfma_f32_16x16x32_bf16 (A = 16 query rows x 32 dims from registers, B =
-// 32 dims x 16 keys from LDS), so lane l holds rows 4 (l >> 4) + i and key
-// l & 15 of each 16-key quarter; gate, mask and online softmax per row with
-// 16-lane DPP reductions; P goes through the wavefront's LDS slice into the
-// A layout and p.V runs on the MFMAs with B = V^T from LDS; fp32 accumulators.
+// longest blocks first; wavefront w owns query rows 16 w .. 16 w + 15.  Per
+// 64-key block the workgroup stages K and V row-major in LDS (the next block is
+// loaded into registers meanwhile).  Everything is computed transposed so that
+// each lane owns one query row: S^T = K Q^T on v_mfma_f32_16x16x32_bf16 (A = 16
+// keys x 32 dims from LDS, B = 32 dims x 16 queries from registers) gives lane l
+// the scores of query l & 15 against keys 4 (l >> 4) + i of each 16-key
+// quarter; the gate, mask and online softmax are per lane, with the four lane
+// groups of a row combined by row / half-wave swaps; O^T += V^T P^T takes B =
+// the lane's own gated weights (bf16), the contraction over keys permuted
+// consistently on both sides, and A = V^T from two LDS transpose reads
+// (ds_read_b64_tr_b16) of the row-major V tile.  fp32 accumulators.
 
 constexpr int kPfQ = 64;     // query rows per workgroup
 constexpr int kPfK = 64;     // keys per block
@@ -1474,23 +1477,22 @@ struct PrefillArgs {
   int additive;
 };
 
-// 16-lane group reductions (rows of the MFMA result); all lanes of the group
-// end with the value
-__device__ __forceinline__ float row16_max(float x) {
-  x = fmaxf(x, dpp_mov<0xB1>(x));
-  x = fmaxf(x, dpp_mov<0x4E>(x));
-  x = fmaxf(x, dpp_mov<0x141>(x));
-  return fmaxf(x, dpp_mov<0x140>(x));
-}
-__device__ __forceinline__ float row16_sum(float x) {
-  x += dpp_mov<0xB1>(x);
-  x += dpp_mov<0x4E>(x);
-  x += dpp_mov<0x141>(x);
-  return x + dpp_mov<0x140>(x);
-}
-
-// Native vector (a value, not a struct: register staging never goes through memory).
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+
+// lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same query row
+__device__ __forceinline__ float row4_max(float x) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float row4_sum(float x) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 // This thread's share of a 64-key block of K and V (rows past the cache read its last row).
 template <int D, int LPT>
@@ -1509,16 +1511,13 @@ __device__ __forceinline__ void prefill_load_kv(const uint16_t* __restrict__ kh,
 
 template <int D>
 __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
-  constexpr int KC = D / 32;             // 32-dim chunks (QK^T contraction)
+  constexpr int KC = D / 32;             // 32-dim chunks (score contraction)
   constexpr int DB = D / 16;             // 16-dim output blocks
-  constexpr int KLD = D + kPfPad;        // K row stride in LDS (bf16)
-  constexpr int VLD = kPfK + kPfPad;     // V^T row stride in LDS (bf16)
-  constexpr int PLD = kPfK + kPfPad;     // P row stride
-  constexpr int CPR = D / 8;             // 16-byte chunks per K / V row
+  constexpr int LD = D + kPfPad;         // K / V row stride in LDS (bf16)
+  constexpr int CPR = D / 8;             // 16-byte chunks per row
   constexpr int LPT = kPfK * CPR / 256;  // chunks per thread per block
-  __shared__ __attribute__((aligned(16))) uint16_t k_s[kPfK * KLD];
-  __shared__ __attribute__((aligned(16))) uint16_t vt_s[D * VLD];
-  __shared__ __attribute__((aligned(16))) uint16_t p_s[4][16 * PLD];
+  __shared__ __attribute__((aligned(16))) uint16_t k_s[kPfK * LD];
+  __shared__ __attribute__((aligned(16))) uint16_t v_s[kPfK * LD];
 
   const int nqb = (a.T + kPfQ - 1) / kPfQ;
   const int qblk = nqb - 1 - (int)blockIdx.x;        // longest causal ranges first
@@ -1532,27 +1531,22 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
   const uint16_t* vh = a.v + (((int64_t)b * a.Hkv + h / G) * a.T) * D;
   const float scale = 1.0f / sqrtf((float)D);
 
-  // this wavefront's query rows as the A operand (rows past the cache read its last row)
-  const int qa_row = min(qblk * kPfQ + 16 * w + r16, a.T - 1);
-  uint4 qa[KC];
+  // this lane's query row and its B operand (dims 32 kc + 8 g4 .. + 7)
+  const int t = qblk * kPfQ + 16 * w + r16;
+  const int tq = min(t, a.T - 1);
+  u32x4 qb[KC];
 #pragma unroll
   for (int kc = 0; kc < KC; ++kc)
-    qa[kc] = *reinterpret_cast<const uint4*>(a.q + (qrow0 + qa_row) * D + 32 * kc + 8 * g4);
-  int t_i[4];
-  float tau_i[4], m_i[4], l_i[4], r_i[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    t_i[i] = qblk * kPfQ + 16 * w + 4 * g4 + i;
-    tau_i[i] = a.tau[qrow0 + min(t_i[i], a.T - 1)];
-    m_i[i] = kNegInf;
-    l_i[i] = 0.f;
-    r_i[i] = 0.f;
-  }
+    qb[kc] = *reinterpret_cast<const u32x4*>(a.q + (qrow0 + tq) * D + 32 * kc + 8 * g4);
+  const float tau_t = a.tau[qrow0 + tq];
+  float m_i = kNegInf, l_i = 0.f, r_i = 0.f;
   f32x4 acc[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // transpose-read address of V: the lane provides key 4 g4 + (r16 >> 2) (+16 for keys
+  // 16..31 of a 32-key chunk), dims 4 (lane & 3) of a 16-dim block
+  const int vt_off = (4 * g4 + (r16 >> 2)) * LD + 4 * (lane & 3);
 
-  // key blocks 0 .. last: up to the block's last query row and the sequence's length
   const int last_row = min(qblk * kPfQ + kPfQ, Tb) - 1;
   const int nkb = last_row >= 0 ? last_row / kPfK + 1 : 0;
   u32x4 kr[LPT], vr[LPT];
@@ -1562,97 +1556,94 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
     for (int u = 0; u < LPT; ++u) {
       const int c = tid + 256 * u;
-      const int key = c / CPR, d0 = 8 * (c % CPR);
-      *reinterpret_cast<u32x4*>(&k_s[key * KLD + d0]) = kr[u];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        vt_s[(d0 + 2 * e) * VLD + key] = (uint16_t)(vr[u][e] & 0xffffu);
-        vt_s[(d0 + 2 * e + 1) * VLD + key] = (uint16_t)(vr[u][e] >> 16);
-      }
+      *reinterpret_cast<u32x4*>(&k_s[(c / CPR) * LD + 8 * (c % CPR)]) = kr[u];
+      *reinterpret_cast<u32x4*>(&v_s[(c / CPR) * LD + 8 * (c % CPR)]) = vr[u];
     }
     __syncthreads();
     // the next block's loads are in flight during this block's arithmetic (the last
     // iteration reloads its own block: an unconditional load keeps one copy of kr, vr)
     prefill_load_kv<D, LPT>(kh, vh, kb + 1 < nkb ? kb + 1 : kb, a.T, tid, kr, vr);
 
-    // scores of the wavefront's 16 rows against the 64 keys
+    // S^T: lane holds query t against keys 16 nb + 4 g4 + i
     f32x4 c[4];
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
       c[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kc = 0; kc < KC; ++kc) {
-        const bf16x8 bk = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const uint4*>(&k_s[(16 * nb + r16) * KLD + 32 * kc + 8 * g4]));
-        c[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, qa[kc]), bk, c[nb], 0, 0, 0);
+        const u32x4 ka = *reinterpret_cast<const u32x4*>(&k_s[(16 * nb + r16) * LD + 32 * kc + 8 * g4]);
+        c[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka),
+                                                         __builtin_bit_cast(bf16x8, qb[kc]), c[nb], 0, 0, 0);
       }
     }
-    // gate, mask, online softmax; P to the wavefront's LDS slice
-    float alpha[4];
+    // gate, mask, online softmax of the lane's row
+    float sg[4][4], mx = kNegInf;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int t = t_i[i];
-      float sg[4], mx = kNegInf;
+    for (int nb = 0; nb < 4; ++nb)
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) {
-        const int s = kb * kPfK + 16 * nb + r16;
+      for (int i = 0; i < 4; ++i) {
+        const int s = kb * kPfK + 16 * nb + 4 * g4 + i;
         const bool valid = s <= t && t < Tb;
         const float S = c[nb][i] * scale;
-        const float gate = 1.0f / (1.0f + __expf(-a.beta * (S - tau_i[i])));
-        r_i[i] += valid ? gate : 0.f;
+        const float gate = 1.0f / (1.0f + __expf(-a.beta * (S - tau_t)));
+        r_i += valid ? gate : 0.f;
         float x = a.additive ? S + a.C * gate - a.C : S * gate;
         if (s == t) x = S;
-        sg[nb] = valid ? x : kNegInf;
-        mx = fmaxf(mx, sg[nb]);
+        sg[nb][i] = valid ? x : kNegInf;
+        mx = fmaxf(mx, sg[nb][i]);
       }
-      mx = row16_max(mx);
-      const float mn = fmaxf(m_i[i], mx);
-      alpha[i] = mn == kNegInf ? 1.f : __expf(m_i[i] - mn);
-      float ps = 0.f;
+    mx = row4_max(mx);
+    const float mn = fmaxf(m_i, mx);
+    const float alpha = mn == kNegInf ? 1.f : __expf(m_i - mn);
+    float ps = 0.f;
+    uint32_t pw[8];                        // bf16 pairs: B operands of the two 32-key chunks
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) {
-        const float p = mn == kNegInf ? 0.f : __expf(sg[nb] - mn);
-        ps += p;
-        p_s[w][(4 * g4 + i) * PLD + 16 * nb + r16] = to_bf16(p);
+    for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+      for (int i = 0; i < 4; i += 2) {
+        const float p0 = mn == kNegInf ? 0.f : __expf(sg[nb][i] - mn);
+        const float p1 = mn == kNegInf ? 0.f : __expf(sg[nb][i + 1] - mn);
+        ps += p0 + p1;
+        pw[nb * 2 + i / 2] = (uint32_t)to_bf16(p0) | ((uint32_t)to_bf16(p1) << 16);
       }
-      l_i[i] = l_i[i] * alpha[i] + row16_sum(ps);
-      m_i[i] = mn;
-    }
+    l_i = l_i * alpha + row4_sum(ps);
+    m_i = mn;
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) acc[db][i] *= alpha[i];
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    // acc += P V: A = P rows (16 x 32 keys), B = V^T (32 keys x 16 dims)
+    for (int db = 0; db < DB; ++db) acc[db] *= alpha;
+    // O^T += V^T P^T over the two 32-key chunks; chunk kk holds keys 4 g4 + j (j < 4)
+    // and 16 + 4 g4 + j - 4 (j >= 4), on both operands
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      const bf16x8 pa = __builtin_bit_cast(
-          bf16x8, *reinterpret_cast<const uint4*>(&p_s[w][r16 * PLD + 32 * kk + 8 * g4]));
+      const u32x4 pb = {pw[4 * kk + 0], pw[4 * kk + 1], pw[4 * kk + 2], pw[4 * kk + 3]};
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const bf16x8 bv = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const uint4*>(&vt_s[(16 * db + r16) * VLD + 32 * kk + 8 * g4]));
-        acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, bv, acc[db], 0, 0, 0);
+        const uint16_t* vp = &v_s[32 * kk * LD + 16 * db + vt_off];
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) i16x4*)(vp));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) i16x4*)(vp + 16 * LD));
+        const u32x4 va = {(uint32_t)(uint16_t)lo[0] | ((uint32_t)(uint16_t)lo[1] << 16),
+                          (uint32_t)(uint16_t)lo[2] | ((uint32_t)(uint16_t)lo[3] << 16),
+                          (uint32_t)(uint16_t)hi[0] | ((uint32_t)(uint16_t)hi[1] << 16),
+                          (uint32_t)(uint16_t)hi[2] | ((uint32_t)(uint16_t)hi[3] << 16)};
+        acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, va),
+                                                           __builtin_bit_cast(bf16x8, pb), acc[db], 0, 0, 0);
       }
     }
-    __builtin_amdgcn_wave_barrier();
   }
-  // outputs: rows 4 g4 + i of the wavefront, dims 16 db + r16
+  // lane holds O[t][16 db + 4 g4 + i]
+  const float rs = row4_sum(r_i);
+  if (t < a.T) {
+    const float inv = l_i > 0.f ? 1.0f / l_i : 0.f;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int t = t_i[i];
-    const float rs = row16_sum(r_i[i]);
-    if (t < a.T) {
-      const float inv = l_i[i] > 0.f ? 1.0f / l_i[i] : 0.f;
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-        a.out[(qrow0 + t) * D + 16 * db + r16] = to_bf16(acc[db][i] * inv);
-      if (r16 == 0) {
-        a.R[qrow0 + t] = t < Tb ? rs : 0.f;
-        a.L[qrow0 + t] = l_i[i] > 0.f ? m_i[i] + logf(l_i[i]) : kNegInf;
-      }
+    for (int db = 0; db < DB; ++db) {
+      const uint32_t lo = (uint32_t)to_bf16(acc[db][0] * inv) | ((uint32_t)to_bf16(acc[db][1] * inv) << 16);
+      const uint32_t hi = (uint32_t)to_bf16(acc[db][2] * inv) | ((uint32_t)to_bf16(acc[db][3] * inv) << 16);
+      *reinterpret_cast<uint2*>(a.out + (qrow0 + t) * D + 16 * db + 4 * g4) = make_uint2(lo, hi);
+    }
+    if (g4 == 0) {
+      a.R[qrow0 + t] = t < Tb ? rs : 0.f;
+      a.L[qrow0 + t] = l_i > 0.f ? m_i + logf(l_i) : kNegInf;
     }
   }
 }
