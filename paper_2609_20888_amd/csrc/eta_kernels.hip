@@ -36,11 +36,14 @@ __device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w <
 __device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
 // fp32 -> bf16, round to nearest even; NaN stays NaN.
+// fp32 -> bf16, round to nearest even (the hardware conversion, v_cvt_pk_bf16_f32)
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint16_t to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+  return __builtin_bit_cast(uint16_t, (__bf16)f);
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 // Element access for the two storage types: float and bf16 (raw uint16 bits).
@@ -789,7 +792,7 @@ template <bool DENSE>
 __device__ __forceinline__ float gated(float S, bool attend, bool ungated, float teff, float beta) {
   if (!attend) return kNegInf;
   if (DENSE || ungated || teff == kNegInf) return S;
-  return S / (1.0f + __expf(-beta * (S - teff)));
+  return S * __builtin_amdgcn_rcpf(1.0f + __expf(-beta * (S - teff)));
 }
 
 // Online-softmax update of one head with this lane's score `sc`; returns the
@@ -1551,7 +1554,12 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
   const int nkb = last_row >= 0 ? last_row / kPfK + 1 : 0;
   u32x4 kr[LPT], vr[LPT];
   if (nkb > 0) prefill_load_kv<D, LPT>(kh, vh, 0, a.T, tid, kr, vr);
-  for (int kb = 0; kb < nkb; ++kb) {
+  // One key block.  MASKED: the last block, the only one that can hold keys past
+  // a row (causality, sequence end) or the row's own key; in every earlier block
+  // each key precedes every row of the workgroup.  Rows at or past the sequence's
+  // end compute on regardless and are cleared when stored.
+  auto block = [&](int kb, auto masked_tag) {
+    constexpr bool MASKED = decltype(masked_tag)::value;
     __syncthreads();                       // every wavefront is done with the previous block
 #pragma unroll
     for (int u = 0; u < LPT; ++u) {
@@ -1582,15 +1590,20 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
     for (int nb = 0; nb < 4; ++nb)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int s = kb * kPfK + 16 * nb + 4 * g4 + i;
-        const bool valid = s <= t && t < Tb;
         const float S = c[nb][i] * scale;
-        const float gate = 1.0f / (1.0f + __expf(-a.beta * (S - tau_t)));
-        r_i += valid ? gate : 0.f;
+        const float gate = __builtin_amdgcn_rcpf(1.0f + __expf(-a.beta * (S - tau_t)));
         float x = a.additive ? S + a.C * gate - a.C : S * gate;
-        if (s == t) x = S;
-        sg[nb][i] = valid ? x : kNegInf;
-        mx = fmaxf(mx, sg[nb][i]);
+        if constexpr (MASKED) {
+          const int s = kb * kPfK + 16 * nb + 4 * g4 + i;
+          const bool valid = s <= t && t < Tb;
+          r_i += valid ? gate : 0.f;
+          if (s == t) x = S;
+          x = valid ? x : kNegInf;
+        } else {
+          r_i += gate;
+        }
+        sg[nb][i] = x;
+        mx = fmaxf(mx, x);
       }
     mx = row4_max(mx);
     const float mn = fmaxf(m_i, mx);
@@ -1601,10 +1614,13 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
     for (int nb = 0; nb < 4; ++nb)
 #pragma unroll
       for (int i = 0; i < 4; i += 2) {
-        const float p0 = mn == kNegInf ? 0.f : __expf(sg[nb][i] - mn);
-        const float p1 = mn == kNegInf ? 0.f : __expf(sg[nb][i + 1] - mn);
+        float p0 = __expf(sg[nb][i] - mn), p1 = __expf(sg[nb][i + 1] - mn);
+        if constexpr (MASKED) {
+          p0 = mn == kNegInf ? 0.f : p0;
+          p1 = mn == kNegInf ? 0.f : p1;
+        }
         ps += p0 + p1;
-        pw[nb * 2 + i / 2] = (uint32_t)to_bf16(p0) | ((uint32_t)to_bf16(p1) << 16);
+        pw[nb * 2 + i / 2] = pack_bf16x2(p0, p1);
       }
     l_i = l_i * alpha + row4_sum(ps);
     m_i = mn;
@@ -1630,20 +1646,23 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
                                                            __builtin_bit_cast(bf16x8, pb), acc[db], 0, 0, 0);
       }
     }
-  }
-  // lane holds O[t][16 db + 4 g4 + i]
+  };
+  for (int kb = 0; kb + 1 < nkb; ++kb) block(kb, std::integral_constant<bool, false>{});
+  if (nkb > 0) block(nkb - 1, std::integral_constant<bool, true>{});
+  // lane holds O[t][16 db + 4 g4 + i]; rows at or past the sequence's end are cleared
   const float rs = row4_sum(r_i);
   if (t < a.T) {
-    const float inv = l_i > 0.f ? 1.0f / l_i : 0.f;
+    const bool row_ok = t < Tb && l_i > 0.f;
+    const float inv = row_ok ? 1.0f / l_i : 0.f;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      const uint32_t lo = (uint32_t)to_bf16(acc[db][0] * inv) | ((uint32_t)to_bf16(acc[db][1] * inv) << 16);
-      const uint32_t hi = (uint32_t)to_bf16(acc[db][2] * inv) | ((uint32_t)to_bf16(acc[db][3] * inv) << 16);
+      const uint32_t lo = pack_bf16x2(acc[db][0] * inv, acc[db][1] * inv);
+      const uint32_t hi = pack_bf16x2(acc[db][2] * inv, acc[db][3] * inv);
       *reinterpret_cast<uint2*>(a.out + (qrow0 + t) * D + 16 * db + 4 * g4) = make_uint2(lo, hi);
     }
     if (g4 == 0) {
       a.R[qrow0 + t] = t < Tb ? rs : 0.f;
-      a.L[qrow0 + t] = l_i > 0.f ? m_i + logf(l_i) : kNegInf;
+      a.L[qrow0 + t] = row_ok ? m_i + logf(l_i) : kNegInf;
     }
   }
 }
