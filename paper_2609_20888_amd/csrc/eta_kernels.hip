@@ -1532,7 +1532,11 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
   const int64_t qrow0 = ((int64_t)b * a.Hq + h) * a.T;
   const uint16_t* kh = a.k + (((int64_t)b * a.Hkv + h / G) * a.T) * D;
   const uint16_t* vh = a.v + (((int64_t)b * a.Hkv + h / G) * a.T) * D;
-  const float scale = 1.0f / sqrtf((float)D);
+  // Softmax and gate in base-2 units: S' = S log2(e), so exp(S~ - m) = 2^(S~' - m')
+  // and sigmoid(beta (S - tau)) = 1 / (1 + 2^(-beta (S' - tau'))).
+  constexpr float kLog2e = 1.4426950408889634f;
+  const float scale2 = kLog2e / sqrtf((float)D);
+  const float C2 = a.C * kLog2e;
 
   // this lane's query row and its B operand (dims 32 kc + 8 g4 .. + 7)
   const int t = qblk * kPfQ + 16 * w + r16;
@@ -1541,7 +1545,7 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
   for (int kc = 0; kc < KC; ++kc)
     qb[kc] = *reinterpret_cast<const u32x4*>(a.q + (qrow0 + tq) * D + 32 * kc + 8 * g4);
-  const float tau_t = a.tau[qrow0 + tq];
+  const float btau2 = a.beta * a.tau[qrow0 + tq] * kLog2e;   // beta tau
   float m_i = kNegInf, l_i = 0.f, r_i = 0.f;
   f32x4 acc[DB];
 #pragma unroll
@@ -1584,20 +1588,21 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
                                                          __builtin_bit_cast(bf16x8, qb[kc]), c[nb], 0, 0, 0);
       }
     }
-    // gate, mask, online softmax of the lane's row
+    // gate, mask, online softmax of the lane's row (base-2 units)
     float sg[4][4], mx = kNegInf;
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float S = c[nb][i] * scale;
-        const float gate = __builtin_amdgcn_rcpf(1.0f + __expf(-a.beta * (S - tau_t)));
-        float x = a.additive ? S + a.C * gate - a.C : S * gate;
+        const float S2 = c[nb][i] * scale2;
+        const float gate =
+            __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(fmaf(-a.beta, S2, btau2)));
+        float x = a.additive ? fmaf(C2, gate, S2 - C2) : S2 * gate;
         if constexpr (MASKED) {
           const int s = kb * kPfK + 16 * nb + 4 * g4 + i;
           const bool valid = s <= t && t < Tb;
           r_i += valid ? gate : 0.f;
-          if (s == t) x = S;
+          if (s == t) x = S2;
           x = valid ? x : kNegInf;
         } else {
           r_i += gate;
@@ -1605,27 +1610,34 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
         sg[nb][i] = x;
         mx = fmaxf(mx, x);
       }
+    // The reference maximum moves only when some row's block maximum exceeds it by
+    // more than 8 (a wavefront-wide decision): the weights stay below 2^8, and the
+    // accumulators are rescaled only then, not on every block.
     mx = row4_max(mx);
-    const float mn = fmaxf(m_i, mx);
-    const float alpha = mn == kNegInf ? 1.f : __expf(m_i - mn);
+    if (__ballot(mx > m_i + 8.0f) != 0ull) {
+      const float mn = fmaxf(m_i, mx);
+      const float alpha = mn == kNegInf ? 1.f : __builtin_amdgcn_exp2f(m_i - mn);
+      l_i *= alpha;
+      m_i = mn;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) acc[db] *= alpha;
+    }
     float ps = 0.f;
     uint32_t pw[8];                        // bf16 pairs: B operands of the two 32-key chunks
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb)
 #pragma unroll
       for (int i = 0; i < 4; i += 2) {
-        float p0 = __expf(sg[nb][i] - mn), p1 = __expf(sg[nb][i + 1] - mn);
+        float p0 = __builtin_amdgcn_exp2f(sg[nb][i] - m_i);
+        float p1 = __builtin_amdgcn_exp2f(sg[nb][i + 1] - m_i);
         if constexpr (MASKED) {
-          p0 = mn == kNegInf ? 0.f : p0;
-          p1 = mn == kNegInf ? 0.f : p1;
+          p0 = m_i == kNegInf ? 0.f : p0;
+          p1 = m_i == kNegInf ? 0.f : p1;
         }
         ps += p0 + p1;
         pw[nb * 2 + i / 2] = pack_bf16x2(p0, p1);
       }
-    l_i = l_i * alpha + row4_sum(ps);
-    m_i = mn;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) acc[db] *= alpha;
+    l_i += row4_sum(ps);
     // O^T += V^T P^T over the two 32-key chunks; chunk kk holds keys 4 g4 + j (j < 4)
     // and 16 + 4 g4 + j - 4 (j >= 4), on both operands
 #pragma unroll
@@ -1662,7 +1674,7 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
     }
     if (g4 == 0) {
       a.R[qrow0 + t] = t < Tb ? rs : 0.f;
-      a.L[qrow0 + t] = row_ok ? m_i + logf(l_i) : kNegInf;
+      a.L[qrow0 + t] = row_ok ? (m_i + __log2f(l_i)) * 0.6931471805599453f : kNegInf;
     }
   }
 }
