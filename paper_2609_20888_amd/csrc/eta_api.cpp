@@ -176,9 +176,13 @@ LaunchHook active_hook() {
 }  // namespace
 
 int default_splits(const Geom& g) {
-  // about one resident round of split workgroups (two per compute unit)
+  // About one resident round of split workgroups.  One sequence: one workgroup
+  // per compute unit (256) -- a split streams as fast with four wavefronts per
+  // compute unit as with eight, and half the splits halve the combine's reads.
+  // Several sequences: two per compute unit (512), slack for ragged lengths.
   const int64_t groups = (int64_t)g.B * g.Hkv;
-  int64_t S = (512 + groups - 1) / groups;
+  const int64_t target = g.B == 1 ? 256 : 512;
+  int64_t S = (target + groups - 1) / groups;
   if (S > 256) S = 256;
   const int64_t half = g.ncap / 2 > 0 ? g.ncap / 2 : 1;
   if (S > half) S = half;
