@@ -1450,9 +1450,12 @@ __global__ __launch_bounds__(256) void calib_solve_kernel(CalibSolveArgs a) {
 // causal attention over gated scores S~ = S sigma(beta (S - tau_i)) (or the
 // additive S + C sigma - C), diagonal ungated, with the gate row sums R and the
 // log-sum-exp L.  One workgroup per (64-query block, query head, sequence),
-// longest blocks first; wavefront w owns query rows 16 w .. 16 w + 15.  Per
-// 64-key block the workgroup stages K and V row-major in LDS (the next block is
-// loaded into registers meanwhile).  Everything is computed transposed so that
+// longest blocks first; wavefront w owns query rows 16 w .. 16 w + 15.  K and
+// V blocks of 64 keys go straight from global memory into one of two LDS
+// buffers (global_load_lds, 16 bytes per lane, no staging registers) while the
+// other buffer is in use; rows are unpadded with their 16-byte chunks XOR
+// swizzled by row, so the column reads of all 16 rows hit distinct banks.  One
+// barrier per block.  Everything is computed transposed so that
 // each lane owns one query row: S^T = K Q^T on v_mfma_f32_16x16x32_bf16 (A = 16
 // keys x 32 dims from LDS, B = 32 dims x 16 queries from registers) gives lane l
 // the scores of query l & 15 against keys 4 (l >> 4) + i of each 16-key
@@ -1464,7 +1467,6 @@ __global__ __launch_bounds__(256) void calib_solve_kernel(CalibSolveArgs a) {
 
 constexpr int kPfQ = 64;     // query rows per workgroup
 constexpr int kPfK = 64;     // keys per block
-constexpr int kPfPad = 8;    // bf16 padding of LDS rows
 
 struct PrefillArgs {
   const uint16_t* q;
@@ -1477,7 +1479,6 @@ struct PrefillArgs {
   float* L;
   int Hq, Hkv, T;
   float beta, C;
-  int additive;
 };
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -1497,30 +1498,45 @@ __device__ __forceinline__ float row4_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// This thread's share of a 64-key block of K and V (rows past the cache read its last row).
-template <int D, int LPT>
-__device__ __forceinline__ void prefill_load_kv(const uint16_t* __restrict__ kh,
-                                                const uint16_t* __restrict__ vh, int kb, int T,
-                                                int tid, u32x4 (&kr)[LPT], u32x4 (&vr)[LPT]) {
+// Swizzled 16-byte chunk of (row, chunk) in an unpadded LDS tile of rows of D
+// bf16: rows sharing a 256-byte bank line are XORed with different values.
+template <int D>
+__device__ __forceinline__ int pf_chunk(int row, int chunk) {
+  constexpr int CPR = D / 8, RPL = 128 / D;   // chunks per row, rows per 256 bytes
+  return chunk ^ ((row / RPL) & (CPR - 1));
+}
+
+// Issue the DMA of key block kb of K and V into an LDS buffer pair: LDS slot
+// u (16 bytes, in order) holds row u / CPR, physical chunk u % CPR, i.e. the
+// global chunk that the swizzle maps there (rows past the cache read its last row).
+template <int D>
+__device__ __forceinline__ void prefill_dma(const uint16_t* __restrict__ kh,
+                                            const uint16_t* __restrict__ vh, int kb, int T,
+                                            uint16_t* kdst, uint16_t* vdst, int tid) {
   constexpr int CPR = D / 8;
+  constexpr int NI = kPfK * CPR / 256;          // 16-byte slots per thread
 #pragma unroll
-  for (int u = 0; u < LPT; ++u) {
-    const int c = tid + 256 * u;
-    const int row = min(kb * kPfK + c / CPR, T - 1);
-    kr[u] = *reinterpret_cast<const u32x4*>(kh + (int64_t)row * D + 8 * (c % CPR));
-    vr[u] = *reinterpret_cast<const u32x4*>(vh + (int64_t)row * D + 8 * (c % CPR));
+  for (int j = 0; j < NI; ++j) {
+    const int u = 256 * j + tid;
+    const int row = u / CPR, pc = u % CPR;
+    const int grow = min(kb * kPfK + row, T - 1);
+    const int64_t src = (int64_t)grow * D + 8 * pf_chunk<D>(row, pc);
+    const int wave_slot = 256 * j + (tid & ~63);  // wave-uniform LDS base (16-byte slots)
+    __builtin_amdgcn_global_load_lds((const void*)(kh + src),
+                                     (__attribute__((address_space(3))) void*)(kdst + 8 * wave_slot),
+                                     16, 0, 0);
+    __builtin_amdgcn_global_load_lds((const void*)(vh + src),
+                                     (__attribute__((address_space(3))) void*)(vdst + 8 * wave_slot),
+                                     16, 0, 0);
   }
 }
 
-template <int D>
+template <int D, bool ADD>
 __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
   constexpr int KC = D / 32;             // 32-dim chunks (score contraction)
   constexpr int DB = D / 16;             // 16-dim output blocks
-  constexpr int LD = D + kPfPad;         // K / V row stride in LDS (bf16)
-  constexpr int CPR = D / 8;             // 16-byte chunks per row
-  constexpr int LPT = kPfK * CPR / 256;  // chunks per thread per block
-  __shared__ __attribute__((aligned(16))) uint16_t k_s[kPfK * LD];
-  __shared__ __attribute__((aligned(16))) uint16_t v_s[kPfK * LD];
+  __shared__ __attribute__((aligned(16))) uint16_t k_s[2][kPfK * D];
+  __shared__ __attribute__((aligned(16))) uint16_t v_s[2][kPfK * D];
 
   const int nqb = (a.T + kPfQ - 1) / kPfQ;
   const int qblk = nqb - 1 - (int)blockIdx.x;        // longest causal ranges first
@@ -1550,31 +1566,26 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
   f32x4 acc[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // transpose-read address of V: the lane provides key 4 g4 + (r16 >> 2) (+16 for keys
-  // 16..31 of a 32-key chunk), dims 4 (lane & 3) of a 16-dim block
-  const int vt_off = (4 * g4 + (r16 >> 2)) * LD + 4 * (lane & 3);
+  // transpose reads of V: the lane provides key 4 g4 + (r16 >> 2) (+16 for keys
+  // 16..31 of a 32-key chunk) and dims 4 (lane & 3) .. + 3 of a 16-dim block
+  const int vt_row = 4 * g4 + (r16 >> 2), vt_c = lane & 3;
 
   const int last_row = min(qblk * kPfQ + kPfQ, Tb) - 1;
   const int nkb = last_row >= 0 ? last_row / kPfK + 1 : 0;
-  u32x4 kr[LPT], vr[LPT];
-  if (nkb > 0) prefill_load_kv<D, LPT>(kh, vh, 0, a.T, tid, kr, vr);
+  if (nkb > 0) prefill_dma<D>(kh, vh, 0, a.T, k_s[0], v_s[0], tid);
   // One key block.  MASKED: the last block, the only one that can hold keys past
   // a row (causality, sequence end) or the row's own key; in every earlier block
   // each key precedes every row of the workgroup.  Rows at or past the sequence's
   // end compute on regardless and are cleared when stored.
   auto block = [&](int kb, auto masked_tag) {
     constexpr bool MASKED = decltype(masked_tag)::value;
-    __syncthreads();                       // every wavefront is done with the previous block
-#pragma unroll
-    for (int u = 0; u < LPT; ++u) {
-      const int c = tid + 256 * u;
-      *reinterpret_cast<u32x4*>(&k_s[(c / CPR) * LD + 8 * (c % CPR)]) = kr[u];
-      *reinterpret_cast<u32x4*>(&v_s[(c / CPR) * LD + 8 * (c % CPR)]) = vr[u];
-    }
+    // this thread's DMA of block kb is done; after the barrier everyone's is, and
+    // everyone is done with block kb - 1, whose buffer the next DMA overwrites
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    // the next block's loads are in flight during this block's arithmetic (the last
-    // iteration reloads its own block: an unconditional load keeps one copy of kr, vr)
-    prefill_load_kv<D, LPT>(kh, vh, kb + 1 < nkb ? kb + 1 : kb, a.T, tid, kr, vr);
+    if (kb + 1 < nkb) prefill_dma<D>(kh, vh, kb + 1, a.T, k_s[(kb + 1) & 1], v_s[(kb + 1) & 1], tid);
+    const uint16_t* kt = k_s[kb & 1];
+    const uint16_t* vt = v_s[kb & 1];
 
     // S^T: lane holds query t against keys 16 nb + 4 g4 + i
     f32x4 c[4];
@@ -1583,7 +1594,8 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
       c[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kc = 0; kc < KC; ++kc) {
-        const u32x4 ka = *reinterpret_cast<const u32x4*>(&k_s[(16 * nb + r16) * LD + 32 * kc + 8 * g4]);
+        const int krow = 16 * nb + r16;
+        const u32x4 ka = *reinterpret_cast<const u32x4*>(&kt[krow * D + 8 * pf_chunk<D>(krow, 4 * kc + g4)]);
         c[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka),
                                                          __builtin_bit_cast(bf16x8, qb[kc]), c[nb], 0, 0, 0);
       }
@@ -1597,7 +1609,7 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
         const float S2 = c[nb][i] * scale2;
         const float gate =
             __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(fmaf(-a.beta, S2, btau2)));
-        float x = a.additive ? fmaf(C2, gate, S2 - C2) : S2 * gate;
+        float x = ADD ? fmaf(C2, gate, S2 - C2) : S2 * gate;
         if constexpr (MASKED) {
           const int s = kb * kPfK + 16 * nb + 4 * g4 + i;
           const bool valid = s <= t && t < Tb;
@@ -1645,11 +1657,12 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
       const u32x4 pb = {pw[4 * kk + 0], pw[4 * kk + 1], pw[4 * kk + 2], pw[4 * kk + 3]};
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const uint16_t* vp = &v_s[32 * kk * LD + 16 * db + vt_off];
+        const int r0 = 32 * kk + vt_row, r1 = r0 + 16;
+        const int lc = 2 * db + (vt_c >> 1), half = 4 * (vt_c & 1);
         const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) i16x4*)(vp));
+            (__attribute__((address_space(3))) i16x4*)(&vt[r0 * D + 8 * pf_chunk<D>(r0, lc) + half]));
         const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) i16x4*)(vp + 16 * LD));
+            (__attribute__((address_space(3))) i16x4*)(&vt[r1 * D + 8 * pf_chunk<D>(r1, lc) + half]));
         const u32x4 va = {(uint32_t)(uint16_t)lo[0] | ((uint32_t)(uint16_t)lo[1] << 16),
                           (uint32_t)(uint16_t)lo[2] | ((uint32_t)(uint16_t)lo[3] << 16),
                           (uint32_t)(uint16_t)hi[0] | ((uint32_t)(uint16_t)hi[1] << 16),
@@ -1939,11 +1952,16 @@ hipError_t launch_prefill(const eta_prefill_desc_t& pd, const void* q, const voi
   PrefillArgs pa{reinterpret_cast<const uint16_t*>(q), reinterpret_cast<const uint16_t*>(k),
                  reinterpret_cast<const uint16_t*>(v), tau, seq_lens,
                  reinterpret_cast<uint16_t*>(out), R, L, pd.num_q_heads, pd.num_kv_heads,
-                 pd.capacity_tokens, pd.beta, pd.C, pd.additive};
+                 pd.capacity_tokens, pd.beta, pd.C};
   dim3 grid((pd.capacity_tokens + kPfQ - 1) / kPfQ, pd.num_q_heads, pd.batch);
   return with_hook(hook, ETA_KERNEL_PREFILL, stream, [&] {
-    if (pd.head_dim == 64) hipLaunchKernelGGL(prefill_kernel<64>, grid, dim3(256), 0, stream, pa);
-    if (pd.head_dim == 128) hipLaunchKernelGGL(prefill_kernel<128>, grid, dim3(256), 0, stream, pa);
+    if (pd.additive) {
+      if (pd.head_dim == 64) hipLaunchKernelGGL((prefill_kernel<64, true>), grid, dim3(256), 0, stream, pa);
+      if (pd.head_dim == 128) hipLaunchKernelGGL((prefill_kernel<128, true>), grid, dim3(256), 0, stream, pa);
+    } else {
+      if (pd.head_dim == 64) hipLaunchKernelGGL((prefill_kernel<64, false>), grid, dim3(256), 0, stream, pa);
+      if (pd.head_dim == 128) hipLaunchKernelGGL((prefill_kernel<128, false>), grid, dim3(256), 0, stream, pa);
+    }
   });
 }
 
