@@ -4,7 +4,9 @@
 
 hipcc compiles the kernels and the host API into one shared library beside
 this file.  Packed-fp32 instruction selection is disabled for device code
-(`-target-feature -packed-fp32-ops`).
+(`-target-feature -packed-fp32-ops`), and MFMA accumulators are kept in the
+ordinary vector registers (`-amdgpu-mfma-vgpr-form`): the prefill kernel then
+needs no copies between accumulation and arithmetic registers.
 """
 import os
 import subprocess
@@ -28,6 +30,7 @@ def hipcc() -> str:
 def build(verbose: bool = False, jobs: int = 2) -> str:
     cmd = [hipcc(), "-O3", "-std=c++17", f"--offload-arch={ARCH}", "-shared", "-fPIC",
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           "-mllvm", "-amdgpu-mfma-vgpr-form",
            "-Wall", "-Wno-unused-function",
            f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}",
            *SOURCES, "-o", OUT + ".tmp"]
