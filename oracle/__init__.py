@@ -80,6 +80,11 @@ def _load():
     lib.eta_oracle_prefill.argtypes = [_vp, _vp, _vp, ctypes.c_int, _vp, _vp, ctypes.c_int,
                                        ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                        ctypes.c_double, ctypes.c_int, ctypes.c_double, _vp, _vp, _vp]
+    lib.eta_oracle_prefill_rows.restype = None
+    lib.eta_oracle_prefill_rows.argtypes = [_vp, _vp, _vp, ctypes.c_int, _vp, _vp, ctypes.c_int,
+                                            ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                            ctypes.c_double, ctypes.c_int, ctypes.c_double, _vp,
+                                            ctypes.c_int, _vp, _vp, _vp]
     lib.eta_oracle_round_f16.restype = ctypes.c_double
     lib.eta_oracle_round_f16.argtypes = [ctypes.c_double]
     lib.eta_oracle_round_f16_array.restype = None
@@ -388,4 +393,28 @@ def prefill(q: np.ndarray, k: np.ndarray, v: np.ndarray, tau: np.ndarray, seq_le
     _load().eta_oracle_prefill(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), _ptr(tau), _ptr(sl), B, Hq,
                                Hkv, T, d, float(beta), int(bool(additive)), float(C), _ptr(r.o),
                                _ptr(r.r), _ptr(r.lse))
+    return r
+
+
+def prefill_rows(q: np.ndarray, k: np.ndarray, v: np.ndarray, tau: np.ndarray,
+                 seq_lens: Sequence[int], rows: np.ndarray, *, beta: float, additive: bool = False,
+                 C: float = 0.0) -> PrefillResult:
+    """The rows (b, h, i) of `rows` ([n][3]) of prefill(...), computed alone (same per-row
+    arithmetic): o [n][d], r, lse [n].  For sampling long sequences."""
+    q, k, v = _c(q), _c(k), _c(v)
+    B, Hq, T, d = q.shape
+    Hkv = k.shape[1]
+    assert k.shape == (B, Hkv, T, d) and v.shape == k.shape and Hq % Hkv == 0
+    assert _dtype_code(q) == _dtype_code(k) == _dtype_code(v)
+    tau = np.ascontiguousarray(np.asarray(tau, np.float64))
+    assert tau.shape == (B, Hq, T)
+    rows = np.ascontiguousarray(np.asarray(rows, np.int32).reshape(-1, 3))
+    assert np.all((rows[:, 0] >= 0) & (rows[:, 0] < B) & (rows[:, 1] >= 0) & (rows[:, 1] < Hq)
+                  & (rows[:, 2] >= 0) & (rows[:, 2] < T))
+    sl = np.ascontiguousarray(np.asarray(seq_lens, np.int32))
+    n = rows.shape[0]
+    r = PrefillResult(o=np.zeros((n, d)), r=np.zeros(n), lse=np.zeros(n))
+    _load().eta_oracle_prefill_rows(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), _ptr(tau), _ptr(sl),
+                                    B, Hq, Hkv, T, d, float(beta), int(bool(additive)), float(C),
+                                    _ptr(rows), n, _ptr(r.o), _ptr(r.r), _ptr(r.lse))
     return r

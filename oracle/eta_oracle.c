@@ -527,51 +527,78 @@ double eta_oracle_calib_solve(const double* hist, int nb, double lo, double hi, 
  * Layouts q, O [B][Hq][T][d], k, v [B][Hkv][T][d] (fp32 or bf16 words),
  * tau, R, L [B][Hq][T].  Rows i >= T_b: O = 0, R = 0, L = -inf.
  */
+/* One row (b, h, i) of the above; st is scratch of at least i + 1 doubles. */
+static void prefill_row(const void* q, const void* k, const void* v, int dt, const double* tau,
+                        const int32_t* seq_lens, int Hq, int Hkv, int T, int d, double beta,
+                        int additive, double C, int b, int h, int i, double* o, double* R_out,
+                        double* L_out, double* st) {
+  const int G = Hq / Hkv;
+  const double scale = 1.0 / sqrt((double)d);
+  const int Tb = seq_lens[b] < 0 ? 0 : (seq_lens[b] > T ? T : seq_lens[b]);
+  const int64_t qb = (((int64_t)b * Hq + h) * T) * d;
+  const int64_t kb = (((int64_t)b * Hkv + h / G) * T) * d;
+  const int64_t row = ((int64_t)b * Hq + h) * T + i;
+  for (int c = 0; c < d; ++c) o[c] = 0.0;
+  if (i >= Tb) {
+    *R_out = 0.0;
+    *L_out = -INFINITY;
+    return;
+  }
+  double rsum = 0.0, m = -INFINITY;
+  for (int j = 0; j <= i; ++j) {
+    double dot = 0.0;
+    for (int c = 0; c < d; ++c)
+      dot += ld(q, dt, qb + (int64_t)i * d + c) * ld(k, dt, kb + (int64_t)j * d + c);
+    const double S = dot * scale;
+    const double g = sigmoid(beta * (S - tau[row]));
+    rsum += g;
+    double Sg = additive ? S + C * g - C : S * g;
+    if (j == i) Sg = S;
+    st[j] = Sg;
+    if (Sg > m) m = Sg;
+  }
+  double l = 0.0;
+  for (int j = 0; j <= i; ++j) {
+    const double w = exp(st[j] - m);
+    l += w;
+    for (int c = 0; c < d; ++c) o[c] += w * ld(v, dt, kb + (int64_t)j * d + c);
+  }
+  for (int c = 0; c < d; ++c) o[c] /= l;
+  *R_out = rsum;
+  *L_out = m + log(l);
+}
+
 void eta_oracle_prefill(const void* q, const void* k, const void* v, int dt, const double* tau,
                         const int32_t* seq_lens, int B, int Hq, int Hkv, int T, int d, double beta,
                         int additive, double C, double* O, double* R, double* L) {
-  const int G = Hq / Hkv;
-  const double scale = 1.0 / sqrt((double)d);
 #pragma omp parallel for collapse(2) schedule(dynamic, 1)
   for (int b = 0; b < B; ++b) {
     for (int h = 0; h < Hq; ++h) {
-      const int Tb = seq_lens[b] < 0 ? 0 : (seq_lens[b] > T ? T : seq_lens[b]);
-      const int64_t qb = (((int64_t)b * Hq + h) * T) * d;
-      const int64_t kb = (((int64_t)b * Hkv + h / G) * T) * d;
       double* st = (double*)malloc(sizeof(double) * (size_t)(T > 0 ? T : 1));
       for (int i = 0; i < T; ++i) {
         const int64_t row = ((int64_t)b * Hq + h) * T + i;
-        double* o = O + row * d;
-        for (int c = 0; c < d; ++c) o[c] = 0.0;
-        if (i >= Tb) {
-          R[row] = 0.0;
-          L[row] = -INFINITY;
-          continue;
-        }
-        double rsum = 0.0, m = -INFINITY;
-        for (int j = 0; j <= i; ++j) {
-          double dot = 0.0;
-          for (int c = 0; c < d; ++c)
-            dot += ld(q, dt, qb + (int64_t)i * d + c) * ld(k, dt, kb + (int64_t)j * d + c);
-          const double S = dot * scale;
-          const double g = sigmoid(beta * (S - tau[row]));
-          rsum += g;
-          double Sg = additive ? S + C * g - C : S * g;
-          if (j == i) Sg = S;
-          st[j] = Sg;
-          if (Sg > m) m = Sg;
-        }
-        double l = 0.0;
-        for (int j = 0; j <= i; ++j) {
-          const double w = exp(st[j] - m);
-          l += w;
-          for (int c = 0; c < d; ++c) o[c] += w * ld(v, dt, kb + (int64_t)j * d + c);
-        }
-        for (int c = 0; c < d; ++c) o[c] /= l;
-        R[row] = rsum;
-        L[row] = m + log(l);
+        prefill_row(q, k, v, dt, tau, seq_lens, Hq, Hkv, T, d, beta, additive, C, b, h, i,
+                    O + row * d, R + row, L + row, st);
       }
       free(st);
     }
+  }
+}
+
+/*
+ * The same outputs for n selected rows only: rows[3 r .. 3 r + 2] = (b, h, i);
+ * O [n][d], R, L [n].  For checking long sequences on a sample of rows.
+ */
+void eta_oracle_prefill_rows(const void* q, const void* k, const void* v, int dt,
+                             const double* tau, const int32_t* seq_lens, int B, int Hq, int Hkv,
+                             int T, int d, double beta, int additive, double C,
+                             const int32_t* rows, int n, double* O, double* R, double* L) {
+  (void)B;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int r = 0; r < n; ++r) {
+    double* st = (double*)malloc(sizeof(double) * (size_t)(T > 0 ? T : 1));
+    prefill_row(q, k, v, dt, tau, seq_lens, Hq, Hkv, T, d, beta, additive, C, rows[3 * r],
+                rows[3 * r + 1], rows[3 * r + 2], O + (int64_t)r * d, R + r, L + r, st);
+    free(st);
   }
 }

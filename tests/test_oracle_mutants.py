@@ -46,10 +46,10 @@ MUTANTS = {
     "calib_weight_off_by_one": ("const double wt = 1.0 / (double)(t + 1);", "const double wt = 1.0 / (double)(t + 2);"),
     "calib_not_causal_diag": ("for (int s2 = 0; s2 <= t; ++s2) {", "for (int s2 = 0; s2 < t || s2 == 0; ++s2) {"),
     "calib_bin_left_edge": ("g += hist[b] * sigmoid(beta * (lo + ((double)b + 0.5) * w - c));", "g += hist[b] * sigmoid(beta * (lo + (double)b * w - c));"),
-    "prefill_diagonal_gated": ("          if (j == i) Sg = S;", "          ;"),
-    "prefill_r_without_diagonal": ("          rsum += g;", "          if (j < i) rsum += g;"),
+    "prefill_diagonal_gated": ("    if (j == i) Sg = S;", "    ;"),
+    "prefill_r_without_diagonal": ("    rsum += g;", "    if (j < i) rsum += g;"),
     "prefill_additive_sign": ("double Sg = additive ? S + C * g - C : S * g;", "double Sg = additive ? S - C * g + C : S * g;"),
-    "prefill_lse_without_max": ("        L[row] = m + log(l);", "        L[row] = log(l);"),
+    "prefill_lse_without_max": ("  *L_out = m + log(l);", "  *L_out = log(l);"),
     "calib_bisect_direction": ("if (eta_oracle_calib_g(hist, nb, lo, hi, beta, m) > target) a = m; else b = m;", "if (eta_oracle_calib_g(hist, nb, lo, hi, beta, m) < target) a = m; else b = m;"),
 }
 

@@ -603,3 +603,17 @@ def test_prefill_matches_brute_force_definition():
                 np.testing.assert_allclose(r.o[0, h, i], o, atol=1e-12)
                 assert abs(r.r[0, h, i] - gs) < 1e-12
                 assert abs(r.lse[0, h, i] - (mx + math.log(sum(w)))) < 1e-12
+
+
+def test_prefill_rows_are_the_full_rows():
+    """prefill_rows (sampled rows of long sequences) returns exactly the rows of the
+    pinned full forward, rows past a sequence's length included."""
+    q, k, v = _prefill_inputs(17, B=2, Hq=4, Hkv=2, T=40, d=16)
+    tau = np.random.default_rng(18).normal(0.2, 0.5, (2, 4, 40))
+    for additive in (False, True):
+        full = oracle.prefill(q, k, v, tau, [40, 23], beta=3.0, additive=additive, C=1.5)
+        rows = np.array([[0, 0, 0], [0, 3, 39], [1, 2, 22], [1, 1, 23], [1, 0, 39], [0, 1, 17]])
+        r = oracle.prefill_rows(q, k, v, tau, [40, 23], rows, beta=3.0, additive=additive, C=1.5)
+        for n, (b, h, i) in enumerate(rows):
+            np.testing.assert_array_equal(r.o[n], full.o[b, h, i])
+            assert r.r[n] == full.r[b, h, i] and r.lse[n] == full.lse[b, h, i]
