@@ -37,7 +37,9 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0
 PRIMARY_SURVIVAL = 0.20
 SWEEP = (0.01, 0.05, 0.20, 1.00)
-KERNEL_SRC = os.path.join(ROOT, "paper_2609_20888_amd", "csrc", "eta_kernels.hip")
+# sources of the decode-path kernels: the counter file's traffic is valid only for these
+DECODE_SRCS = [os.path.join(ROOT, "paper_2609_20888_amd", "csrc", f)
+               for f in ("eta_kernels.hip", "eta_device.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "split_decode_512k_traffic.json")
 
 
@@ -46,8 +48,11 @@ def log(*a):
 
 
 def kernel_src_sha() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in DECODE_SRCS:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def parse():
@@ -60,6 +65,8 @@ def parse():
                     help="approximate CPU time budget of the oracle baseline")
     ap.add_argument("--no-prefill", action="store_true",
                     help="skip the gated prefill forward measurement")
+    ap.add_argument("--prefill-only", action="store_true",
+                    help="measure only the gated prefill forward and print its JSON (profiling)")
     ap.add_argument("--no-calibration", action="store_true",
                     help="skip the offline threshold calibration measurement")
     ap.add_argument("--only-primary", action="store_true",
@@ -71,6 +78,34 @@ def parse():
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run a plain device copy of this size (counter calibration)")
     return ap.parse_args()
+
+
+def measure_prefill(torch, eta, dev):
+    """Gated prefill / training forward: one 16K-token sequence at the ragged
+    workload's head shape (32 query / 8 kv heads, d = 128), bf16, causal."""
+    pB, pHq, pHkv, pT, pd = 1, 32, 8, 16384, 128
+    g = torch.Generator(device=dev).manual_seed(10)
+    pq = torch.randn(pB, pHq, pT, pd, generator=g, device=dev).to(torch.bfloat16)
+    pk = torch.randn(pB, pHkv, pT, pd, generator=g, device=dev).to(torch.bfloat16)
+    pv = torch.randn(pB, pHkv, pT, pd, generator=g, device=dev).to(torch.bfloat16)
+    ptau = 0.5 + 0.5 * torch.randn(pB, pHq, pT, generator=g, device=dev)
+    psl = torch.full((pB,), pT, dtype=torch.int32, device=dev)
+    pout, pR, pL = eta.gated_prefill(pq, pk, pv, ptau, psl, beta=4.0)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 5
+    e0.record()
+    for _ in range(reps):
+        eta.gated_prefill(pq, pk, pv, ptau, psl, beta=4.0, out=pout, R=pR, L=pL)
+    e1.record()
+    torch.cuda.synchronize()
+    pms = e0.elapsed_time(e1) / reps
+    pflops = 4.0 * pd * pHq * pT * (pT + 1) / 2      # QK^T and p.V over the causal pairs
+    prefill = {"workload": f"B={pB}, {pT} tokens, {pHq}/{pHkv} heads, d={pd}, bf16, causal",
+               "ms": round(pms, 3), "tflops": round(pflops / pms / 1e9, 1),
+               "frac_of_bf16_mfma_peak": round(pflops / pms / 1e9 / 2500.0, 4)}
+    log(f"[bench] gated prefill: {prefill}")
+    return prefill
 
 
 def main():
@@ -93,6 +128,9 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     eta.load_library()
+    if args.prefill_only:
+        print(json.dumps({"gated_prefill": measure_prefill(torch, eta, dev)}), flush=True)
+        return
 
     log("[bench] generating the 512K workload on the GPU")
     wl = config4(device=dev, survival=PRIMARY_SURVIVAL)
@@ -341,33 +379,8 @@ def main():
         log(f"[bench] calibration: {calib}")
         del cs, cal
 
-    # ---- gated prefill / training forward: one 16K-token sequence at the ragged
-    # workload's head shape (32 query / 8 kv heads, d = 128), bf16
-    prefill = None
-    if not args.no_prefill:
-        pB, pHq, pHkv, pT, pd = 1, 32, 8, 16384, 128
-        g = torch.Generator(device=dev).manual_seed(10)
-        pq = torch.randn(pB, pHq, pT, pd, generator=g, device=dev).to(torch.bfloat16)
-        pk = torch.randn(pB, pHkv, pT, pd, generator=g, device=dev).to(torch.bfloat16)
-        pv = torch.randn(pB, pHkv, pT, pd, generator=g, device=dev).to(torch.bfloat16)
-        ptau = 0.5 + 0.5 * torch.randn(pB, pHq, pT, generator=g, device=dev)
-        psl = torch.full((pB,), pT, dtype=torch.int32, device=dev)
-        pout, pR, pL = eta.gated_prefill(pq, pk, pv, ptau, psl, beta=4.0)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        reps = 5
-        e0.record()
-        for _ in range(reps):
-            eta.gated_prefill(pq, pk, pv, ptau, psl, beta=4.0, out=pout, R=pR, L=pL)
-        e1.record()
-        torch.cuda.synchronize()
-        pms = e0.elapsed_time(e1) / reps
-        pflops = 4.0 * pd * pHq * pT * (pT + 1) / 2      # QK^T and p.V over the causal pairs
-        prefill = {"workload": f"B={pB}, {pT} tokens, {pHq}/{pHkv} heads, d={pd}, bf16, causal",
-                   "ms": round(pms, 3), "tflops": round(pflops / pms / 1e9, 1),
-                   "frac_of_bf16_mfma_peak": round(pflops / pms / 1e9 / 2500.0, 4)}
-        log(f"[bench] gated prefill: {prefill}")
-        del pq, pk, pv, ptau, pout, pR, pL
+    # ---- gated prefill / training forward
+    prefill = None if args.no_prefill else measure_prefill(torch, eta, dev)
 
     ms, gpu_ms, kt, kv_b, step_b, ub, dh, du, steps, warm, cold_ms = primary
     split_ms, split_n = kt["split_decode"]

@@ -2,21 +2,25 @@
 
     python -m paper_2609_20888_amd.build [-v]
 
-hipcc compiles the kernels and the host API into one shared library beside
-this file.  Packed-fp32 instruction selection is disabled for device code
+hipcc compiles the kernel sources and the host API to objects (in parallel)
+and links them into one shared library beside this file.  Packed-fp32
+instruction selection is disabled for device code
 (`-target-feature -packed-fp32-ops`), and MFMA accumulators are kept in the
 ordinary vector registers (`-amdgpu-mfma-vgpr-form`): the prefill kernel then
 needs no copies between accumulation and arithmetic registers.
 """
 import os
+import shutil
 import subprocess
 import sys
+import tempfile
+import time
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libeta.so")
-SOURCES = [os.path.join(CSRC, "eta_kernels.hip"), os.path.join(CSRC, "eta_api.cpp")]
+SOURCES = [os.path.join(CSRC, f) for f in ("eta_kernels.hip", "eta_prefill.hip", "eta_api.cpp")]
 ARCH = "gfx950"
 
 
@@ -27,24 +31,56 @@ def hipcc() -> str:
     return "hipcc"
 
 
-def build(verbose: bool = False, jobs: int = 2) -> str:
-    cmd = [hipcc(), "-O3", "-std=c++17", f"--offload-arch={ARCH}", "-shared", "-fPIC",
-           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           "-mllvm", "-amdgpu-mfma-vgpr-form",
-           "-Wall", "-Wno-unused-function",
-           f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}",
-           *SOURCES, "-o", OUT + ".tmp"]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    # hipcc's host pass does not know the packed-fp32 feature and says so; drop that line
-    noise = "'-packed-fp32-ops' is not a recognized feature"
-    err = "\n".join(l for l in r.stderr.splitlines() if noise not in l)
-    if r.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({r.returncode}):\n{err}")
-    if verbose and err.strip():
-        print(err, file=sys.stderr)
-    os.replace(OUT + ".tmp", OUT)
+def _flags():
+    return ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC",
+            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+            "-mllvm", "-amdgpu-mfma-vgpr-form",
+            "-Wall", "-Wno-unused-function",
+            f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}"]
+
+
+# hipcc's host pass does not know the packed-fp32 feature and says so; drop that line
+_NOISE = "'-packed-fp32-ops' is not a recognized feature"
+
+
+def _clean(stderr: str) -> str:
+    return "\n".join(l for l in stderr.splitlines() if _NOISE not in l)
+
+
+def build(verbose: bool = False, jobs: int = 3) -> str:
+    """Compile every source to an object (in parallel), then link libeta.so."""
+    objdir = tempfile.mkdtemp(prefix="eta_build_")
+    try:
+        cmds = [[hipcc(), *_flags(), "-c", src, "-o",
+                 os.path.join(objdir, os.path.basename(src) + ".o")] for src in SOURCES]
+        procs = []
+        for cmd in cmds:
+            if verbose:
+                print(" ".join(cmd), flush=True)
+            while len([p for p in procs if p.poll() is None]) >= max(1, jobs):
+                time.sleep(0.2)
+            procs.append(subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE,
+                                          text=True))
+        errs = []
+        for cmd, p in zip(cmds, procs):
+            _, err = p.communicate()
+            err = _clean(err)
+            if p.returncode != 0:
+                errs.append(f"hipcc failed ({p.returncode}) on {cmd[-3]}:\n{err}")
+            elif verbose and err.strip():
+                print(err, file=sys.stderr)
+        if errs:
+            raise RuntimeError("\n".join(errs))
+        link = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC",
+                *[c[-1] for c in cmds], "-o", OUT + ".tmp"]
+        if verbose:
+            print(" ".join(link), flush=True)
+        r = subprocess.run(link, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"link failed ({r.returncode}):\n{_clean(r.stderr)}")
+        os.replace(OUT + ".tmp", OUT)
+    finally:
+        shutil.rmtree(objdir, ignore_errors=True)
     return OUT
 
 

@@ -1,5 +1,5 @@
 // Internal declarations shared by the host API (eta_api.cpp) and the HIP
-// kernels (eta_kernels.hip).  Not part of the public ABI.
+// kernels (eta_kernels.hip, eta_prefill.hip).  Not part of the public ABI.
 #pragma once
 
 #include <hip/hip_runtime.h>
