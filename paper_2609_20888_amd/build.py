@@ -5,9 +5,8 @@
 hipcc compiles the kernel sources and the host API to objects (in parallel)
 and links them into one shared library beside this file.  Packed-fp32
 instruction selection is disabled for device code
-(`-target-feature -packed-fp32-ops`), and MFMA accumulators are kept in the
-ordinary vector registers (`-amdgpu-mfma-vgpr-form`): the prefill kernel then
-needs no copies between accumulation and arithmetic registers.
+(`-target-feature -packed-fp32-ops`); the prefill source keeps MFMA
+accumulators in the ordinary vector registers (`-amdgpu-mfma-vgpr-form`).
 """
 import os
 import shutil
@@ -31,10 +30,16 @@ def hipcc() -> str:
     return "hipcc"
 
 
-def _flags():
+# MFMA results kept in the ordinary vector registers: for the prefill kernel only
+# (no copies between accumulation and arithmetic registers there; the
+# calibration kernel is faster with the default register classes)
+VGPR_FORM = {"eta_prefill.hip"}
+
+
+def _flags(src: str):
+    extra = ["-mllvm", "-amdgpu-mfma-vgpr-form"] if os.path.basename(src) in VGPR_FORM else []
     return ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC",
-            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-            "-mllvm", "-amdgpu-mfma-vgpr-form",
+            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", *extra,
             "-Wall", "-Wno-unused-function",
             f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}"]
 
@@ -51,7 +56,7 @@ def build(verbose: bool = False, jobs: int = 3) -> str:
     """Compile every source to an object (in parallel), then link libeta.so."""
     objdir = tempfile.mkdtemp(prefix="eta_build_")
     try:
-        cmds = [[hipcc(), *_flags(), "-c", src, "-o",
+        cmds = [[hipcc(), *_flags(src), "-c", src, "-o",
                  os.path.join(objdir, os.path.basename(src) + ".o")] for src in SOURCES]
         procs = []
         for cmd in cmds:
