@@ -738,9 +738,11 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
 
 // ---------------------------------------------------------------- split decode
 //
-// One workgroup (4 wavefronts) per (split, kv head, sequence).  The split owns
-// a contiguous slice of the (sequence, kv head)'s union list; wavefront w takes
-// the slice's blocks w, w+4, ...  A block is processed 64 tokens at a time,
+// One workgroup (kSplitWaves wavefronts) per (split, kv head, sequence).  The
+// split owns a contiguous range of the (sequence, kv head)'s union list in
+// 64-token tiles (bf16; whole blocks for fp32), so split shares differ by at
+// most one tile; wavefront w takes the range's tiles w, w + kSplitWaves, ...
+// A block is processed 64 tokens at a time,
 // lane = token for the scores (each lane reads its own K row with 16-byte
 // loads) and lane = head-dimension pair for p.V (coalesced rows of V), with
 // the weights p passed through the wavefront's LDS slice.  A head skips blocks
@@ -1068,9 +1070,12 @@ __device__ __forceinline__ void attend_bf16_stream(const uint16_t* __restrict__ 
 }
 
 constexpr int kItemChunk = 256;
+// Wavefronts per split-decode workgroup.
+constexpr int kSplitWaves = 4;
 
 template <int D, int BS, int G, typename KVT, bool DENSE>
-__global__ __launch_bounds__(256) void split_kernel(SplitArgs a) {
+__global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
+  constexpr int NW = kSplitWaves, NT = 64 * NW;
   constexpr int DPL = D / 64;
   constexpr bool BF = sizeof(KVT) == 2;
   constexpr int NQ = G > 4 ? G / 4 : 1;
@@ -1084,10 +1089,10 @@ __global__ __launch_bounds__(256) void split_kernel(SplitArgs a) {
   __shared__ bf16x8 qa_s[BF ? NQ * 2 * 4 * DC : 1];      // bf16 path: q chunks (hi, lo)
   __shared__ float teff_s[G];
   __shared__ int pref_s[kMaxTiles + 1];
-  __shared__ int wsum_s[4];
-  __shared__ float mrg_ml[4][G][2];
-  __shared__ float mrg_acc[4][G][D];
-  __shared__ __attribute__((aligned(16))) float p_s[4][64 * GQ];
+  __shared__ int wsum_s[NW];
+  __shared__ float mrg_ml[NW][G][2];
+  __shared__ float mrg_acc[NW][G][D];
+  __shared__ __attribute__((aligned(16))) float p_s[NW][64 * GQ];
   __shared__ int32_t item_j[kItemChunk];
   __shared__ uint8_t item_bits[kItemChunk];
 
@@ -1102,11 +1107,11 @@ __global__ __launch_bounds__(256) void split_kernel(SplitArgs a) {
   const int tc0 = (!DENSE && tid < g.n_tiles) ? tc[tid] : 0;
   const float tau_in = (!DENSE && tid < G) ? a.tau[hq0 + tid] : 0.f;
   constexpr int QE = BF ? NQ * 4 * D : G * D;          // staged query elements
-  constexpr int QR = (QE + 255) / 256;
+  constexpr int QR = (QE + NT - 1) / NT;
   uint32_t qraw[QR];
 #pragma unroll
   for (int r = 0; r < QR; ++r) {
-    const int idx = tid + 256 * r;
+    const int idx = tid + NT * r;
     const int hh = idx / D, i = idx % D;
     const int64_t src = (hq0 + ((idx < QE && hh < G) ? hh : 0)) * D + i;
     qraw[r] = a.q_dtype == ETA_DT_F32 ? reinterpret_cast<const uint32_t*>(a.q)[src]
@@ -1116,7 +1121,7 @@ __global__ __launch_bounds__(256) void split_kernel(SplitArgs a) {
   const int ntail = (int)(T - N * BS);
 #pragma unroll
   for (int r = 0; r < QR; ++r) {
-    const int idx = tid + 256 * r;
+    const int idx = tid + NT * r;
     if (idx < QE) {
       const int hh = idx / D, i = idx % D;
       const float x = hh < G ? (a.q_dtype == ETA_DT_F32 ? __uint_as_float(qraw[r])
@@ -1136,16 +1141,21 @@ __global__ __launch_bounds__(256) void split_kernel(SplitArgs a) {
     }
   }
   if (tid < G) teff_s[tid] = DENSE ? 0.f : tau_in - a.offset_a;
-  for (int idx = tid; idx < 4 * 64 * GQ; idx += 256) (&p_s[0][0])[idx] = 0.f;
+  for (int idx = tid; idx < NW * 64 * GQ; idx += NT) (&p_s[0][0])[idx] = 0.f;
 
-  int64_t lo, hi;
+  // The split's share: on the bf16 path a contiguous range [tlo, thi) of the
+  // list's 64-token tiles (a block may be shared by two neighbouring splits, so
+  // shares differ by at most one tile); on the fp32 path a range of whole blocks.
+  // lo, hi: the list items (blocks) the share touches.
+  constexpr int SPB = BF ? BS / 64 : 1;
+  int64_t lo, hi, tlo, thi;
   if constexpr (DENSE) {
-    lo = (N * s) / S;
-    hi = (N * (s + 1)) / S;
+    tlo = (N * SPB * s) / S;
+    thi = (N * SPB * (s + 1)) / S;
   } else {
-    // exclusive prefix sum of the per-tile union counts, 256 tiles at a time
+    // exclusive prefix sum of the per-tile union counts, NT tiles at a time
     int carry = 0;
-    for (int base = 0; base < g.n_tiles; base += 256) {
+    for (int base = 0; base < g.n_tiles; base += NT) {
       const int t = base + tid;
       const int x = base == 0 ? tc0 : (t < g.n_tiles ? tc[t] : 0);
       int incl = x;
@@ -1158,7 +1168,7 @@ __global__ __launch_bounds__(256) void split_kernel(SplitArgs a) {
       __syncthreads();
       int woff = 0, tot = 0;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
+      for (int k = 0; k < NW; ++k) {
         woff += (k < w) ? wsum_s[k] : 0;
         tot += wsum_s[k];
       }
@@ -1168,9 +1178,11 @@ __global__ __launch_bounds__(256) void split_kernel(SplitArgs a) {
     }
     if (tid == 0) pref_s[g.n_tiles] = carry;
     const int64_t U = carry;
-    lo = (U * s) / S;
-    hi = (U * (s + 1)) / S;
+    tlo = (U * SPB * s) / S;
+    thi = (U * SPB * (s + 1)) / S;
   }
+  lo = tlo / SPB;
+  hi = (thi + SPB - 1) / SPB;
   __syncthreads();
 
   const KVT* kb = reinterpret_cast<const KVT*>(a.k) + (int64_t)b * g.sb + (int64_t)gh * g.sh;
@@ -1222,21 +1234,24 @@ __global__ __launch_bounds__(256) void split_kernel(SplitArgs a) {
     }
     __syncthreads();
     if constexpr (BF) {
-      // the chunk's n items are n * BS / 64 tiles of 64 tokens; wavefront w
-      // takes tiles w, w + 4, ... so the four finish within one tile
-      constexpr int SPB = BS / 64;
-      const int ntl = n * SPB;
-      const int nmine = ntl > w ? (ntl - w + 3) / 4 : 0;
+      // the share's tiles among the chunk's n items: [c0, c1) counted from the
+      // chunk's first tile; wavefront w takes tiles c0 + w, c0 + w + NW, ... so
+      // the wavefronts finish within one tile
+      const int64_t cb = base * SPB;
+      const int c0 = (int)((tlo > cb ? tlo : cb) - cb);
+      const int c1 = (int)((thi < cb + (int64_t)n * SPB ? thi : cb + (int64_t)n * SPB) - cb);
+      const int ntl = c1 - c0;
+      const int nmine = ntl > w ? (ntl - w + NW - 1) / NW : 0;
       attend_bf16_stream<D, G, DENSE>(
           kb, vb, g.st, nmine,
           [&](int u) {
-            const int x = w + 4 * u;
+            const int x = c0 + w + NW * u;
             return (int64_t)item_j[x / SPB] * BS + 64 * (x % SPB);
           },
-          [&](int u) { return (uint32_t)item_bits[(w + 4 * u) / SPB]; }, qa_s, use_lo, teff_s,
-          p_s[w], a.beta, scale, self_t, lane, m_, l_, acc);
+          [&](int u) { return (uint32_t)item_bits[(c0 + w + NW * u) / SPB]; }, qa_s, use_lo,
+          teff_s, p_s[w], a.beta, scale, self_t, lane, m_, l_, acc);
     } else {
-      for (int k = w; k < n; k += 4) attend((int64_t)item_j[k] * BS, BS, item_bits[k]);
+      for (int k = w; k < n; k += NW) attend((int64_t)item_j[k] * BS, BS, item_bits[k]);
     }
     __syncthreads();
   }
@@ -1252,15 +1267,15 @@ __global__ __launch_bounds__(256) void split_kernel(SplitArgs a) {
 #pragma unroll
     for (int e = 0; e < DPL; ++e) mrg_acc[w][h][lane * DPL + e] = acc[h][e];
   __syncthreads();
-  for (int idx = tid; idx < G * D; idx += 256) {
+  for (int idx = tid; idx < G * D; idx += NT) {
     const int h = idx / D, i = idx % D;
     float ms = kNegInf;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) ms = fmaxf(ms, mrg_ml[k][h][0]);
+    for (int k = 0; k < NW; ++k) ms = fmaxf(ms, mrg_ml[k][h][0]);
     float L = 0.f, o = 0.f;
     if (ms != kNegInf) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
+      for (int k = 0; k < NW; ++k) {
         const float mk = mrg_ml[k][h][0];
         if (mk == kNegInf) continue;
         const float wk = __expf(mk - ms);
@@ -1598,7 +1613,7 @@ void launch_split_impl(const Geom& g, int S, const SplitArgs& sp, hipStream_t st
   dim3 grid(S, g.Hkv, g.B);
 #define ETA_SPL(D_, BS_, G_, T_)                                                                \
   if (g.D == D_ && g.BS == BS_ && g.G == G_)                                                    \
-    hipLaunchKernelGGL((split_kernel<D_, BS_, G_, T_, DENSE>), grid, dim3(256), 0, stream, sp);
+    hipLaunchKernelGGL((split_kernel<D_, BS_, G_, T_, DENSE>), grid, dim3(64 * kSplitWaves), 0, stream, sp);
 #define ETA_SPL_G(D_, BS_, T_) \
   ETA_SPL(D_, BS_, 1, T_) ETA_SPL(D_, BS_, 2, T_) ETA_SPL(D_, BS_, 4, T_) ETA_SPL(D_, BS_, 8, T_)
   if (g.kv_dtype == ETA_DT_F32) {
