@@ -848,61 +848,15 @@ __device__ __forceinline__ void attend_f32(const float* __restrict__ kb, const f
 }
 
 // bf16 K/V: scores on the matrix cores.
-// bf16 p.V layout.  One 16-byte-per-lane load covers VR = 512 / D whole V
-// rows (1 KB contiguous): lane l reads row VR q + l / VL, dimensions
-// 8 (l % VL) .. + 7 (VL = D / 8 lanes per row), so a 64-token tile is VI = 64 /
-// VR loads.  The lane accumulates its 8 dimensions over the rows congruent to
-// l / VL modulo VR; the VR lane groups are added once per split (vgroup_sum).
-template <int D>
-struct VLayout {
-  static constexpr int VL = D / 8, VR = 512 / D, VI = 64 / VR;
-};
-
-// acc[h][j] += p[t][h] * V[t][8 (lane % VL) + j] for the rows of load q of a tile
-template <int D, int G>
-__device__ __forceinline__ void pv_load(const uint4& vq, int t, const float* p_s,
-                                        float (&acc)[G][8]) {
-  constexpr int NQ = G > 4 ? G / 4 : 1;
-  constexpr int GQ = 4 * NQ;
-  const uint32_t w4[4] = {vq.x, vq.y, vq.z, vq.w};
-  float vv[8];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    vv[2 * j] = bf16lo(w4[j]);
-    vv[2 * j + 1] = bf16hi(w4[j]);
-  }
-#pragma unroll
-  for (int hq = 0; hq < NQ; ++hq) {
-    const float4 p4 = *reinterpret_cast<const float4*>(p_s + t * GQ + 4 * hq);
-    const float pr[4] = {p4.x, p4.y, p4.z, p4.w};
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int h = 4 * hq + r;
-      if (h < G) {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc[h][j] = fmaf(pr[r], vv[j], acc[h][j]);
-      }
-    }
-  }
-}
-
-// sum over the lanes that hold the same dimensions (l % VL equal), fixed order
-template <int D>
-__device__ __forceinline__ float vgroup_sum(float x) {
-  constexpr int VL = VLayout<D>::VL;
-#pragma unroll
-  for (int o = VL; o < 64; o <<= 1) x += __shfl_xor(x, o, 64);
-  return x;
-}
-
 template <int D, int G, bool DENSE>
 __device__ __forceinline__ void attend_bf16(const uint16_t* __restrict__ kb,
                                             const uint16_t* __restrict__ vb, int64_t st, int64_t t0,
                                             int nvalid, uint32_t bits, const bf16x8* qa_s,
                                             bool use_lo, const float* teff_s, float* p_s,
                                             float beta, float scale, int64_t self_t, int lane,
-                                            float (&m_)[G], float (&l_)[G], float (&acc)[G][8]) {
-  using VLy = VLayout<D>;
+                                            float (&m_)[G], float (&l_)[G],
+                                            float (&acc)[G][D / 64]) {
+  constexpr int DPL = D / 64;
   constexpr int DC = D / 8;               // 16-byte chunks per row = MFMAs per head quad
   constexpr int NQ = G > 4 ? G / 4 : 1;   // head quads
   constexpr int GQ = 4 * NQ;              // padded heads (LDS row of p)
@@ -913,17 +867,21 @@ __device__ __forceinline__ void attend_bf16(const uint16_t* __restrict__ kb,
     const int nv = nvalid - sb < 64 ? nvalid - sb : 64;
     const bool valid = lane < nv;
     const int64_t tb = t0 + sb;
-    // issue every load of the 64-token step first: this lane's K row and its
-    // V loads (rows past the valid ones read token tb again and get weight 0)
+    // issue every load of the 64-token step first: this lane's K row and, for
+    // every token, this lane's head-dimension pair of V (rows past the valid
+    // ones read token tb again and get weight 0)
     uint4 kr[DC];
     const uint16_t* krow = kb + (tb + (valid ? lane : 0)) * st;
 #pragma unroll
     for (int c = 0; c < DC; ++c) kr[c] = *reinterpret_cast<const uint4*>(krow + 8 * c);
-    uint4 vq[VLy::VI];
+    uint32_t vr[64];
 #pragma unroll
-    for (int q = 0; q < VLy::VI; ++q) {
-      const int t = VLy::VR * q + lane / VLy::VL;
-      vq[q] = *reinterpret_cast<const uint4*>(vb + (tb + (t < nv ? t : 0)) * st + 8 * (lane % VLy::VL));
+    for (int t = 0; t < 64; ++t) {
+      const int64_t r = tb + (t < nv ? t : 0);
+      if constexpr (DPL == 2)
+        vr[t] = *reinterpret_cast<const uint32_t*>(vb + r * st + 2 * lane);
+      else
+        vr[t] = vb[r * st + lane];
     }
     const bool ung = (tb + lane) == self_t;
 #pragma unroll
@@ -946,14 +904,35 @@ __device__ __forceinline__ void attend_bf16(const uint16_t* __restrict__ kb,
         if (h < G) {
           const float sc =
               gated<DENSE>(c[r] * scale, valid && ((bits >> h) & 1u), ung, teff_s[h], beta);
-          p_s[lane * GQ + h] = softmax_step<8>(sc, m_[h], l_[h], acc[h]);
+          p_s[lane * GQ + h] = softmax_step<DPL>(sc, m_[h], l_[h], acc[h]);
         }
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
 #pragma unroll
-    for (int q = 0; q < VLy::VI; ++q) pv_load<D, G>(vq[q], VLy::VR * q + lane / VLy::VL, p_s, acc);
+    for (int t = 0; t < 64; ++t) {
+      float vv[DPL];
+      if constexpr (DPL == 2) {
+        vv[0] = bf16lo(vr[t]);
+        vv[1] = bf16hi(vr[t]);
+      } else {
+        vv[0] = bf16lo(vr[t]);
+      }
+#pragma unroll
+      for (int hq = 0; hq < NQ; ++hq) {
+        const float4 p4 = *reinterpret_cast<const float4*>(p_s + t * GQ + 4 * hq);
+        const float pr[4] = {p4.x, p4.y, p4.z, p4.w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int h = 4 * hq + r;
+          if (h < G) {
+#pragma unroll
+            for (int e = 0; e < DPL; ++e) acc[h][e] = fmaf(pr[r], vv[e], acc[h][e]);
+          }
+        }
+      }
+    }
     __builtin_amdgcn_wave_barrier();
   }
 }
@@ -971,8 +950,8 @@ __device__ __forceinline__ void attend_bf16_stream(const uint16_t* __restrict__ 
                                                    const float* teff_s, float* p_s, float beta,
                                                    float scale, int64_t self_t, int lane,
                                                    float (&m_)[G], float (&l_)[G],
-                                                   float (&acc)[G][8]) {
-  using VLy = VLayout<D>;
+                                                   float (&acc)[G][D / 64]) {
+  constexpr int DPL = D / 64;
   constexpr int DC = D / 8;
   constexpr int NQ = G > 4 ? G / 4 : 1;
   constexpr int GQ = 4 * NQ;
@@ -980,22 +959,24 @@ __device__ __forceinline__ void attend_bf16_stream(const uint16_t* __restrict__ 
   const bool diag = ((lane & 15) >> 2) == (lane >> 4);
   const int qrow = lane & 3;
   uint4 kr[DC];
-  uint4 vq[VLy::VI];
-  constexpr int QV = VLy::VI / 4;          // V loads per quarter tile
-  const int vrow = lane / VLy::VL, vcol = 8 * (lane % VLy::VL);
+  uint32_t vr[64];
   auto load_k = [&](int64_t tb) {
     const uint16_t* krow = kb + (tb + lane) * st;
 #pragma unroll
     for (int c = 0; c < DC; ++c) kr[c] = *reinterpret_cast<const uint4*>(krow + 8 * c);
   };
-  auto load_v_rows = [&](int64_t tb, int qt) {
+  auto load_v_rows = [&](int64_t tb, int t0) {
 #pragma unroll
-    for (int q = QV * qt; q < QV * qt + QV; ++q)
-      vq[q] = *reinterpret_cast<const uint4*>(vb + (tb + VLy::VR * q + vrow) * st + vcol);
+    for (int t = t0; t < t0 + 16; ++t) {
+      if constexpr (DPL == 2)
+        vr[t] = *reinterpret_cast<const uint32_t*>(vb + (tb + t) * st + 2 * lane);
+      else
+        vr[t] = vb[(tb + t) * st + lane];
+    }
   };
   auto load_v = [&](int64_t tb) {
 #pragma unroll
-    for (int qt = 0; qt < 4; ++qt) load_v_rows(tb, qt);
+    for (int qt = 0; qt < 4; ++qt) load_v_rows(tb, 16 * qt);
   };
   // One tile: scores on the MFMAs, then (MORE) the next tile's K loads into the
   // freed K registers, the softmax update, p.V, then (MORE) the next tile's V
@@ -1035,23 +1016,43 @@ __device__ __forceinline__ void attend_bf16_stream(const uint16_t* __restrict__ 
         const int h = 4 * hq + r;
         if (h < G) {
           const float sc = gated<DENSE>(c[hq][r] * scale, (bits >> h) & 1u, ung, teff_s[h], beta);
-          p_s[lane * GQ + h] = softmax_step<8>(sc, m_[h], l_[h], acc[h]);
+          p_s[lane * GQ + h] = softmax_step<DPL>(sc, m_[h], l_[h], acc[h]);
         }
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
-    // p.V in four quarters of the tile's V loads; as soon as a quarter's V
-    // registers are consumed, that quarter of the next tile's V is requested,
-    // so those loads overlap the rest of this tile and the next tile's scores
+    // p.V in four quarters of 16 tokens; as soon as a quarter's V registers
+    // are consumed, that quarter of the next tile's V rows is requested, so
+    // those loads overlap the rest of this tile and the next tile's scores
 #pragma unroll
     for (int qt = 0; qt < 4; ++qt) {
 #pragma unroll
-      for (int q = QV * qt; q < QV * qt + QV; ++q)
-        pv_load<D, G>(vq[q], VLy::VR * q + vrow, p_s, acc);
+      for (int t = 16 * qt; t < 16 * qt + 16; ++t) {
+        float vv[DPL];
+        if constexpr (DPL == 2) {
+          vv[0] = bf16lo(vr[t]);
+          vv[1] = bf16hi(vr[t]);
+        } else {
+          vv[0] = bf16lo(vr[t]);
+        }
+#pragma unroll
+        for (int hq = 0; hq < NQ; ++hq) {
+          const float4 p4 = *reinterpret_cast<const float4*>(p_s + t * GQ + 4 * hq);
+          const float pr[4] = {p4.x, p4.y, p4.z, p4.w};
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int h = 4 * hq + r;
+            if (h < G) {
+#pragma unroll
+              for (int e = 0; e < DPL; ++e) acc[h][e] = fmaf(pr[r], vv[e], acc[h][e]);
+            }
+          }
+        }
+      }
       if constexpr (MORE) {
         __builtin_amdgcn_sched_barrier(0);
-        load_v_rows(tbn, qt);
+        load_v_rows(tbn, 16 * qt);
         __builtin_amdgcn_sched_barrier(0);
       }
     }
@@ -1188,16 +1189,13 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
   const KVT* vb = reinterpret_cast<const KVT*>(a.v) + (int64_t)b * g.sb + (int64_t)gh * g.sh;
   const int64_t self_t = (!DENSE && a.self_ungated) ? T - 1 : -1;
   const bool use_lo = a.q_dtype == ETA_DT_F32;
-  // accumulators: bf16, 8 dimensions per lane over its V rows (summed over the
-  // lane groups at the merge); fp32, the lane's DPL dimensions
-  constexpr int AW = BF ? 8 : DPL;
-  float m_[G], l_[G], acc[G][AW];
+  float m_[G], l_[G], acc[G][DPL];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
     m_[h] = kNegInf;
     l_[h] = 0.f;
 #pragma unroll
-    for (int e = 0; e < AW; ++e) acc[h][e] = 0.f;
+    for (int e = 0; e < DPL; ++e) acc[h][e] = 0.f;
   }
   auto attend = [&](int64_t t0, int nvalid, uint32_t bits) {
     if constexpr (BF)
@@ -1259,29 +1257,15 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
   }
   if (s == S - 1 && ntail > 0 && w == 0) attend(N * BS, ntail, all_bits);
 
-  // merge the wavefront states
+  // merge the four wavefront states
   if (lane == 0) {
 #pragma unroll
     for (int h = 0; h < G; ++h) { mrg_ml[w][h][0] = m_[h]; mrg_ml[w][h][1] = l_[h]; }
   }
-  if constexpr (BF) {
-    constexpr int VL = VLayout<D>::VL;
 #pragma unroll
-    for (int h = 0; h < G; ++h)
+  for (int h = 0; h < G; ++h)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) acc[h][j] = vgroup_sum<D>(acc[h][j]);
-    if (lane < VL) {
-#pragma unroll
-      for (int h = 0; h < G; ++h)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) mrg_acc[w][h][8 * lane + j] = acc[h][j];
-    }
-  } else {
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-      for (int e = 0; e < DPL; ++e) mrg_acc[w][h][lane * DPL + e] = acc[h][e];
-  }
+    for (int e = 0; e < DPL; ++e) mrg_acc[w][h][lane * DPL + e] = acc[h][e];
   __syncthreads();
   for (int idx = tid; idx < G * D; idx += NT) {
     const int h = idx / D, i = idx % D;
