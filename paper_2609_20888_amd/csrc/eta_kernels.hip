@@ -118,6 +118,33 @@ __device__ __forceinline__ float wave_reduce(float x, Op op) {
   return op(__uint_as_float(r32[0]), __uint_as_float(r32[1]));
 }
 
+// (largest value, smallest index among its lanes) over the wavefront, in every
+// lane: the max / min-index order is a total order, so the same steps as
+// wave_reduce pair every lane with every other
+__device__ __forceinline__ void wave_argmax(float& v, int& i) {
+  auto take = [&](float ov, int oi) {
+    if (ov > v || (ov == v && oi < i)) { v = ov; i = oi; }
+  };
+  take(dpp_mov<0xB1>(v), __float_as_int(dpp_mov<0xB1>(__int_as_float(i))));
+  take(dpp_mov<0x4E>(v), __float_as_int(dpp_mov<0x4E>(__int_as_float(i))));
+  take(dpp_mov<0x141>(v), __float_as_int(dpp_mov<0x141>(__int_as_float(i))));
+  take(dpp_mov<0x140>(v), __float_as_int(dpp_mov<0x140>(__int_as_float(i))));
+  {
+    const auto rv = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    const auto ri = __builtin_amdgcn_permlane16_swap((uint32_t)i, (uint32_t)i, false, false);
+    v = __uint_as_float(rv[0]);
+    i = (int)ri[0];
+    take(__uint_as_float(rv[1]), (int)ri[1]);
+  }
+  {
+    const auto rv = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    const auto ri = __builtin_amdgcn_permlane32_swap((uint32_t)i, (uint32_t)i, false, false);
+    v = __uint_as_float(rv[0]);
+    i = (int)ri[0];
+    take(__uint_as_float(rv[1]), (int)ri[1]);
+  }
+}
+
 __device__ __forceinline__ float wave_max(float x) {
   return wave_reduce(x, [](float a, float b) { return fmaxf(a, b); });
 }
@@ -704,12 +731,7 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
           const bool ok = inw && !isnan(wb[h]);
           float bv = ok ? wb[h] : kNegInf;
           int bi = ok ? (int)jj : 0x7fffffff;
-#pragma unroll
-          for (int o = 32; o > 0; o >>= 1) {
-            const float ov = __shfl_xor(bv, o, 64);
-            const int oi = __shfl_xor(bi, o, 64);
-            if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
-          }
+          wave_argmax(bv, bi);
           if (bi != 0x7fffffff && (arg[h] < 0 || bv > best[h])) { best[h] = bv; arg[h] = bi; }
         }
       }
