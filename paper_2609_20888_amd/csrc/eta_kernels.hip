@@ -405,43 +405,64 @@ __device__ __forceinline__ float pred_x(uint32_t raw, int q_dtype) {
   return q_dtype == ETA_DT_F32 ? __uint_as_float(raw) : __uint_as_float(raw << 16);
 }
 
-// All loads unconditional (indexes clamped, the unused values zeroed in
-// pred_sum) so that the kPredRows rows are in flight together; the query is
-// kept as raw bits until pred_sum so that no conversion waits for its load.
-template <int NC>
+// Loads rows j0 + threadIdx.x + kPredThreads k (k < kPredRows), all
+// unconditional (indexes clamped, the unused values zeroed in pred_fma) so that
+// they are in flight together; the query is kept as raw bits until pred_fma so
+// that no conversion waits for its load.  VEC: the NC columns are whole,
+// 16-byte aligned groups of four (ncols == NC, h0 and Hq multiples of 4).
+template <int NC, bool VEC>
 __device__ __forceinline__ void pred_load(const void* __restrict__ q, int q_dtype, int64_t qoff,
                                           const float* __restrict__ W, int Hq, int J, int h0,
-                                          int ncols, PredRows<NC>& r) {
+                                          int ncols, int j0, PredRows<NC>& r) {
 #pragma unroll
   for (int k = 0; k < kPredRows; ++k) {
-    const int j = (int)threadIdx.x + kPredThreads * k;
+    const int j = j0 + (int)threadIdx.x + kPredThreads * k;
     const int jc = j < J ? j : 0;
     r.x[k] = q_dtype == ETA_DT_F32 ? reinterpret_cast<const uint32_t*>(q)[qoff + jc]
                                    : (uint32_t)reinterpret_cast<const uint16_t*>(q)[qoff + jc];
     const float* wr = W + (int64_t)jc * Hq + h0;
+    if constexpr (VEC) {
 #pragma unroll
-    for (int c = 0; c < NC; ++c) r.w[k][c] = wr[c < ncols ? c : 0];
+      for (int c = 0; c < NC; c += 4) {
+        const float4 w4 = *reinterpret_cast<const float4*>(wr + c);
+        r.w[k][c] = w4.x;
+        r.w[k][c + 1] = w4.y;
+        r.w[k][c + 2] = w4.z;
+        r.w[k][c + 3] = w4.w;
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < NC; ++c) r.w[k][c] = wr[c < ncols ? c : 0];
+    }
   }
 }
 
 template <int NC>
+__device__ __forceinline__ void pred_fma(int q_dtype, int J, int ncols, int j0,
+                                         const PredRows<NC>& r, float (&acc)[NC]) {
+#pragma unroll
+  for (int k = 0; k < kPredRows; ++k) {
+    const bool in = j0 + (int)threadIdx.x + kPredThreads * k < J;
+    const float x = in ? pred_x(r.x[k], q_dtype) : 0.f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) acc[c] = fmaf(x, (in && c < ncols) ? r.w[k][c] : 0.f, acc[c]);
+  }
+}
+
+// Thread t's partial sums over rows t, t + kPredThreads, ... in that order: the
+// first kPredRows from r (loaded by pred_load at j0 = 0), the rest loaded
+// kPredRows at a time.
+template <int NC, bool VEC>
 __device__ __forceinline__ void pred_sum(const void* __restrict__ q, int q_dtype, int64_t qoff,
                                          const float* __restrict__ W, int Hq, int J, int h0,
                                          int ncols, const PredRows<NC>& r, float (&acc)[NC]) {
 #pragma unroll
   for (int c = 0; c < NC; ++c) acc[c] = 0.f;
-#pragma unroll
-  for (int k = 0; k < kPredRows; ++k) {
-    const bool in = (int)threadIdx.x + kPredThreads * k < J;
-    const float x = in ? pred_x(r.x[k], q_dtype) : 0.f;
-#pragma unroll
-    for (int c = 0; c < NC; ++c) acc[c] = fmaf(x, (in && c < ncols) ? r.w[k][c] : 0.f, acc[c]);
-  }
-  for (int j = (int)threadIdx.x + kPredThreads * kPredRows; j < J; j += kPredThreads) {
-    const float x = load_q(q, q_dtype, qoff + j);
-    const float* wr = W + (int64_t)j * Hq + h0;
-#pragma unroll
-    for (int c = 0; c < NC; ++c) acc[c] = fmaf(x, (c < ncols) ? wr[c] : 0.f, acc[c]);
+  pred_fma<NC>(q_dtype, J, ncols, 0, r, acc);
+  for (int j0 = kPredThreads * kPredRows; j0 < J; j0 += kPredThreads * kPredRows) {
+    PredRows<NC> r2;
+    pred_load<NC, VEC>(q, q_dtype, qoff, W, Hq, J, h0, ncols, j0, r2);
+    pred_fma<NC>(q_dtype, J, ncols, j0, r2, acc);
   }
 }
 
@@ -477,10 +498,14 @@ __global__ __launch_bounds__(kPredThreads) void predict_kernel(const void* __res
   const int ncols = Hq - h0 < kPredCols ? Hq - h0 : kPredCols;
   const int64_t J = (int64_t)Hq * D;
   float acc[kPredCols];
-  if (W != nullptr) {
+  if (W != nullptr && ncols == kPredCols && Hq % 4 == 0) {
     PredRows<kPredCols> rows;
-    pred_load<kPredCols>(q, q_dtype, (int64_t)b * J, W, Hq, (int)J, h0, ncols, rows);
-    pred_sum<kPredCols>(q, q_dtype, (int64_t)b * J, W, Hq, (int)J, h0, ncols, rows, acc);
+    pred_load<kPredCols, true>(q, q_dtype, (int64_t)b * J, W, Hq, (int)J, h0, ncols, 0, rows);
+    pred_sum<kPredCols, true>(q, q_dtype, (int64_t)b * J, W, Hq, (int)J, h0, ncols, rows, acc);
+  } else if (W != nullptr) {
+    PredRows<kPredCols> rows;
+    pred_load<kPredCols, false>(q, q_dtype, (int64_t)b * J, W, Hq, (int)J, h0, ncols, 0, rows);
+    pred_sum<kPredCols, false>(q, q_dtype, (int64_t)b * J, W, Hq, (int)J, h0, ncols, rows, acc);
   } else {
 #pragma unroll
     for (int c = 0; c < kPredCols; ++c) acc[c] = 0.f;
@@ -594,7 +619,9 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
   const bool predict = !BOUNDS_ONLY && a.predict && a.W != nullptr;
   const int64_t Jq = (int64_t)g.Hq * D;
   PredRows<G> prow;
-  if (predict) pred_load<G>(a.q, a.q_dtype, (int64_t)b * Jq, a.W, g.Hq, (int)Jq, gh * G, G, prow);
+  // the group's G columns: whole 16-byte groups when G is a multiple of 4
+  constexpr bool PVEC = G % 4 == 0;
+  if (predict) pred_load<G, PVEC>(a.q, a.q_dtype, (int64_t)b * Jq, a.W, g.Hq, (int)Jq, gh * G, G, 0, prow);
   float m0[DQ], sd0[DQ], M0;
   issue((int64_t)tile * kScreenTile, m0, sd0, M0);
 
@@ -620,7 +647,7 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
     if (a.predict) {
       float acc[G];
       if (predict) {
-        pred_sum<G>(a.q, a.q_dtype, (int64_t)b * Jq, a.W, g.Hq, (int)Jq, gh * G, G, prow, acc);
+        pred_sum<G, PVEC>(a.q, a.q_dtype, (int64_t)b * Jq, a.W, g.Hq, (int)Jq, gh * G, G, prow, acc);
       } else {
 #pragma unroll
         for (int h = 0; h < G; ++h) acc[h] = 0.f;
