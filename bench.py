@@ -67,6 +67,8 @@ def parse():
                     help="skip the gated prefill forward measurement")
     ap.add_argument("--prefill-only", action="store_true",
                     help="measure only the gated prefill forward and print its JSON (profiling)")
+    ap.add_argument("--no-other-configs", action="store_true",
+                    help="skip the 8 x 128K and 32-sequence ragged decode timings")
     ap.add_argument("--no-calibration", action="store_true",
                     help="skip the offline threshold calibration measurement")
     ap.add_argument("--only-primary", action="store_true",
@@ -106,6 +108,45 @@ def measure_prefill(torch, eta, dev):
                "frac_of_bf16_mfma_peak": round(pflops / pms / 1e9 / 2500.0, 4)}
     log(f"[bench] gated prefill: {prefill}")
     return prefill
+
+
+def measure_config(torch, np, eta, dev, wl, steps):
+    """Decode step time of another workload (library defaults, predicted or constant
+    thresholds, predictor bias placed from the GPU's own bounds): us per step and the
+    union K / V bytes the step reads, per second."""
+    from synth import place_bias
+    sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
+    summ = eta.build_block_summaries(wl.k, sl, wl.block, num_q_heads=wl.Hq)
+    nblk = [t // wl.block for t in wl.seq_lens]
+    if wl.W is not None:
+        bounds = eta.block_bounds(wl.q, sl, summ, wl.k, block_size=wl.block, z=wl.z).cpu().numpy()
+        qW = eta.predict_threshold(wl.q, wl.W, torch.zeros(wl.Hq, device=dev)).cpu().numpy()
+        bias = torch.as_tensor(place_bias(bounds, nblk, qW.astype(np.float64), wl.target_survival,
+                                          wl.a), device=dev)
+    else:
+        bias = wl.bias.to(dev)
+    p = eta.decode_params(beta=wl.beta, z=wl.z, offset_a=wl.a, rescue_window=wl.rescue_window,
+                          lwb=wl.lwb)
+    st = eta.DecodeStep(wl.q, wl.k, wl.v, sl, summ, wl.W, bias, block_size=wl.block, params=p)
+    for _ in range(10):
+        st.run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        st.run()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / steps
+    G = wl.Hq // wl.Hkv
+    union = int(st.mask.reshape(wl.B, wl.Hkv, G, -1).any(dim=2).sum())
+    tail = sum(t % wl.block for t in wl.seq_lens) * wl.Hkv
+    kv = (union * wl.block + tail) * wl.d * 2 * 2
+    r = {"us_per_step": round(us, 2), "union_blocks": union,
+         "d_union": round(union / float(wl.Hkv * sum(nblk)), 4),
+         "union_kv_GBps": round(kv / us / 1e3, 1), "union_kv_frac_of_peak": round(kv / us / 1e3 / 8000.0, 4)}
+    log(f"[bench] {wl.name}: {r}")
+    return r
 
 
 def main():
@@ -382,6 +423,20 @@ def main():
     # ---- gated prefill / training forward
     prefill = None if args.no_prefill else measure_prefill(torch, eta, dev)
 
+    # ---- the other decode workloads at their library-default launch: 8 x 128K
+    # (16/4 heads, b = 64, clustered + random planted blocks, predictor, ~10%) and 32
+    # ragged 16K-64K sequences (32/8 heads, b = 64, calibrated constant thresholds)
+    others = None
+    if not args.no_other_configs and not args.only_primary:
+        from synth import config3, config5
+        others = {}
+        for name, mk in (("b8_128k_gqa16x4_d128_blk64_predictor", config3),
+                         ("b32_ragged_16k_64k_gqa32x8_d128_blk64_constants", config5)):
+            owl = mk(device=dev)
+            others[name] = measure_config(torch, np, eta, dev, owl, 50)
+            del owl
+            torch.cuda.empty_cache()
+
     ms, gpu_ms, kt, kv_b, step_b, ub, dh, du, steps, warm, cold_ms = primary
     split_ms, split_n = kt["split_decode"]
     split_avg_ms = split_ms / max(split_n, 1)
@@ -441,6 +496,7 @@ def main():
         "index_f16_us_per_step": index_f16,
         "calibration": calib,
         "gated_prefill": prefill,
+        "other_configs": others,
         "roofline": {"bound": "hbm", "kernel": "split_decode", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "algorithmic_bytes_per_launch": kv_b,
