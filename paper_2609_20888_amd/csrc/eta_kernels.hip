@@ -787,11 +787,11 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
 
 // ---------------------------------------------------------------- split decode
 //
-// One workgroup (kSplitWaves wavefronts) per (split, kv head, sequence).  The
-// split owns a contiguous range of the (sequence, kv head)'s union list in
-// 64-token tiles (bf16; whole blocks for fp32), so split shares differ by at
-// most one tile; wavefront w takes the range's tiles w, w + kSplitWaves, ...
-// A block is processed 64 tokens at a time,
+// One workgroup (kSplitWaves wavefronts) per (split, kv head, sequence).  Split
+// s of S owns the (sequence, kv head)'s union-list tiles of 64 tokens s, s + S,
+// s + 2 S, ... (bf16; a contiguous range of whole blocks for fp32), so shares
+// differ by at most one tile; wavefront w takes its share's tiles w,
+// w + kSplitWaves, ...  A block is processed 64 tokens at a time,
 // lane = token for the scores (each lane reads its own K row with 16-byte
 // loads) and lane = head-dimension pair for p.V (coalesced rows of V), with
 // the weights p passed through the wavefront's LDS slice.  A head skips blocks
@@ -1144,6 +1144,7 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
   __shared__ __attribute__((aligned(16))) float p_s[NW][64 * GQ];
   __shared__ int32_t item_j[kItemChunk];
   __shared__ uint8_t item_bits[kItemChunk];
+  __shared__ uint8_t item_sub[kItemChunk];
 
   const int64_t hq0 = (int64_t)b * g.Hq + (int64_t)gh * G;
   const int64_t bg = (int64_t)b * g.Hkv + gh;
@@ -1192,15 +1193,15 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
   if (tid < G) teff_s[tid] = DENSE ? 0.f : tau_in - a.offset_a;
   for (int idx = tid; idx < NW * 64 * GQ; idx += NT) (&p_s[0][0])[idx] = 0.f;
 
-  // The split's share: on the bf16 path a contiguous range [tlo, thi) of the
-  // list's 64-token tiles (a block may be shared by two neighbouring splits, so
-  // shares differ by at most one tile); on the fp32 path a range of whole blocks.
-  // lo, hi: the list items (blocks) the share touches.
+  // The split's share of the list (the union's blocks, or every block when
+  // dense): on the bf16 path the list's 64-token tiles s, s + S, s + 2 S, ...
+  // (shares differ by at most one tile and each spreads over the whole list,
+  // which measured faster than contiguous ranges); on the fp32 path the
+  // contiguous range of whole blocks [lo, hi).
   constexpr int SPB = BF ? BS / 64 : 1;
-  int64_t lo, hi, tlo, thi;
+  int64_t UI;                // items (blocks) in the list
   if constexpr (DENSE) {
-    tlo = (N * SPB * s) / S;
-    thi = (N * SPB * (s + 1)) / S;
+    UI = N;
   } else {
     // exclusive prefix sum of the per-tile union counts, NT tiles at a time
     int carry = 0;
@@ -1226,12 +1227,9 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
       __syncthreads();
     }
     if (tid == 0) pref_s[g.n_tiles] = carry;
-    const int64_t U = carry;
-    tlo = (U * SPB * s) / S;
-    thi = (U * SPB * (s + 1)) / S;
+    UI = carry;
   }
-  lo = tlo / SPB;
-  hi = (thi + SPB - 1) / SPB;
+  const int64_t lo = (UI * s) / S, hi = (UI * (s + 1)) / S;
   __syncthreads();
 
   const KVT* kb = reinterpret_cast<const KVT*>(a.k) + (int64_t)b * g.sb + (int64_t)gh * g.sh;
@@ -1256,53 +1254,58 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
                               m_, l_, acc);
   };
   constexpr uint32_t all_bits = (1u << G) - 1u;
-  // The split's items are resolved (union slot -> block id -> head bits) 256 at
-  // a time by all threads at once and kept in LDS, so a wavefront's K/V loads
+  // The split's items are resolved (union slot -> block id -> head bits) in
+  // chunks by all threads at once and kept in LDS, so a wavefront's K/V loads
   // never wait on those lookups.
-  for (int64_t base = lo; base < hi; base += kItemChunk) {
-    const int n = (int)(hi - base < kItemChunk ? hi - base : kItemChunk);
-    if (tid < n) {
-      const int64_t it = base + tid;
-      int64_t j;
-      uint32_t bits;
-      if constexpr (DENSE) {
-        j = it;
-        bits = all_bits;
-      } else {
-        int tl = 0, th = g.n_tiles;       // pref_s[tl] <= it < pref_s[th]
-        while (th - tl > 1) {
-          const int mid = (tl + th) >> 1;
-          if (pref_s[mid] <= it) tl = mid; else th = mid;
-        }
-        const uint32_t id = (uint32_t)a.ids[bg * g.ncap + (int64_t)tl * kScreenTile + (it - pref_s[tl])];
-        j = id & kIdMask;
-        bits = id >> 24;
+  // list item -> (block id, head bits)
+  auto resolve = [&](int64_t it, int32_t& jo, uint8_t& bo) {
+    if constexpr (DENSE) {
+      jo = (int32_t)it;
+      bo = (uint8_t)all_bits;
+    } else {
+      int tl = 0, th = g.n_tiles;       // pref_s[tl] <= it < pref_s[th]
+      while (th - tl > 1) {
+        const int mid = (tl + th) >> 1;
+        if (pref_s[mid] <= it) tl = mid; else th = mid;
       }
-      item_j[tid] = (int32_t)j;
-      item_bits[tid] = (uint8_t)bits;
+      const uint32_t id = (uint32_t)a.ids[bg * g.ncap + (int64_t)tl * kScreenTile + (it - pref_s[tl])];
+      jo = (int32_t)(id & kIdMask);
+      bo = (uint8_t)(id >> 24);
     }
-    __syncthreads();
-    if constexpr (BF) {
-      // the share's tiles among the chunk's n items: [c0, c1) counted from the
-      // chunk's first tile; wavefront w takes tiles c0 + w, c0 + w + NW, ... so
-      // the wavefronts finish within one tile
-      const int64_t cb = base * SPB;
-      const int c0 = (int)((tlo > cb ? tlo : cb) - cb);
-      const int c1 = (int)((thi < cb + (int64_t)n * SPB ? thi : cb + (int64_t)n * SPB) - cb);
-      const int ntl = c1 - c0;
-      const int nmine = ntl > w ? (ntl - w + NW - 1) / NW : 0;
+  };
+  if constexpr (BF) {
+    // kItemChunk of the share's tiles at a time, resolved by all threads at once;
+    // wavefront w takes the chunk's tiles w, w + NW, ... so the wavefronts finish
+    // within one tile
+    const int64_t UT = UI * SPB;
+    const int nt = UT > s ? (int)((UT - s + S - 1) / S) : 0;
+    for (int k0 = 0; k0 < nt; k0 += kItemChunk) {
+      const int n = nt - k0 < kItemChunk ? nt - k0 : kItemChunk;
+      if (tid < n) {
+        const int64_t t = s + (int64_t)S * (k0 + tid);
+        resolve(t / SPB, item_j[tid], item_bits[tid]);
+        item_sub[tid] = (uint8_t)(t % SPB);
+      }
+      __syncthreads();
+      const int nmine = n > w ? (n - w + NW - 1) / NW : 0;
       attend_bf16_stream<D, G, DENSE>(
           kb, vb, g.st, nmine,
           [&](int u) {
-            const int x = c0 + w + NW * u;
-            return (int64_t)item_j[x / SPB] * BS + 64 * (x % SPB);
+            const int x = w + NW * u;
+            return (int64_t)item_j[x] * BS + 64 * item_sub[x];
           },
-          [&](int u) { return (uint32_t)item_bits[(c0 + w + NW * u) / SPB]; }, qa_s, use_lo,
-          teff_s, p_s[w], a.beta, scale, self_t, lane, m_, l_, acc);
-    } else {
-      for (int k = w; k < n; k += NW) attend((int64_t)item_j[k] * BS, BS, item_bits[k]);
+          [&](int u) { return (uint32_t)item_bits[w + NW * u]; }, qa_s, use_lo, teff_s, p_s[w],
+          a.beta, scale, self_t, lane, m_, l_, acc);
+      __syncthreads();
     }
-    __syncthreads();
+  } else {
+    for (int64_t base = lo; base < hi; base += kItemChunk) {
+      const int n = (int)(hi - base < kItemChunk ? hi - base : kItemChunk);
+      if (tid < n) resolve(base + tid, item_j[tid], item_bits[tid]);
+      __syncthreads();
+      for (int k = w; k < n; k += NW) attend((int64_t)item_j[k] * BS, BS, item_bits[k]);
+      __syncthreads();
+    }
   }
   if (s == S - 1 && ntail > 0 && w == 0) attend(N * BS, ntail, all_bits);
 
