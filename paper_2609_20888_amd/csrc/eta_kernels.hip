@@ -643,30 +643,40 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
       if (lane == 0) qn_s[h] = sqrtf(ss);
     }
   }
+  // predictor: this wavefront's partial sums of the group's G columns (the
+  // wavefronts' partials are added after the barrier below, in the stand-alone
+  // predictor's order, so the thresholds are bit-identical to it)
   if constexpr (!BOUNDS_ONLY) {
-    if (a.predict) {
+    if (predict) {
       float acc[G];
-      if (predict) {
-        pred_sum<G, PVEC>(a.q, a.q_dtype, (int64_t)b * Jq, a.W, g.Hq, (int)Jq, gh * G, G, prow, acc);
-      } else {
+      pred_sum<G, PVEC>(a.q, a.q_dtype, (int64_t)b * Jq, a.W, g.Hq, (int)Jq, gh * G, G, prow, acc);
 #pragma unroll
-        for (int h = 0; h < G; ++h) acc[h] = 0.f;
+      for (int h = 0; h < G; ++h) {
+        const float x = wave_sum(acc[h]);
+        if (lane == 0) pred_red[w * G + h] = x;
       }
-      float t = 0.f;
-      pred_reduce<G>(acc, G, pred_red, &t);
-      if (tid < G) {
-        const float tau = t + tau_in;
-        teff_s[tid] = tau - a.offset_a;
+    }
+  }
+  __syncthreads();
+  // thresholds: read by the selection only, after the barriers in `finish`
+  if constexpr (!BOUNDS_ONLY) {
+    if (tid < G) {
+      float tau = tau_in;
+      if (a.predict) {
+        float t = 0.f;
+        if (predict) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) t += pred_red[k * G + tid];
+        }
+        tau = t + tau_in;
         if (tile == 0) {
           a.tau_store[hq0 + tid] = tau;
           if (a.tau_out != nullptr) a.tau_out[hq0 + tid] = tau;
         }
       }
-    } else if (tid < G) {
-      teff_s[tid] = tau_in - a.offset_a;
+      teff_s[tid] = tau - a.offset_a;
     }
   }
-  __syncthreads();
 
   const int64_t N = T / g.BS;
 
