@@ -89,6 +89,8 @@ def _load():
     lib.eta_oracle_round_f16.argtypes = [ctypes.c_double]
     lib.eta_oracle_round_f16_array.restype = None
     lib.eta_oracle_round_f16_array.argtypes = [_vp, _vp, ctypes.c_int64]
+    lib.eta_oracle_round_e4m3_array.restype = None
+    lib.eta_oracle_round_e4m3_array.argtypes = [_vp, _vp, ctypes.c_int64]
     lib.eta_oracle_bound.restype = ctypes.c_double
     lib.eta_oracle_bound.argtypes = [_vp, _vp, _vp, ctypes.c_double, ctypes.c_int, ctypes.c_double]
     lib.eta_oracle_predict.restype = None
@@ -154,6 +156,15 @@ def round_f16(x) -> np.ndarray:
     a = np.ascontiguousarray(np.asarray(x, np.float64))
     out = np.empty_like(a)
     _load().eta_oracle_round_f16_array(_ptr(a), _ptr(out), a.size)
+    return out
+
+
+def round_e4m3(x) -> np.ndarray:
+    """Nearest 8-bit E4M3 values (ties to even, saturating at +-448) as float64: the
+    FP8 index records (Sec. "Limitations and Conclusion": FP8 metadata quantisation)."""
+    a = np.ascontiguousarray(np.asarray(x, np.float64))
+    out = np.empty_like(a)
+    _load().eta_oracle_round_e4m3_array(_ptr(a), _ptr(out), a.size)
     return out
 
 

@@ -153,6 +153,37 @@ void eta_oracle_round_f16_array(const double* in, double* out, int64_t n) {
   for (int64_t i = 0; i < n; ++i) out[i] = eta_oracle_round_f16(in[i]);
 }
 
+/*
+ * Nearest 8-bit E4M3 value to x (1 sign, 4 exponent bits with bias 7, 3
+ * fraction bits; the OCP "e4m3fn" format), ties to even, returned as a double:
+ * 4 significant bits, binades 2^-6 .. 2^8, fixed spacing 2^-9 below 2^-6
+ * (subnormals), largest finite 448.  The format has no infinity; magnitudes
+ * of 464 (the tie between 448 and the next step) and above saturate to 448.
+ * NaN and zeros pass through.  The FP8 index records (Sec. "Limitations and
+ * Conclusion" names FP8 metadata quantisation as a way to cut screening
+ * traffic).
+ */
+double eta_oracle_round_e4m3(double x) {
+  if (isnan(x) || x == 0.0) return x;
+  const double a = fabs(x);
+  double r;
+  if (a >= 464.0) {
+    r = 448.0;
+  } else {
+    int e;
+    frexp(a, &e);              /* a in [2^(e-1), 2^e) */
+    int ex = e - 1;
+    if (ex < -6) ex = -6;      /* subnormal range: the spacing of the lowest binade */
+    const double ulp = ldexp(1.0, ex - 3);
+    r = nearbyint(a / ulp) * ulp;   /* a / ulp is exact; default mode rounds half to even */
+  }
+  return copysign(r, x);
+}
+
+void eta_oracle_round_e4m3_array(const double* in, double* out, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) out[i] = eta_oracle_round_e4m3(in[i]);
+}
+
 void eta_oracle_envelope(const void* k, int dt, int64_t row_stride, int64_t T, int d, int b,
                          int b_sub, const double* mu, double* env) {
   int64_t N = T / b;

@@ -41,6 +41,9 @@ MUTANTS = {
     "f16_ties_away": ("r = nearbyint(a / ulp) * ulp;", "r = round(a / ulp) * ulp;"),
     "f16_no_subnormal_floor": ("if (ex < -14) ex = -14;", ";"),
     "f16_short_significand": ("const double ulp = ldexp(1.0, ex - 10);", "const double ulp = ldexp(1.0, ex - 9);"),
+    "e4m3_ties_away": ("    r = nearbyint(a / ulp) * ulp;   /* a / ulp is exact; default mode rounds half to even */\n  }\n  return copysign(r, x);\n}\n\nvoid eta_oracle_round_e4m3_array", "    r = round(a / ulp) * ulp;\n  }\n  return copysign(r, x);\n}\n\nvoid eta_oracle_round_e4m3_array"),
+    "e4m3_no_subnormal_floor": ("if (ex < -6) ex = -6;", ";"),
+    "e4m3_long_significand": ("const double ulp = ldexp(1.0, ex - 3);", "const double ulp = ldexp(1.0, ex - 4);"),
     "envelope_block_divisor": ("double sd = sqrt(acc / (double)b_sub);", "double sd = sqrt(acc / (double)b);"),
     "calib_unweighted": ("const double wt = 1.0 / (double)(t + 1);", "const double wt = 1.0;"),
     "calib_weight_off_by_one": ("const double wt = 1.0 / (double)(t + 1);", "const double wt = 1.0 / (double)(t + 2);"),

@@ -424,6 +424,33 @@ def test_round_f16_is_ieee_binary16_nearest_even():
         == [1.0, 1 + 2.0 ** -9, 0.0, 2.0 ** -23]
 
 
+def test_round_e4m3_is_fp8_nearest_even():
+    """FP8 index records (Sec. "Limitations and Conclusion": FP8 metadata): on the
+    finite range the oracle's rounding equals torch's float32 -> float8_e4m3fn
+    conversion, an independent round-to-nearest-even implementation of the format;
+    from 464 (the tie between 448 and the first step past it) it saturates to 448,
+    where the format has no finite value and torch gives NaN."""
+    rng = np.random.default_rng(6)
+    mag = 2.0 ** rng.uniform(-13, np.log2(463.9), 20000)
+    x = np.concatenate([mag * rng.choice([-1.0, 1.0], mag.size),
+                        rng.standard_normal(5000) * 3.0,
+                        np.array([0.0, -0.0, 448.0, 447.9, 463.9, -463.9, 2.0 ** -9, 2.0 ** -10,
+                                  3 * 2.0 ** -10, 2.0 ** -6, 2.0 ** -6 - 2.0 ** -10, 1 + 2.0 ** -4,
+                                  1 + 3 * 2.0 ** -4, 240.0 + 8.0, 256.0 + 16.0])])
+    x = x.astype(np.float32)                          # exactly representable inputs
+    ref = torch.from_numpy(x).to(torch.float8_e4m3fn).to(torch.float64).numpy()
+    got = oracle.round_e4m3(x.astype(np.float64))
+    assert np.array_equal(got, ref)
+    assert np.array_equal(np.signbit(got), np.signbit(ref))
+    assert np.isnan(oracle.round_e4m3([np.nan]))[0]
+    assert oracle.round_e4m3([464.0, 480.0, 1e6, -500.0, np.inf]).tolist() == [448.0, 448.0, 448.0,
+                                                                                -448.0, 448.0]
+    # ties go to the even significand: 1 + 2^-4 -> 1, 1 + 3 * 2^-4 -> 1.25, half the
+    # smallest subnormal -> 0, 1.5 of it -> 2^-8
+    assert oracle.round_e4m3([1 + 2.0 ** -4, 1 + 3 * 2.0 ** -4, 2.0 ** -10, 3 * 2.0 ** -10]).tolist() \
+        == [1.0, 1.25, 0.0, 2.0 ** -8]
+
+
 # ------------------------------------------------------------- offline calibration
 # App. "Offline Threshold Calibration via 1/t-Weighted Histograms",
 # Alg. "Density-Matched Offline Threshold Calibration".
