@@ -364,31 +364,36 @@ def main():
         if is_primary:
             primary = (ms, gpu_ms, kt, kv_b, step_b, ub, dh, du, steps, warm, cold_ms)
 
-    # ---- the same steps screening on half-precision records (fp16 mu / sigma, as the
-    # paper's compact record); the headline keeps the fp32 index
-    summ16 = eta.build_block_summaries(k, sl, bs, num_q_heads=Hq, stat_dtype=torch.float16)
-    prep16 = eta.DecodeStep(q, k, v, sl, summ16, W, bias_buf, block_size=bs, params=params)
-    index_f16 = {}
-    for s in (SWEEP if not args.only_primary else (PRIMARY_SURVIVAL,)):
-        set_point(biases[s])
-        for _ in range(5):
-            prep16.run()
+    # ---- the same steps screening on compact records (fp16 mu / sigma, the paper's
+    # compact record; FP8 E4M3 mu / sigma, its FP8 metadata), at the fp32 index's
+    # thresholds; the headline keeps the fp32 index
+    def compact_index(stat_dtype, label):
+        summ_c = eta.build_block_summaries(k, sl, bs, num_q_heads=Hq, stat_dtype=stat_dtype)
+        prep_c = eta.DecodeStep(q, k, v, sl, summ_c, W, bias_buf, block_size=bs, params=params)
+        res = {}
+        for s in (SWEEP if not args.only_primary else (PRIMARY_SURVIVAL,)):
+            set_point(biases[s])
+            for _ in range(5):
+                prep_c.run()
+            torch.cuda.synchronize()
+            n_c = max(20, args.steps // 4)
+            t0 = time.perf_counter()
+            for _ in range(n_c):
+                prep_c.run()
+            torch.cuda.synchronize()
+            res[f"{int(round(s * 100))}%"] = round((time.perf_counter() - t0) * 1e6 / n_c, 2)
+        set_point(biases[PRIMARY_SURVIVAL])
+        eta.profile_begin()
+        for _ in range(50):
+            prep_c.run()
         torch.cuda.synchronize()
-        n16 = max(20, args.steps // 4)
-        t0 = time.perf_counter()
-        for _ in range(n16):
-            prep16.run()
-        torch.cuda.synchronize()
-        index_f16[f"{int(round(s * 100))}%"] = round((time.perf_counter() - t0) * 1e6 / n16, 2)
-    set_point(biases[PRIMARY_SURVIVAL])
-    eta.profile_begin()
-    for _ in range(50):
-        prep16.run()
-    torch.cuda.synchronize()
-    kt16 = eta.profile_end()
-    index_f16["screen_avg_us_20%"] = round(kt16["screen"][0] / max(kt16["screen"][1], 1) * 1e3, 2)
-    log(f"[bench] fp16 index: {index_f16}")
-    del prep16, summ16
+        kt_c = eta.profile_end()
+        res["screen_avg_us_20%"] = round(kt_c["screen"][0] / max(kt_c["screen"][1], 1) * 1e3, 2)
+        log(f"[bench] {label} index: {res}")
+        return res
+
+    index_f16 = compact_index(torch.float16, "fp16")
+    index_fp8 = compact_index(torch.float8_e4m3fn, "fp8")
 
     # ---- offline threshold calibration: 16 calibration sequences of 4096 steps at the
     # ragged workload's head shape (32 query / 8 kv heads, d = 128), 1024 bins
@@ -494,6 +499,7 @@ def main():
         "summary_envelope_sub_block": env_sub,
         "summary_update_us_per_step": round(upd_ms * 1e3, 2),
         "index_f16_us_per_step": index_f16,
+        "index_fp8_us_per_step": index_fp8,
         "calibration": calib,
         "gated_prefill": prefill,
         "other_configs": others,

@@ -59,8 +59,9 @@ typedef enum {
 } eta_status_t;
 
 /* Element types.  q, K and V are ETA_DT_F32 or ETA_DT_BF16; block-index
- * records (mu, sigma) are ETA_DT_F32 or ETA_DT_F16. */
-typedef enum { ETA_DT_F32 = 0, ETA_DT_BF16 = 1, ETA_DT_F16 = 2 } eta_dtype_t;
+ * records (mu, sigma) are ETA_DT_F32, ETA_DT_F16 or ETA_DT_FP8 (8-bit E4M3:
+ * bias 7, 3 fraction bits, largest finite 448). */
+typedef enum { ETA_DT_F32 = 0, ETA_DT_BF16 = 1, ETA_DT_F16 = 2, ETA_DT_FP8 = 3 } eta_dtype_t;
 
 /*
  * KV cache geometry.  K and V share it.  Element (b, h, t, i) of K lives at
@@ -96,6 +97,9 @@ typedef struct {
  * computed in fp32 and rounded to nearest-even when stored as fp16; the bound
  * is evaluated in fp32 either way.  The standard deviation (not the variance)
  * is stored, as the paper does, so small spreads do not underflow in fp16.
+ * ETA_DT_FP8 stores mu and sigma as 8-bit E4M3 codes (the FP8 metadata of Sec.
+ * "Limitations and Conclusion"): nearest-even rounding of the fp32 statistic,
+ * magnitudes from 464 saturated to 448; a quarter of the fp32 record bytes.
  * n_blk_cap >= capacity_tokens / block_size, n_blk_cap < 2^24 and
  * n_blk_cap <= 131072 (2048 screening tiles of 64 blocks).
  */
@@ -104,7 +108,7 @@ typedef struct {
   void* sigma;
   float* max_norm;
   int64_t n_blk_cap;
-  int32_t stat_dtype;          /* ETA_DT_F32 (0) or ETA_DT_F16 */
+  int32_t stat_dtype;          /* ETA_DT_F32 (0), ETA_DT_F16 or ETA_DT_FP8 */
   int32_t reserved;            /* 0 */
 } eta_summary_t;
 

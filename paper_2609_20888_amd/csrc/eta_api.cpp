@@ -100,8 +100,9 @@ eta_status_t check_summary(const eta_summary_t* s, Geom* g) {
     return fail(ETA_ERR_INVALID_ARG, "summary buffers must be non-NULL");
   if (!aligned16(s->mu) || !aligned16(s->sigma) || !aligned16(s->max_norm))
     return fail(ETA_ERR_INVALID_ARG, "summary buffers must be 16-byte aligned");
-  if (s->stat_dtype != ETA_DT_F32 && s->stat_dtype != ETA_DT_F16)
-    return fail(ETA_ERR_INVALID_ARG, "stat_dtype %d: summaries are ETA_DT_F32 or ETA_DT_F16", s->stat_dtype);
+  if (s->stat_dtype != ETA_DT_F32 && s->stat_dtype != ETA_DT_F16 && s->stat_dtype != ETA_DT_FP8)
+    return fail(ETA_ERR_INVALID_ARG,
+                "stat_dtype %d: summaries are ETA_DT_F32, ETA_DT_F16 or ETA_DT_FP8", s->stat_dtype);
   g->stat_dtype = s->stat_dtype;
   if (s->n_blk_cap < g->cap / g->BS)
     return fail(ETA_ERR_INVALID_ARG, "n_blk_cap (%lld) < capacity_tokens / block_size (%lld)",

@@ -27,7 +27,7 @@ struct Geom {
   int64_t sb, sh, st;        // K/V strides in elements
   int64_t ncap;              // summary n_blk_cap
   int n_tiles;               // ceil(ncap / kScreenTile)
-  int stat_dtype;            // summary mu / sigma element type (ETA_DT_F32 or ETA_DT_F16)
+  int stat_dtype;            // summary mu / sigma element type (ETA_DT_F32, ETA_DT_F16 or ETA_DT_FP8)
 };
 
 // Workspace carve-up of eta_decode.

@@ -40,6 +40,35 @@ __device__ __forceinline__ uint16_t to_bf16(float f) {
   return __builtin_bit_cast(uint16_t, (__bf16)f);
 }
 
+// fp32 -> 8-bit E4M3 code (bias 7, 3 fraction bits), round to nearest even;
+// magnitudes from 464 (the tie past 448, the largest finite value) saturate
+// to 448, NaN gives the NaN code.
+__device__ __forceinline__ uint8_t to_e4m3(float f) {
+  const uint32_t sgn = (__float_as_uint(f) >> 24) & 0x80u;
+  const float a = fabsf(f);
+  if (!(a == a)) return (uint8_t)(sgn | 0x7fu);
+  if (a >= 464.0f) return (uint8_t)(sgn | 0x7eu);
+  if (a < 0.015625f)                              // below 2^-6: multiples of 2^-9
+    return (uint8_t)(sgn | (uint32_t)rintf(a * 512.0f));   // 0 .. 8 (8: the code of 2^-6)
+  const uint32_t au = __float_as_uint(a);
+  int e = (int)(au >> 23) - 127;                  // -6 .. 8
+  uint32_t keep = (au >> 20) & 7u;
+  const uint32_t rest = au & 0xfffffu;
+  if (rest > 0x80000u || (rest == 0x80000u && (keep & 1u))) ++keep;
+  if (keep == 8u) {
+    keep = 0u;
+    ++e;
+  }
+  return (uint8_t)(sgn | ((uint32_t)(e + 7) << 3) | keep);
+}
+
+// record element -> fp32 (E4M3 codes decoded exactly by the hardware conversion)
+__device__ __forceinline__ float stat_f32(float x) { return x; }
+__device__ __forceinline__ float stat_f32(_Float16 x) { return (float)x; }
+__device__ __forceinline__ float stat_f32(uint8_t x) {
+  return __builtin_amdgcn_cvt_f32_fp8((int)x, 0);
+}
+
 // Element access for the two storage types: float and bf16 (raw uint16 bits).
 template <typename T>
 struct Elem;
@@ -360,7 +389,7 @@ __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ 
   // whole rows of the dimension-major output (blocks j0 .. j0 + nv - 1)
   const int nv = N - j0 < kSumBlocks ? (int)(N - j0) : kSumBlocks;
   const int64_t ob = bg * D * g.ncap + j0;
-  const bool f16 = g.stat_dtype == ETA_DT_F16;
+  const bool f16 = g.stat_dtype == ETA_DT_F16, fp8 = g.stat_dtype == ETA_DT_FP8;
   for (int idx = tid; idx < D * kSumBlocks; idx += 256) {
     const int i = idx / kSumBlocks, jj = idx % kSumBlocks;
     if (jj < nv) {
@@ -368,6 +397,9 @@ __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ 
       if (f16) {   // round to nearest even
         reinterpret_cast<_Float16*>(mu)[o] = (_Float16)mu_s[i][jj];
         reinterpret_cast<_Float16*>(sigma)[o] = (_Float16)sg_s[i][jj];
+      } else if (fp8) {
+        reinterpret_cast<uint8_t*>(mu)[o] = to_e4m3(mu_s[i][jj]);
+        reinterpret_cast<uint8_t*>(sigma)[o] = to_e4m3(sg_s[i][jj]);
       } else {
         reinterpret_cast<float*>(mu)[o] = mu_s[i][jj];
         reinterpret_cast<float*>(sigma)[o] = sg_s[i][jj];
@@ -592,8 +624,8 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
     const ST* sgp = reinterpret_cast<const ST*>(a.sigma) + (bg * D + w * DQ) * g.ncap + jc;
 #pragma unroll
     for (int i = 0; i < DQ; ++i) {
-      m[i] = (float)mup[(int64_t)i * g.ncap];
-      sd[i] = (float)sgp[(int64_t)i * g.ncap];
+      m[i] = stat_f32(mup[(int64_t)i * g.ncap]);
+      sd[i] = stat_f32(sgp[(int64_t)i * g.ncap]);
     }
     M = a.mx[bg * g.ncap + jc];
   };
@@ -1660,6 +1692,9 @@ void launch_screen_impl(const Geom& g, const ScreenArgs& sa, hipStream_t stream)
   if (g.D == D_ && g.G == G_) {                                                                 \
     if (g.stat_dtype == ETA_DT_F16)                                                             \
       hipLaunchKernelGGL((screen_kernel<D_, G_, BOUNDS_ONLY, _Float16>), grid,                  \
+                         dim3(kScreenThreads), 0, stream, sa);                                  \
+    else if (g.stat_dtype == ETA_DT_FP8)                                                        \
+      hipLaunchKernelGGL((screen_kernel<D_, G_, BOUNDS_ONLY, uint8_t>), grid,                   \
                          dim3(kScreenThreads), 0, stream, sa);                                  \
     else                                                                                        \
       hipLaunchKernelGGL((screen_kernel<D_, G_, BOUNDS_ONLY, float>), grid,                     \

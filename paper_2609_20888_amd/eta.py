@@ -18,7 +18,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libeta.so")
 
 ETA_OK, ETA_ERR_INVALID_ARG, ETA_ERR_UNSUPPORTED, ETA_ERR_WORKSPACE, ETA_ERR_HIP = range(5)
-ETA_DT_F32, ETA_DT_BF16, ETA_DT_F16 = 0, 1, 2
+ETA_DT_F32, ETA_DT_BF16, ETA_DT_F16, ETA_DT_FP8 = 0, 1, 2, 3
 KERNEL_KINDS = ("summaries", "predict", "screen", "split_decode", "combine", "dense_split",
                 "dense_combine", "bounds", "calib_accumulate", "calib_solve", "prefill")
 
@@ -175,17 +175,25 @@ class Summaries:
         return self.mu.shape[-1]
 
     def desc(self) -> SummaryDesc:
-        st = {torch.float32: ETA_DT_F32, torch.float16: ETA_DT_F16}[self.mu.dtype]
+        st = {torch.float32: ETA_DT_F32, torch.float16: ETA_DT_F16,
+              torch.float8_e4m3fn: ETA_DT_FP8}[self.mu.dtype]
         return SummaryDesc(mu=_ptr(self.mu), sigma=_ptr(self.sigma), max_norm=_ptr(self.max_norm),
                            n_blk_cap=self.n_blk_cap, stat_dtype=st)
 
     @staticmethod
     def empty(B: int, Hkv: int, d: int, n_blk_cap: int, device,
               stat_dtype: torch.dtype = torch.float32) -> "Summaries":
-        """stat_dtype: torch.float32 or torch.float16 (mu and sigma records)."""
+        """stat_dtype: torch.float32, torch.float16 or torch.float8_e4m3fn (mu and sigma
+        records; FP8 as 8-bit E4M3 codes, nearest even, saturating at +-448)."""
         n = max(int(n_blk_cap), 1)
-        return Summaries(mu=torch.zeros(B, Hkv, d, n, device=device, dtype=stat_dtype),
-                         sigma=torch.zeros(B, Hkv, d, n, device=device, dtype=stat_dtype),
+        if stat_dtype not in (torch.float32, torch.float16, torch.float8_e4m3fn):
+            raise TypeError(f"unsupported record dtype {stat_dtype}")
+
+        def rec():   # zero bits (zero in all three formats), filled as plain words
+            if stat_dtype == torch.float8_e4m3fn:
+                return torch.zeros(B, Hkv, d, n, device=device, dtype=torch.uint8).view(stat_dtype)
+            return torch.zeros(B, Hkv, d, n, device=device, dtype=stat_dtype)
+        return Summaries(mu=rec(), sigma=rec(),
                          max_norm=torch.zeros(B, Hkv, n, device=device, dtype=torch.float32))
 
 
@@ -204,7 +212,8 @@ def build_block_summaries(k: torch.Tensor, seq_lens: torch.Tensor, block_size: i
                           stream=None) -> Summaries:
     """eta_build_block_summaries: mu, sigma, M of every full block of K
     (sub_block > 0: eta_build_block_summaries_envelope, sigma = sub-block envelope;
-    stat_dtype torch.float16: half-precision mu / sigma records)."""
+    stat_dtype torch.float16 / torch.float8_e4m3fn: half-precision / FP8 E4M3 mu / sigma
+    records)."""
     B, Hkv, T_cap, d = k.shape
     desc = kv_desc(k, num_q_heads or Hkv, block_size)
     if out is None:

@@ -136,8 +136,10 @@ U32 = 2.0 ** -24   # fp32 unit roundoff
 
 
 def f16_record_ranges(wl: Workload, k: np.ndarray, mu: np.ndarray, sg: np.ndarray,
-                      sub_block: int = 0):
-    """For each fp16 record value, the interval [lo, hi] of values the GPU may store.
+                      sub_block: int = 0, rnd=None):
+    """For each fp16 record value, the interval [lo, hi] of values the GPU may store
+    (rnd: the record format's rounding, oracle.round_f16 by default; any monotone
+    rounding, e.g. oracle.round_e4m3, works the same way).
 
     The GPU rounds (nearest even) fp32 statistics that lie within the classical
     summation error bound of the exact ones:
@@ -163,8 +165,8 @@ def f16_record_ranges(wl: Workload, k: np.ndarray, mu: np.ndarray, sg: np.ndarra
         dsg = (bs + 8) * U32 * sg + dmu
     else:
         dsg = (bs + 8) * U32 * sg + np.minimum(dmu, dmu ** 2 / (2.0 * np.maximum(sg, 1e-300)))
-    return (oracle.round_f16(mu - dmu), oracle.round_f16(mu + dmu),
-            oracle.round_f16(sg - dsg), oracle.round_f16(sg + dsg))
+    rnd = oracle.round_f16 if rnd is None else rnd
+    return rnd(mu - dmu), rnd(mu + dmu), rnd(sg - dsg), rnd(sg + dsg)
 
 
 def f16_band(wl: Workload, q: np.ndarray, mu16: np.ndarray, sg16: np.ndarray, ranges) -> np.ndarray:
