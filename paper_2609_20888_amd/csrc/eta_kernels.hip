@@ -597,11 +597,25 @@ struct ScreenArgs {
 constexpr int kScreenThreads = 256;
 constexpr uint32_t kIdMask = 0x00ffffffu;   // union id: block index | head bits << 24
 
+// Tile of screening workgroup k.  With one-byte records a tile's coordinate row
+// is 64 bytes, half a 128-byte line; workgroups are dealt to the eight XCDs
+// (each with its own L2) round robin, so with the identity mapping the two
+// halves of every line would be fetched by two XCDs.  When the grid's x extent
+// is a multiple of 16 the mapping pairs tiles 2j and 2j + 1 on workgroups j and
+// j + 8 of each group of 16, which land on the same XCD.
+template <typename ST>
+__device__ __forceinline__ int screen_tile(int k) {
+  if constexpr (sizeof(ST) == 1) {
+    if ((gridDim.x & 15u) == 0) return (k & ~15) | ((k & 7) << 1) | ((k >> 3) & 1);
+  }
+  return k;
+}
+
 template <int D, int G, bool BOUNDS_ONLY, typename ST>
 __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
   constexpr int DQ = D / 4;            // dimensions per quarter
   const Geom& g = a.g;
-  const int tile = blockIdx.x, gh = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
+  const int tile = screen_tile<ST>(blockIdx.x), gh = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
   const int lane = tid & 63, w = tid >> 6;
   __shared__ float q_s[D][G];
   __shared__ float q2_s[D][G];
