@@ -163,6 +163,16 @@ def test_summary_variants_reject(lib):
     assert upd(ctypes.byref(d), FAKE, FAKE, FAKE, 0, 4, ctypes.byref(s), None) == eta.ETA_OK
 
 
+def test_summary_stat_dtypes_accepted(lib):
+    """fp32, fp16 and FP8 (E4M3) records pass validation (an update with no block
+    to write launches nothing and returns OK)."""
+    d = good_desc()
+    for ok in (eta.ETA_DT_F32, eta.ETA_DT_F16, eta.ETA_DT_FP8):
+        s = eta.SummaryDesc(mu=FAKE, sigma=FAKE, max_norm=FAKE, n_blk_cap=64, stat_dtype=ok)
+        assert lib.eta_update_block_summaries(ctypes.byref(d), FAKE, FAKE, FAKE, 0, 0,
+                                              ctypes.byref(s), None) == eta.ETA_OK
+
+
 def test_summary_stat_dtype_rejected(lib):
     d = good_desc()
     for bad in (eta.ETA_DT_BF16, 7):
