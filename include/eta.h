@@ -238,8 +238,12 @@ eta_status_t eta_decode(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q,
  * eta_decode_predicted -- eta_decode with the threshold predictor of Eq.
  * (tau_pred) fused into the screening launch: tau = concat(q) W + bias (W ==
  * NULL: the frozen constants bias), computed with the same summation order as
- * eta_predict_threshold, so the thresholds are bit-identical to it.  This is
- * one whole decode step of the paper's layer: predict, screen, attend.
+ * eta_predict_threshold, so the thresholds are bit-identical to it.  When the
+ * screening workgroups' re-reads of W would exceed 64 MiB per step (batch x
+ * kv heads x screening tiles x num_q_heads x head_dim x group x 4 bytes; e.g.
+ * 32 sequences at 32/8 heads and 64K capacity), the thresholds are predicted
+ * once per step in a launch of their own instead, with the same result.  This
+ * is one whole decode step of the paper's layer: predict, screen, attend.
  *   W, bias   as in eta_predict_threshold (bias required)
  *   tau_out   fp32 [batch][num_q_heads] receives the thresholds, or NULL
  * Every other argument, the results and the workspace size are as for eta_decode.

@@ -719,6 +719,8 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
           a.tau_store[hq0 + tid] = tau;
           if (a.tau_out != nullptr) a.tau_out[hq0 + tid] = tau;
         }
+      } else if (tile == 0 && a.tau_out != nullptr) {
+        a.tau_out[hq0 + tid] = tau;   // thresholds predicted by predict_kernel
       }
       teff_s[tid] = tau - a.offset_a;
     }
@@ -736,6 +738,9 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
     for (int h = 0; h < G; ++h) { dot[h] = 0.f; var[h] = 0.f; }
 #pragma unroll
     for (int i = 0; i < DQ; ++i) {
+      // keep the query's LDS reads inside the loop: hoisted out of the rescue
+      // window's loop they held ~30 registers and cost a wavefront per SIMD
+      asm volatile("" ::: "memory");
       const float s2 = sd[i] * sd[i];
 #pragma unroll
       for (int h = 0; h < G; ++h) {
@@ -1746,6 +1751,9 @@ void launch_combine_impl(const Geom& g, const CombineArgs& ca, hipStream_t strea
 
 }  // namespace
 
+// L2 bytes of W that the fused predictor may re-read per step (see launch_decode)
+constexpr int64_t kFusedPredictMaxBytes = 64ll << 20;
+
 hipError_t launch_decode(const Geom& g, const DecodeCfg& c, int q_dtype, const void* q,
                          const void* k, const void* v, const int32_t* seq_lens,
                          const eta_summary_t& s, const float* tau, const float* W,
@@ -1753,9 +1761,21 @@ hipError_t launch_decode(const Geom& g, const DecodeCfg& c, int q_dtype, const v
                          int32_t* counts, const DecodeWs& ws, hipStream_t stream,
                          LaunchHook hook) {
   const bool predict = tau == nullptr;
-  ScreenArgs sa{q, seq_lens, tau, W, bias, ws.tau, tau_out, s.mu, s.sigma, s.max_norm, mask,
-                ws.ids, ws.tile_cnt, ws.head_cnt, nullptr, g, q_dtype, predict ? 1 : 0, c.z,
-                c.offset_a, c.rescue_window, c.lwb, c.screen_all};
+  // The fused predictor reads its group's W columns in every screening
+  // workgroup: B Hkv n_tiles Hq D G 4 bytes of L2 reads per step.  Past
+  // kFusedPredictMaxBytes the thresholds are predicted once per step by
+  // predict_kernel into the workspace (the same arithmetic in the same order,
+  // so the thresholds are bit-identical) and screening reads them.
+  const bool separate = predict && W != nullptr &&
+                        (int64_t)g.B * g.Hkv * g.n_tiles * g.Hq * g.D * g.G * 4 > kFusedPredictMaxBytes;
+  if (separate) {
+    const hipError_t e0 = launch_predict(g.B, g.Hq, g.D, q_dtype, q, W, bias, ws.tau, stream, hook);
+    if (e0 != hipSuccess) return e0;
+  }
+  ScreenArgs sa{q, seq_lens, separate ? ws.tau : tau, W, bias, ws.tau, tau_out, s.mu, s.sigma,
+                s.max_norm, mask, ws.ids, ws.tile_cnt, ws.head_cnt, nullptr, g, q_dtype,
+                (predict && !separate) ? 1 : 0, c.z, c.offset_a, c.rescue_window, c.lwb,
+                c.screen_all};
   hipError_t e = with_hook(hook, ETA_KERNEL_SCREEN, stream,
                            [&] { launch_screen_impl<false>(g, sa, stream); });
   if (e != hipSuccess) return e;

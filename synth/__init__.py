@@ -223,29 +223,33 @@ def place_bias(bounds: np.ndarray, n_blocks: Sequence[int], qW: np.ndarray, targ
 
     ``bounds`` [B][Hq][N_cap] are screening bounds computed elsewhere (by the
     oracle in tests, by the GPU path in the benchmark); ``qW`` [B][Hq] is the
-    predictor output with zero bias.  Per head, the effective threshold is put
-    midway between the k-th and (k+1)-th largest bound pooled over the batch
-    (k = ceil(target * n)), so no bound sits at the threshold; the bias then
-    subtracts the batch-mean predictor output and adds back the slack ``a``.
+    predictor output with zero bias.  Sequence b's effective threshold for head
+    h is qW[b, h] + bias[h] - a, so a block survives iff bound - qW[b, h] >=
+    bias[h] - a.  Per head, bias - a is put midway between the k-th and
+    (k+1)-th largest of bound - qW[b, h] pooled over the batch's full blocks
+    (k = ceil(target * n)): exactly k blocks of the batch survive and no bound
+    sits at its threshold.  (Each sequence's predictor output shifts its own
+    threshold, so the survival of single sequences still varies.)
     """
     bounds = np.asarray(bounds, np.float64)
+    qW = np.asarray(qW, np.float64)
     B, Hq, _ = bounds.shape
     bias = np.zeros(Hq, np.float64)
     for h in range(Hq):
-        vals = np.concatenate([bounds[b, h, :n_blocks[b]] for b in range(B)])
+        vals = np.concatenate([bounds[b, h, :n_blocks[b]] - qW[b, h] for b in range(B)])
         vals = np.sort(vals[np.isfinite(vals)])[::-1]
         n = vals.shape[0]
         if n == 0:
-            tau_eff = 0.0
+            t = 0.0
         else:
             kk = int(math.ceil(target * n))
             if kk >= n:
-                tau_eff = vals[-1] - 1.0
+                t = vals[-1] - 1.0
             elif kk <= 0:
-                tau_eff = vals[0] + 1.0
+                t = vals[0] + 1.0
             else:
-                tau_eff = 0.5 * (vals[kk - 1] + vals[kk])
-        bias[h] = tau_eff + a - float(np.mean(qW[:, h]))
+                t = 0.5 * (vals[kk - 1] + vals[kk])
+        bias[h] = t + a
     return bias.astype(np.float32)
 
 

@@ -297,3 +297,41 @@ def test_config5_constant_thresholds_sampled_rows():
 
 def test_config5_predictor_sampled_rows():
     say(_full_size(config5(device="cuda", predictor=True), 16, 6))
+
+
+def test_decode_predicted_predicts_once_per_step_past_the_fused_limit():
+    """At the 32-sequence ragged shape (32/8 heads, 64K capacity) the screening
+    workgroups would re-read ~268 MB of W per step, so eta_decode_predicted runs
+    the stand-alone predictor first: one predict launch, and thresholds, mask,
+    counts and output bit-identical to eta_predict_threshold + eta_decode; a
+    small batch keeps the predictor fused (no predict launch)."""
+    dev = torch.device("cuda")
+    for wl, launches in ((config5(device="cuda", predictor=True), 1),
+                         (make_workload(B=2, Hq=8, Hkv=2, d=128, block=64, seq_lens=[9000, 4000],
+                                        planted={"frac": 0.05}, predictor=True,
+                                        target_survival=0.2, seed=61), 0)):
+        if launches == 0:
+            calibrate_bias(wl)
+        q, k, v = wl.q.to(dev), wl.k.to(dev), wl.v.to(dev)
+        sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
+        summ = eta.build_block_summaries(k, sl, wl.block, num_q_heads=wl.Hq)
+        W, bias = wl.W.to(dev), wl.bias.to(dev)
+        p = eta.decode_params(beta=wl.beta, z=wl.z, rescue_window=wl.rescue_window)
+        tau = eta.predict_threshold(q, W, bias)
+        ref = eta.decode(q, k, v, sl, summ, tau, block_size=wl.block, params=p)
+        tau_out = torch.full_like(tau, float("nan"))
+        torch.cuda.synchronize()
+        eta.profile_begin()
+        fused = eta.decode_predicted(q, k, v, sl, summ, W, bias, block_size=wl.block, params=p,
+                                     tau_out=tau_out)
+        torch.cuda.synchronize()
+        kt = eta.profile_end()
+        assert kt["predict"][1] == launches, (wl.name, kt)
+        assert torch.equal(tau_out, tau)
+        assert torch.equal(fused.mask, ref.mask) and torch.equal(fused.counts, ref.counts)
+        assert torch.equal(fused.out, ref.out)
+        say(f"[gpu] {wl.name}: predict launches {launches}, union "
+            f"{float(fused.mask.float().mean()):.3f}")
+        del q, k, v, summ, ref, fused, wl
+        torch.cuda.empty_cache()
+
