@@ -551,10 +551,37 @@ def cpu_baseline(wl, bias, budget_s):
     per_step_us = elapsed / n * 1e6
     log(f"[bench] cpu baseline {per_step_us:.0f} us/step over {n} steps "
         f"(block index {t_index:.1f} s, untimed)")
+    # the same step on one thread (a few steps: ~0.4 s each), then the thread count back
+    one_thread_us = None
+    try:
+        import ctypes
+        gomp = ctypes.CDLL("libgomp.so.1")
+        gomp.omp_set_num_threads(1)
+        m, t1 = 0, 0.0
+        while m < 2 or t1 < 1.0:
+            t0 = time.perf_counter()
+            tau = oracle.predict(q, W, b)
+            oracle.decode(q, k, v, wl.seq_lens, tau, block_size=wl.block, beta=wl.beta, z=wl.z,
+                          a=wl.a, rescue_window=wl.rescue_window, summaries=summ, rows=rows)
+            t1 += time.perf_counter() - t0
+            m += 1
+        gomp.omp_set_num_threads(threads)
+        one_thread_us = round(t1 / m * 1e6, 1)
+        log(f"[bench] cpu baseline on one thread: {one_thread_us:.0f} us/step over {m} steps")
+    except OSError:
+        pass
+    cpu_model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), None)
+    except OSError:
+        pass
     return {"value": round(per_step_us, 1), "unit": "us/step", "cores": min(threads, len(rows)),
             "kind": "oracle",
             "sample": f"the full 512K step (all {len(rows)} query heads), repeated {n}x; "
-                      f"block summaries precomputed by the oracle, untimed"}
+                      f"block summaries precomputed by the oracle, untimed",
+            "one_thread_us_per_step": one_thread_us, "cpu_model": cpu_model,
+            "omp_num_threads": os.environ.get("OMP_NUM_THREADS")}
 
 
 if __name__ == "__main__":
