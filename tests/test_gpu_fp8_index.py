@@ -194,6 +194,10 @@ FP8_DECODE = {
                           planted={"frac": 0.03}, predictor=True, target_survival=0.2, seed=191),
     "gqa4_d128_b128_const": dict(B=1, Hq=8, Hkv=2, d=128, block=128, seq_lens=[30000],
                                  planted={"frac": 0.05}, predictor=False, tau_const=2.0, seed=192),
+    # 16 screening tiles: the FP8 screening pairs neighbouring tiles on one XCD
+    "gqa4_d128_b64_16tiles": dict(B=1, Hq=8, Hkv=2, d=128, block=64, seq_lens=[65536 - 37],
+                                  planted={"frac": 0.03}, predictor=True, target_survival=0.2,
+                                  seed=193),
 }
 
 
@@ -211,3 +215,34 @@ def test_decode_on_fp8_records_matches_oracle(name):
     stats = compare(wl, g, orc, tau_o, np_inputs=np_in, band_extra=extra)
     say(f"[gpu] FP8 index {name}: {stats}, median band {float(np.median(extra)):.2e}, "
         f"max band {float(np.max(extra)):.2e}")
+
+
+def test_fp8_bounds_on_paired_tiles_match_the_oracle():
+    """eta_block_bounds on FP8 records with 32 screening tiles (the paired tile
+    order) against the oracle's bounds from its own E4M3-rounded records: fp32
+    evaluation of the same bound, so within a few fp32 ulps of the bound's
+    terms (plus the record intervals next to rounding midpoints)."""
+    wl = make_workload(B=2, Hq=8, Hkv=2, d=128, block=64, seq_lens=[2048 * 64, 2048 * 64 - 5000],
+                       planted={"frac": 0.03}, predictor=False, tau_const=1.0, seed=194)
+    np_in = oracle_inputs(wl)
+    dev = torch.device("cuda")
+    k = wl.k.to(dev)
+    sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
+    s8 = eta.build_block_summaries(k, sl, wl.block, num_q_heads=wl.Hq, stat_dtype=FP8)
+    gb = eta.block_bounds(wl.q.to(dev), sl, s8, k, block_size=wl.block, z=wl.z).cpu().numpy()
+    mu, sg, mx = oracle_summaries(wl, np_in[1])
+    mu8, sg8 = oracle.round_e4m3(mu), oracle.round_e4m3(sg)
+    r = oracle.decode(np_in[0], np_in[1], np_in[2], wl.seq_lens, None, block_size=wl.block,
+                      z=wl.z, bounds_only=True, summaries=(mu8, sg8, mx))
+    extra = f16_band(wl, np_in[0], mu8, sg8,
+                     f16_record_ranges(wl, np_in[1], mu, sg, rnd=oracle.round_e4m3))
+    worst = 0.0
+    for b in range(wl.B):
+        N = wl.seq_lens[b] // wl.block
+        ob, g = r.bounds[b, :, :N], gb[b, :, :N].astype(np.float64)
+        err = np.abs(g - ob) - extra[b, :, :N]
+        tol = 1e-5 * np.maximum(1.0, np.abs(ob))
+        assert np.all(err <= tol), (b, float(np.max(err - tol)))
+        worst = max(worst, float(np.max(np.abs(g - ob))))
+    say(f"[gpu] FP8 bounds on 32 tiles: largest difference {worst:.2e}")
+
