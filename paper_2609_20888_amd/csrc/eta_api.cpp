@@ -181,14 +181,18 @@ int default_splits(const Geom& g) {
   // streams as fast with four wavefronts per compute unit as with eight, and
   // fewer splits mean fewer partials for the combine.  Several sequences:
   // about 4096 workgroups, i.e. several rounds that the dispatcher balances
-  // over ragged lengths and unions (measured best at both 8 x 128K and 32
-  // ragged 16K-64K sequences, 5-13% faster than one round of 512).
+  // over ragged lengths and unions (32 ragged 16K-64K sequences: 5-13% faster
+  // than one round of 512, within 1-2% of 24 or 32 splits per kv head), but no
+  // split covering less than 32 blocks of capacity: a sparse union would leave
+  // such splits a few tiles each behind their prologue (8 x 128K at 18.6%
+  // union: 116.5 us per step at 64 splits vs 131.8 at 128).
   const int64_t groups = (int64_t)g.B * g.Hkv;
   const int64_t target = g.B == 1 ? 256 : 4096;
   int64_t S = (target + groups - 1) / groups;
   if (S > 256) S = 256;
-  const int64_t half = g.ncap / 2 > 0 ? g.ncap / 2 : 1;
-  if (S > half) S = half;
+  const int64_t floor_cap = g.B == 1 ? g.ncap / 2 : g.ncap / 32;
+  const int64_t cap = floor_cap > 0 ? floor_cap : 1;
+  if (S > cap) S = cap;
   if (S < 1) S = 1;
   return (int)S;
 }
