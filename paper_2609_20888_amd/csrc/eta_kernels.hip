@@ -371,8 +371,10 @@ __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ 
             const float inv_sub = 1.0f / (float)sub;
 #pragma unroll
             for (int e = 0; e < EPL; ++e) {
+              // the largest mean square deviation; its root is taken once at
+              // the end (the root is monotone, so this is the largest root)
               const float t = partial_group_sum<LPR>(v[e], ng);
-              s[e] = fmaxf(s[e], sqrtf(t * inv_sub));
+              s[e] = fmaxf(s[e], t * inv_sub);
               v[e] = 0.f;
             }
           }
@@ -383,7 +385,7 @@ __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ 
     for (int e = 0; e < EPL; ++e) {
       float sd;
       if constexpr (ENV)
-        sd = row_group_reduce<LPR>(s[e], [](float a, float c) { return fmaxf(a, c); });
+        sd = sqrtf(row_group_reduce<LPR>(s[e], [](float a, float c) { return fmaxf(a, c); }));
       else
         sd = sqrtf(row_group_reduce<LPR>(v[e], [](float a, float c) { return a + c; }) * inv_bs);
       if (rg == 0) {
