@@ -335,3 +335,50 @@ def test_decode_predicted_predicts_once_per_step_past_the_fused_limit():
         del q, k, v, summ, ref, fused, wl
         torch.cuda.empty_cache()
 
+
+
+@pytest.mark.parametrize("predictor", [True, False])
+def test_decode_step_replays_in_a_hip_graph_like_eager(predictor):
+    """A prepared decode step captured in a HIP graph (the serving loop's form):
+    replayed four times, with eager work and synchronisations between the
+    replays, every replay reproduces the eager step bit for bit (output, mask,
+    counts, thresholds).  The path records no memset nodes."""
+    wl = make_workload(B=2, Hq=8, Hkv=2, d=128, block=64, seq_lens=[20000, 9001],
+                       planted={"frac": 0.05}, predictor=predictor, target_survival=0.15,
+                       tau_const=1.6, seed=71)
+    if predictor:
+        calibrate_bias(wl)
+    dev = torch.device("cuda")
+    q, k, v = wl.q.to(dev), wl.k.to(dev), wl.v.to(dev)
+    sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
+    summ = eta.build_block_summaries(k, sl, wl.block, num_q_heads=wl.Hq)
+    W = wl.W.to(dev) if wl.W is not None else None
+    bias = wl.bias.to(dev)
+    p = eta.decode_params(beta=wl.beta, z=wl.z, rescue_window=wl.rescue_window)
+    eager = eta.DecodeStep(q, k, v, sl, summ, W, bias, block_size=wl.block, params=p)
+    eager.run()
+    torch.cuda.synchronize()
+    ref = (eager.out.clone(), eager.mask.clone(), eager.counts.clone(), eager.tau.clone())
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        warm = eta.DecodeStep(q, k, v, sl, summ, W, bias, block_size=wl.block, params=p)
+        warm.run()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step = eta.DecodeStep(q, k, v, sl, summ, W, bias, block_size=wl.block, params=p)
+        step.run()
+    for r in range(4):
+        step.out.zero_()
+        step.mask.fill_(7)
+        step.counts.fill_(-1)
+        eager.run()                     # eager work on the same inputs between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        got = (step.out, step.mask, step.counts, step.tau)
+        for name, x, y in zip(("out", "mask", "counts", "tau"), got, ref):
+            assert torch.equal(x, y), (r, name)
+    say(f"[gpu] graph replays of the decode step match eager (predictor={predictor})")
