@@ -373,7 +373,8 @@ eta_status_t eta_dense_decode(const eta_kv_desc_t* kv, int32_t q_dtype, const vo
 /* Human-readable detail of the last failure on this host thread ("" if none). */
 const char* eta_last_error_string(void);
 
-/* ABI version of this header: 1. */
+/* ABI version of this header: 3 (2: eta_summary_t carries the record type;
+ * 3: ETA_DT_FP8 records). */
 int32_t eta_abi_version(void);
 
 /*

@@ -246,7 +246,7 @@ extern "C" {
 
 const char* eta_last_error_string(void) { return g_err.c_str(); }
 
-int32_t eta_abi_version(void) { return 2; }
+int32_t eta_abi_version(void) { return 3; }
 
 static eta_status_t summaries_impl(const eta_kv_desc_t* kv, const void* k,
                                    const int32_t* prev_lens, const int32_t* seq_lens,

@@ -23,7 +23,7 @@ def test_header_declarations_are_all_exported(lib):
     assert declared == set(eta.EXPORTS), declared ^ set(eta.EXPORTS)
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.eta_abi_version() == 2
+    assert lib.eta_abi_version() == 3
 
 
 def good_desc(**kw):
