@@ -44,6 +44,9 @@ MUTANTS = {
     "e4m3_ties_away": ("    r = nearbyint(a / ulp) * ulp;   /* a / ulp is exact; default mode rounds half to even */\n  }\n  return copysign(r, x);\n}\n\nvoid eta_oracle_round_e4m3_array", "    r = round(a / ulp) * ulp;\n  }\n  return copysign(r, x);\n}\n\nvoid eta_oracle_round_e4m3_array"),
     "e4m3_no_subnormal_floor": ("if (ex < -6) ex = -6;", ";"),
     "e4m3_long_significand": ("const double ulp = ldexp(1.0, ex - 3);", "const double ulp = ldexp(1.0, ex - 4);"),
+    "e4m3_no_saturation": ("  if (a >= 464.0) {", "  if (a >= 1e300) {"),
+    "e4m3_sign_dropped": ("  }\n  return copysign(r, x);\n}\n\nvoid eta_oracle_round_e4m3_array",
+                          "  }\n  return r;\n}\n\nvoid eta_oracle_round_e4m3_array"),
     "envelope_block_divisor": ("double sd = sqrt(acc / (double)b_sub);", "double sd = sqrt(acc / (double)b);"),
     "calib_unweighted": ("const double wt = 1.0 / (double)(t + 1);", "const double wt = 1.0;"),
     "calib_weight_off_by_one": ("const double wt = 1.0 / (double)(t + 1);", "const double wt = 1.0 / (double)(t + 2);"),
