@@ -295,6 +295,24 @@ def main():
         wall_ms = (time.perf_counter() - t0) * 1e3
         return wall_ms / steps, ev0.elapsed_time(ev1) / steps
 
+    def step_percentiles(bias, steps):
+        """p10 / p50 / p90 of single-step GPU times: one event between every two
+        steps (each interval includes one event record, ~1-2 us), in a pass of
+        its own so the contract's timed loop carries no events."""
+        set_point(bias)
+        for _ in range(5):
+            step()
+        torch.cuda.synchronize()
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        evs[0].record()
+        for i in range(steps):
+            step()
+            evs[i + 1].record()
+        torch.cuda.synchronize()
+        d = sorted(evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(steps))
+        pick = lambda f: round(d[min(len(d) - 1, int(f * len(d)))], 2)
+        return {"p10": pick(0.1), "p50": pick(0.5), "p90": pick(0.9)}
+
     def kernel_times(bias, steps):
         """Per-kernel durations: HIP events recorded by the library around each launch."""
         set_point(bias)
@@ -352,8 +370,10 @@ def main():
         ms, gpu_ms = time_point(biases[s], steps, warm)
         kv_b, step_b, ub, dh, du = algorithmic(mask.cpu().numpy())
         kt = kernel_times(biases[s], steps) if is_primary else None
+        pct = step_percentiles(biases[s], steps) if is_primary else None
         cold_ms = cold_point(biases[s], 20)
         entry = {"survival_target": s, "us_per_step": round(ms * 1e3, 2),
+                 **({"step_us_percentiles": pct} if pct else {}),
                  "gpu_us_per_step": round(gpu_ms * 1e3, 2), "cold_us_per_step": round(cold_ms * 1e3, 2),
                  "d_head": round(dh, 4), "d_union": round(du, 4), "union_blocks": ub,
                  "step_bytes": step_b, "effective_GBps": round(step_b / ms / 1e6, 1),
