@@ -225,14 +225,18 @@ eta_status_t eta_decode_workspace_size(const eta_kv_desc_t* kv, const eta_decode
  *                      by that head (threshold, pin or rescue); 0 elsewhere, including
  *                      every entry j >= N
  *   head_token_counts  int32 [batch][num_q_heads] attended tokens per head, or NULL
+ *   union_counts       int32 [batch][num_kv_heads] blocks of the GQA union (the full blocks
+ *                      read from HBM for that kv head: selected by any of its G query
+ *                      heads), or NULL; the count App. "Top-1 Rescue, Tail Handling, and
+ *                      Kernel Validation" checks as "GQA union blocks"
  *   workspace          >= eta_decode_workspace_size() bytes, 256-byte aligned
  * Results are deterministic: the same inputs give bitwise-identical outputs.
  */
 eta_status_t eta_decode(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q, const void* k,
                         const void* v, const int32_t* seq_lens, const eta_summary_t* summ,
                         const float* tau, const eta_decode_params_t* p, void* out,
-                        uint8_t* block_mask, int32_t* head_token_counts, void* workspace,
-                        size_t workspace_bytes, void* stream);
+                        uint8_t* block_mask, int32_t* head_token_counts, int32_t* union_counts,
+                        void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * eta_decode_predicted -- eta_decode with the threshold predictor of Eq.
@@ -252,8 +256,9 @@ eta_status_t eta_decode_predicted(const eta_kv_desc_t* kv, int32_t q_dtype, cons
                                   const void* k, const void* v, const int32_t* seq_lens,
                                   const eta_summary_t* summ, const float* W, const float* bias,
                                   const eta_decode_params_t* p, void* out, uint8_t* block_mask,
-                                  int32_t* head_token_counts, float* tau_out, void* workspace,
-                                  size_t workspace_bytes, void* stream);
+                                  int32_t* head_token_counts, int32_t* union_counts,
+                                  float* tau_out, void* workspace, size_t workspace_bytes,
+                                  void* stream);
 
 /*
  * Offline density-matched calibration of static per-head thresholds (App.
@@ -373,8 +378,9 @@ eta_status_t eta_dense_decode(const eta_kv_desc_t* kv, int32_t q_dtype, const vo
 /* Human-readable detail of the last failure on this host thread ("" if none). */
 const char* eta_last_error_string(void);
 
-/* ABI version of this header: 3 (2: eta_summary_t carries the record type;
- * 3: ETA_DT_FP8 records). */
+/* ABI version of this header: 4 (2: eta_summary_t carries the record type;
+ * 3: ETA_DT_FP8 records; 4: eta_decode / eta_decode_predicted return the
+ * per-(sequence, kv head) union counts). */
 int32_t eta_abi_version(void);
 
 /*

@@ -246,7 +246,7 @@ extern "C" {
 
 const char* eta_last_error_string(void) { return g_err.c_str(); }
 
-int32_t eta_abi_version(void) { return 3; }
+int32_t eta_abi_version(void) { return 4; }
 
 static eta_status_t summaries_impl(const eta_kv_desc_t* kv, const void* k,
                                    const int32_t* prev_lens, const int32_t* seq_lens,
@@ -324,8 +324,8 @@ static eta_status_t decode_impl(const eta_kv_desc_t* kv, int32_t q_dtype, const 
                                 const eta_summary_t* summ, const float* tau, const float* W,
                                 const float* bias, float* tau_out,
                                 const eta_decode_params_t* p, void* out, uint8_t* block_mask,
-                                int32_t* head_token_counts, void* workspace,
-                                size_t workspace_bytes, void* stream) {
+                                int32_t* head_token_counts, int32_t* union_counts,
+                                void* workspace, size_t workspace_bytes, void* stream) {
   Geom g;
   eta_status_t st = check_kv(kv, &g);
   if (st) return st;
@@ -335,7 +335,8 @@ static eta_status_t decode_impl(const eta_kv_desc_t* kv, int32_t q_dtype, const 
     return fail(ETA_ERR_INVALID_ARG, "q, k, v, seq_lens, out and block_mask must be non-NULL");
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(seq_lens) ||
       !aligned16(out) || !aligned16(block_mask) ||
-      (head_token_counts && !aligned16(head_token_counts)) || (tau && !aligned16(tau)) ||
+      (head_token_counts && !aligned16(head_token_counts)) ||
+      (union_counts && !aligned16(union_counts)) || (tau && !aligned16(tau)) ||
       (W && !aligned16(W)) || (bias && !aligned16(bias)) || (tau_out && !aligned16(tau_out)))
     return fail(ETA_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
   // the mask and the workspace are laid out with the summary capacity
@@ -351,8 +352,8 @@ static eta_status_t decode_impl(const eta_kv_desc_t* kv, int32_t q_dtype, const 
   DecodeCfg c{p->beta, p->z, p->offset_a, p->rescue_window_blocks, p->pin_recent_blocks,
               p->self_ungated ? 1 : 0, p->screen_all ? 1 : 0, S};
   hipError_t e = launch_decode(g, c, q_dtype, q, k, v, seq_lens, *summ, tau, W, bias, tau_out,
-                               out, block_mask, head_token_counts, ws, (hipStream_t)stream,
-                               active_hook());
+                               out, block_mask, head_token_counts, union_counts, ws,
+                               (hipStream_t)stream, active_hook());
   if (e != hipSuccess) return fail(ETA_ERR_HIP, "decode launch failed: %s", hipGetErrorString(e));
   return ok();
 }
@@ -360,22 +361,25 @@ static eta_status_t decode_impl(const eta_kv_desc_t* kv, int32_t q_dtype, const 
 eta_status_t eta_decode(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q, const void* k,
                         const void* v, const int32_t* seq_lens, const eta_summary_t* summ,
                         const float* tau, const eta_decode_params_t* p, void* out,
-                        uint8_t* block_mask, int32_t* head_token_counts, void* workspace,
-                        size_t workspace_bytes, void* stream) {
+                        uint8_t* block_mask, int32_t* head_token_counts, int32_t* union_counts,
+                        void* workspace, size_t workspace_bytes, void* stream) {
   if (!tau) return fail(ETA_ERR_INVALID_ARG, "tau must be non-NULL");
   return decode_impl(kv, q_dtype, q, k, v, seq_lens, summ, tau, nullptr, nullptr, nullptr, p, out,
-                     block_mask, head_token_counts, workspace, workspace_bytes, stream);
+                     block_mask, head_token_counts, union_counts, workspace, workspace_bytes,
+                     stream);
 }
 
 eta_status_t eta_decode_predicted(const eta_kv_desc_t* kv, int32_t q_dtype, const void* q,
                                   const void* k, const void* v, const int32_t* seq_lens,
                                   const eta_summary_t* summ, const float* W, const float* bias,
                                   const eta_decode_params_t* p, void* out, uint8_t* block_mask,
-                                  int32_t* head_token_counts, float* tau_out, void* workspace,
-                                  size_t workspace_bytes, void* stream) {
+                                  int32_t* head_token_counts, int32_t* union_counts,
+                                  float* tau_out, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
   if (!bias) return fail(ETA_ERR_INVALID_ARG, "bias must be non-NULL");
   return decode_impl(kv, q_dtype, q, k, v, seq_lens, summ, nullptr, W, bias, tau_out, p, out,
-                     block_mask, head_token_counts, workspace, workspace_bytes, stream);
+                     block_mask, head_token_counts, union_counts, workspace, workspace_bytes,
+                     stream);
 }
 
 static eta_status_t check_calib(const eta_calib_desc_t* cd, const eta_calib_state_t* st) {

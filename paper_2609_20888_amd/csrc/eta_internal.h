@@ -72,7 +72,8 @@ hipError_t launch_decode(const Geom& g, const DecodeCfg& c, int q_dtype, const v
                          const void* k, const void* v, const int32_t* seq_lens,
                          const eta_summary_t& s, const float* tau, const float* W,
                          const float* bias, float* tau_out, void* out, uint8_t* mask,
-                         int32_t* counts, const DecodeWs& ws, hipStream_t stream, LaunchHook hook);
+                         int32_t* counts, int32_t* union_counts, const DecodeWs& ws,
+                         hipStream_t stream, LaunchHook hook);
 
 hipError_t launch_bounds(const Geom& g, int q_dtype, const void* q, const int32_t* seq_lens,
                          const eta_summary_t& s, float z, float* bounds, hipStream_t stream,

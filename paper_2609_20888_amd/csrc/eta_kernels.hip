@@ -1590,8 +1590,10 @@ struct CombineArgs {
   const float2* part_ml;
   const float* part_acc;
   const int32_t* head_cnt;
+  const int32_t* tile_cnt;
   const int32_t* seq_lens;
   int32_t* counts;
+  int32_t* union_counts;
   void* out;
   Geom g;
   int q_dtype;
@@ -1631,10 +1633,17 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
   const int64_t row = (int64_t)b * g.Hq + h;
   const float2* ml = a.part_ml + row * a.S;
   const float* accp = a.part_acc + row * a.S * D + i;
-  // per-head selected blocks: wavefront 0 sums the tile counts (issued first)
+  // per-head selected blocks: wavefront 0 sums the head's tile counts; the
+  // union blocks of the (sequence, kv head): wavefront 1 of the group's first
+  // head sums the union's tile counts (both issued first)
   int cnt = 0;
   if (a.counts != nullptr && tid < 64)
     for (int t = tid; t < g.n_tiles; t += 64) cnt += a.head_cnt[row * g.n_tiles + t];
+  const bool do_union = a.union_counts != nullptr && h % g.G == 0 && tid >= 64 && tid < 128;
+  const int64_t bg = (int64_t)b * g.Hkv + h / g.G;
+  int ucnt = 0;
+  if (do_union)
+    for (int t = tid - 64; t < g.n_tiles; t += 64) ucnt += a.tile_cnt[bg * g.n_tiles + t];
   float2 mv[kCombPrefetch];
   float av[kCombPrefetch];
   float mloc = kNegInf;
@@ -1683,6 +1692,11 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
       const int64_t N = T / g.BS;
       a.counts[row] = (int32_t)((int64_t)cnt * g.BS + (T - N * g.BS));
     }
+  }
+  if (do_union) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) ucnt += __shfl_xor(ucnt, o, 64);
+    if (tid == 64) a.union_counts[bg] = ucnt;
   }
 }
 
@@ -1785,8 +1799,8 @@ hipError_t launch_decode(const Geom& g, const DecodeCfg& c, int q_dtype, const v
                          const void* k, const void* v, const int32_t* seq_lens,
                          const eta_summary_t& s, const float* tau, const float* W,
                          const float* bias, float* tau_out, void* out, uint8_t* mask,
-                         int32_t* counts, const DecodeWs& ws, hipStream_t stream,
-                         LaunchHook hook) {
+                         int32_t* counts, int32_t* union_counts, const DecodeWs& ws,
+                         hipStream_t stream, LaunchHook hook) {
   const bool predict = tau == nullptr;
   // The fused predictor reads its group's W columns in every screening
   // workgroup: B Hkv n_tiles Hq D G 4 bytes of L2 reads per step.  Past
@@ -1811,7 +1825,8 @@ hipError_t launch_decode(const Geom& g, const DecodeCfg& c, int q_dtype, const v
   e = with_hook(hook, ETA_KERNEL_SPLIT_DECODE, stream,
                 [&] { launch_split_impl<false>(g, c.S, sp, stream); });
   if (e != hipSuccess) return e;
-  CombineArgs ca{ws.part_ml, ws.part_acc, ws.head_cnt, seq_lens, counts, out, g, q_dtype, c.S};
+  CombineArgs ca{ws.part_ml, ws.part_acc, ws.head_cnt, ws.tile_cnt, seq_lens, counts,
+                 union_counts, out, g, q_dtype, c.S};
   return with_hook(hook, ETA_KERNEL_COMBINE, stream, [&] { launch_combine_impl(g, ca, stream); });
 }
 
@@ -1857,7 +1872,8 @@ hipError_t launch_dense(const Geom& g, int S, int q_dtype, const void* q, const 
   hipError_t e = with_hook(hook, ETA_KERNEL_DENSE_SPLIT, stream,
                            [&] { launch_split_impl<true>(g, S, sp, stream); });
   if (e != hipSuccess) return e;
-  CombineArgs ca{ws.part_ml, ws.part_acc, nullptr, seq_lens, nullptr, out, g, q_dtype, S};
+  CombineArgs ca{ws.part_ml, ws.part_acc, nullptr, nullptr, seq_lens, nullptr, nullptr, out, g,
+                 q_dtype, S};
   return with_hook(hook, ETA_KERNEL_DENSE_COMBINE, stream,
                    [&] { launch_combine_impl(g, ca, stream); });
 }

@@ -108,9 +108,9 @@ def load_library(path: Optional[str] = None):
         "eta_predict_threshold": [i32, i32, i32, i32, _vp, _vp, _vp, _vp, _vp],
         "eta_decode_workspace_size": [P(KvDesc), P(DecodeParams), P(sz)],
         "eta_decode": [P(KvDesc), i32, _vp, _vp, _vp, _vp, P(SummaryDesc), _vp, P(DecodeParams),
-                       _vp, _vp, _vp, _vp, sz, _vp],
+                       _vp, _vp, _vp, _vp, _vp, sz, _vp],
         "eta_decode_predicted": [P(KvDesc), i32, _vp, _vp, _vp, _vp, P(SummaryDesc), _vp, _vp,
-                                 P(DecodeParams), _vp, _vp, _vp, _vp, _vp, sz, _vp],
+                                 P(DecodeParams), _vp, _vp, _vp, _vp, _vp, _vp, sz, _vp],
         "eta_block_bounds": [P(KvDesc), i32, _vp, _vp, P(SummaryDesc), f32, _vp, _vp],
         "eta_dense_workspace_size": [P(KvDesc), i32, P(sz)],
         "eta_dense_decode": [P(KvDesc), i32, _vp, _vp, _vp, _vp, _vp, i32, _vp, sz, _vp],
@@ -272,38 +272,49 @@ class DecodeOut:
     out: torch.Tensor            # [B][Hq][d], dtype of q
     mask: torch.Tensor           # [B][Hq][n_blk_cap] uint8
     counts: Optional[torch.Tensor]  # [B][Hq] int32
+    union_counts: Optional[torch.Tensor] = None  # [B][Hkv] int32 GQA union blocks
 
 
-def decode(q, k, v, seq_lens, summ: Summaries, tau, *, block_size: int,
-           params: Optional[DecodeParams] = None, out=None, mask=None, counts=None,
-           want_counts: bool = True, workspace: Optional[torch.Tensor] = None,
-           stream=None) -> DecodeOut:
-    """eta_decode: one ETA decode step -> output, selected-block mask, attended token counts."""
-    B, Hq, d = q.shape
-    p = params if params is not None else decode_params()
-    desc = kv_desc(k, Hq, block_size)
-    if v.shape != k.shape or v.stride() != k.stride() or v.dtype != k.dtype:
-        raise ValueError("K and V must share shape, strides and dtype")
+def _decode_outputs(q, k, summ, out, mask, counts, union_counts, want_counts):
+    B, Hq, _ = q.shape
     if out is None:
         out = torch.empty_like(q)
     if mask is None:
         mask = torch.empty(B, Hq, summ.n_blk_cap, dtype=torch.uint8, device=q.device)
     if counts is None and want_counts:
         counts = torch.empty(B, Hq, dtype=torch.int32, device=q.device)
+    if union_counts is None and want_counts:
+        union_counts = torch.empty(B, k.shape[1], dtype=torch.int32, device=q.device)
+    return out, mask, counts, union_counts
+
+
+def decode(q, k, v, seq_lens, summ: Summaries, tau, *, block_size: int,
+           params: Optional[DecodeParams] = None, out=None, mask=None, counts=None,
+           union_counts=None, want_counts: bool = True,
+           workspace: Optional[torch.Tensor] = None, stream=None) -> DecodeOut:
+    """eta_decode: one ETA decode step -> output, selected-block mask, attended token
+    counts per head and GQA union counts per (sequence, kv head)."""
+    B, Hq, d = q.shape
+    p = params if params is not None else decode_params()
+    desc = kv_desc(k, Hq, block_size)
+    if v.shape != k.shape or v.stride() != k.stride() or v.dtype != k.dtype:
+        raise ValueError("K and V must share shape, strides and dtype")
+    out, mask, counts, union_counts = _decode_outputs(q, k, summ, out, mask, counts, union_counts,
+                                                      want_counts)
     nbytes = decode_workspace_size(desc, p)
     if workspace is None or workspace.numel() < nbytes:
         workspace = alloc_workspace(nbytes, q.device)
     sd = summ.desc()
     _check(load_library().eta_decode(ctypes.byref(desc), _dtype_code(q), _ptr(q), _ptr(k), _ptr(v),
                                      _ptr(seq_lens), ctypes.byref(sd), _ptr(tau), ctypes.byref(p),
-                                     _ptr(out), _ptr(mask), _ptr(counts), _ptr(workspace),
-                                     workspace.numel(), _stream(stream)))
-    return DecodeOut(out=out, mask=mask, counts=counts)
+                                     _ptr(out), _ptr(mask), _ptr(counts), _ptr(union_counts),
+                                     _ptr(workspace), workspace.numel(), _stream(stream)))
+    return DecodeOut(out=out, mask=mask, counts=counts, union_counts=union_counts)
 
 
 def decode_predicted(q, k, v, seq_lens, summ: Summaries, W, bias, *, block_size: int,
                      params: Optional[DecodeParams] = None, out=None, mask=None, counts=None,
-                     tau_out=None, want_counts: bool = True,
+                     union_counts=None, tau_out=None, want_counts: bool = True,
                      workspace: Optional[torch.Tensor] = None, stream=None) -> DecodeOut:
     """eta_decode_predicted: predictor fused into the decode step (tau = concat(q) W + bias)."""
     B, Hq, d = q.shape
@@ -311,12 +322,8 @@ def decode_predicted(q, k, v, seq_lens, summ: Summaries, W, bias, *, block_size:
     desc = kv_desc(k, Hq, block_size)
     if v.shape != k.shape or v.stride() != k.stride() or v.dtype != k.dtype:
         raise ValueError("K and V must share shape, strides and dtype")
-    if out is None:
-        out = torch.empty_like(q)
-    if mask is None:
-        mask = torch.empty(B, Hq, summ.n_blk_cap, dtype=torch.uint8, device=q.device)
-    if counts is None and want_counts:
-        counts = torch.empty(B, Hq, dtype=torch.int32, device=q.device)
+    out, mask, counts, union_counts = _decode_outputs(q, k, summ, out, mask, counts, union_counts,
+                                                      want_counts)
     nbytes = decode_workspace_size(desc, p)
     if workspace is None or workspace.numel() < nbytes:
         workspace = alloc_workspace(nbytes, q.device)
@@ -324,8 +331,9 @@ def decode_predicted(q, k, v, seq_lens, summ: Summaries, W, bias, *, block_size:
     _check(load_library().eta_decode_predicted(
         ctypes.byref(desc), _dtype_code(q), _ptr(q), _ptr(k), _ptr(v), _ptr(seq_lens),
         ctypes.byref(sd), _ptr(W), _ptr(bias), ctypes.byref(p), _ptr(out), _ptr(mask),
-        _ptr(counts), _ptr(tau_out), _ptr(workspace), workspace.numel(), _stream(stream)))
-    return DecodeOut(out=out, mask=mask, counts=counts)
+        _ptr(counts), _ptr(union_counts), _ptr(tau_out), _ptr(workspace), workspace.numel(),
+        _stream(stream)))
+    return DecodeOut(out=out, mask=mask, counts=counts, union_counts=union_counts)
 
 
 class DecodeStep:
@@ -345,14 +353,16 @@ class DecodeStep:
         self.out = torch.empty_like(q)
         self.mask = torch.empty(B, Hq, summ.n_blk_cap, dtype=torch.uint8, device=q.device)
         self.counts = torch.empty(B, Hq, dtype=torch.int32, device=q.device) if want_counts else None
+        self.union_counts = (torch.empty(B, k.shape[1], dtype=torch.int32, device=q.device)
+                             if want_counts else None)
         self.tau = torch.empty(B, Hq, dtype=torch.float32, device=q.device)
         self.workspace = alloc_workspace(decode_workspace_size(self.desc, self.params), q.device)
         self._fn = load_library().eta_decode_predicted
         self._args = (ctypes.byref(self.desc), _dtype_code(q), _ptr(q), _ptr(k), _ptr(v),
                       _ptr(seq_lens), ctypes.byref(self.sdesc), _ptr(W), _ptr(bias),
                       ctypes.byref(self.params), _ptr(self.out), _ptr(self.mask),
-                      _ptr(self.counts), _ptr(self.tau), _ptr(self.workspace),
-                      self.workspace.numel(), _stream(stream))
+                      _ptr(self.counts), _ptr(self.union_counts), _ptr(self.tau),
+                      _ptr(self.workspace), self.workspace.numel(), _stream(stream))
 
     def run(self) -> None:
         st = self._fn(*self._args)

@@ -1,18 +1,21 @@
 """Helpers for the GPU parity tests: run a workload through the HIP library
 (C ABI via the binding) and through the fp64 oracle, and compare.
 
-Parity rules (the path's contract):
+Parity rules (the path's contract), applied to every requested row (no row is
+ever skipped):
   * block masks: identical, except blocks whose oracle bound lies within
     TIE_BAND of tau_eff (the fp32 GPU and fp64 oracle may decide those either
-    way).  Such a row is compared against the oracle re-run (external-mask
-    mode) on the variant of the oracle's own mask that flips exactly the band
-    blocks the GPU decided the other way.  A rescue decision may differ only
-    when the rescue window's two largest bounds are within TIE_BAND of each
-    other; such rows are checked outside the window only and counted as
-    skipped.
-  * attended-token counts: identical on rows compared.
+    way); inside the top-1 rescue window the GPU's selection must be one the
+    algorithm reaches from bounds within that band of the oracle's (a flipped
+    band block can switch rescue on or off; two window bounds within the band
+    of each other can swap the rescued block).
+  * attended-token counts: identical to the oracle's for the GPU's mask.
   * outputs: max_i |o_gpu - o_ref| / max_i |o_ref| per (sequence, head) row
-    <= 2e-2 for bf16 and <= 1e-4 for fp32.
+    <= 2e-2 for bf16 and <= 1e-4 for fp32, o_ref the oracle's output for the
+    GPU's mask (its own when the masks agree, else the oracle re-run on the GPU's
+    mask in its external-mask mode).
+  * union counts per (sequence, kv head): identical to the union of the GPU's
+    mask (which the first rule ties to the oracle's).
 """
 from __future__ import annotations
 
@@ -49,18 +52,20 @@ class GpuRun:
     counts: torch.Tensor
     tau: torch.Tensor
     summ: eta.Summaries
+    union_counts: Optional[torch.Tensor] = None
 
 
 def oracle_inputs(wl: Workload):
     return as_numpy(wl.q), as_numpy(wl.k), as_numpy(wl.v)
 
 
-def calibrate_bias(wl: Workload, np_inputs=None) -> None:
+def calibrate_bias(wl: Workload, np_inputs=None, summaries=None) -> None:
     """Predictor-mode workloads: set wl.bias from the oracle's bounds for the target survival."""
     if wl.W is None or wl.target_survival is None:
         return
     q, k, v = np_inputs or oracle_inputs(wl)
-    r = oracle.decode(q, k, v, wl.seq_lens, None, block_size=wl.block, z=wl.z, bounds_only=True)
+    r = oracle.decode(q, k, v, wl.seq_lens, None, block_size=wl.block, z=wl.z, bounds_only=True,
+                      summaries=summaries)
     qW = oracle.predict(q, as_numpy(wl.W), None)
     nb = [t // wl.block for t in wl.seq_lens]
     bias = place_bias(r.bounds, nb, qW, wl.target_survival, wl.a)
@@ -85,7 +90,8 @@ def run_gpu(wl: Workload, *, num_splits: int = 0, screen_all: bool = False,
                           num_splits=num_splits)
     r = eta.decode(q, k, v, sl, summ, tau, block_size=wl.block, params=p)
     torch.cuda.synchronize()
-    return GpuRun(out=r.out, mask=r.mask, counts=r.counts, tau=tau, summ=summ)
+    return GpuRun(out=r.out, mask=r.mask, counts=r.counts, tau=tau, summ=summ,
+                  union_counts=r.union_counts)
 
 
 def oracle_summaries(wl: Workload, k: np.ndarray, sub_block: int = 0):
@@ -119,17 +125,6 @@ def run_oracle(wl: Workload, np_inputs=None, rows: Optional[Sequence[int]] = Non
 
 def _f64(t: torch.Tensor) -> np.ndarray:
     return t.detach().float().cpu().numpy().astype(np.float64)
-
-
-def _band_variants(om: np.ndarray, band_idx: np.ndarray):
-    """The oracle's mask with every subset of the tie-band blocks flipped."""
-    k = band_idx.size
-    for bitsel in range(1 << k):
-        m = om.copy()
-        for t in range(k):
-            if (bitsel >> t) & 1:
-                m[band_idx[t]] ^= 1
-        yield m
 
 
 U32 = 2.0 ** -24   # fp32 unit roundoff
@@ -195,19 +190,54 @@ def _q64(q: np.ndarray) -> np.ndarray:
     return q.astype(np.float64)
 
 
-def compare(wl: Workload, g: GpuRun, orc, tau_oracle: np.ndarray,
-            rows: Optional[Sequence[int]] = None, min_compared: float = 0.9,
-            rescue_window: Optional[int] = None, np_inputs=None, screen_all: bool = False,
-            self_ungated: bool = False, max_band: int = 6,
-            band_extra: Optional[np.ndarray] = None) -> dict:
-    """Check masks / counts / outputs of the given rows; returns statistics.
+def _window_admissible(gm: np.ndarray, om: np.ndarray, rescued: int, bnd: np.ndarray,
+                       band: np.ndarray, Wn: int, c: int, slack: float) -> Optional[str]:
+    """Whether the GPU's selection gm inside the rescue window [0, Wn) is one the
+    algorithm can reach from bounds that differ from the oracle's only inside the
+    tie band.  om is the oracle's final selection, rescued its rescued block (-1:
+    none).  The GPU either kept its threshold / pin selection (a set between the
+    oracle's certain and possible selections, non-empty when rescue is on), or
+    selected nothing by threshold there (possible only when the oracle's window
+    holds no certain selection) and rescued one block whose bound is within the
+    band of the window's largest.  Returns None when admissible, else why not."""
+    if Wn <= 0:
+        return None
+    thr = om[:Wn].copy()
+    if rescued >= 0:
+        thr[rescued] = 0
+    certain = (thr == 1) & ~band[:Wn]
+    possible = (thr == 1) | band[:Wn]
+    A = gm[:Wn] == 1
+    if np.all(A[certain]) and not np.any(A & ~possible) and (A.any() or c == 0):
+        return None                      # threshold / pin selection, no rescue
+    if certain.any():
+        return f"window blocks {np.nonzero(certain & ~A)[0][:4].tolist()} certainly selected"
+    if A.sum() != 1:
+        return f"rescue would select one block, GPU has {int(A.sum())} in the window"
+    j = int(np.nonzero(A)[0][0])
+    fin = bnd[:Wn][np.isfinite(bnd[:Wn])]
+    if fin.size == 0 or not np.isfinite(bnd[j]) or bnd[j] < fin.max() - slack:
+        return f"rescued block {j} is not within the band of the window's largest bound"
+    return None
 
-    A row whose oracle bounds put blocks inside the tie band is compared
-    against the oracle run on each of its own masks with those blocks flipped
-    (the oracle's external-mask mode): the GPU mask must be one of them and the
-    GPU output must match the oracle output for that mask.
+
+def compare(wl: Workload, g: GpuRun, orc, tau_oracle: np.ndarray,
+            rows: Optional[Sequence[int]] = None, rescue_window: Optional[int] = None,
+            np_inputs=None, screen_all: bool = False, self_ungated: bool = False,
+            band_extra: Optional[np.ndarray] = None, union_counts=None) -> dict:
+    """Check masks / counts / outputs of the given rows (every row by default); returns
+    statistics.  Every requested row is compared; none is skipped.
+
+    Mask: equal to the oracle's except at tie-band blocks; inside the rescue
+    window the GPU's selection must be one the algorithm reaches from bounds
+    within the band of the oracle's (_window_admissible).  Output and attended
+    count: against the oracle's own result where the masks agree, else against
+    the oracle re-run on the GPU's mask (its external-mask mode), the parity
+    protocol's second step.  union_counts ([B][Hkv], optional): the GQA union of
+    the GPU's mask for every (sequence, kv head) whose rows are all compared.
     """
     B, Hq = wl.B, wl.Hq
+    G = wl.G
     rows = list(range(B * Hq)) if rows is None else list(rows)
     c = wl.rescue_window if rescue_window is None else rescue_window
     mask = g.mask.cpu().numpy()
@@ -215,7 +245,8 @@ def compare(wl: Workload, g: GpuRun, orc, tau_oracle: np.ndarray,
     out = _f64(g.out)
     tol = TOL[wl.dtype]
     Ncap = wl.n_blk_cap
-    compared, banded, skipped, worst = 0, 0, 0, 0.0
+    banded, worst = 0, 0.0
+    ext_rows = []
     for row in rows:
         b, h = divmod(row, Hq)
         N = wl.seq_lens[b] // wl.block
@@ -226,52 +257,54 @@ def compare(wl: Workload, g: GpuRun, orc, tau_oracle: np.ndarray,
         teff = tau_oracle[b, h] - wl.a
         extra = band_extra[b, h, :N] if band_extra is not None else np.zeros(N)
         band = (np.abs(bnd - teff) <= TIE_BAND + extra) if not screen_all else np.zeros(N, bool)
-        Wn = min(c, N)
-        rescue_tie = False
-        if Wn >= 2 and c > 0 and orc.rescued[b, h] >= 0:
-            top = np.sort(bnd[:Wn])[::-1]
-            rescue_tie = bool(top[0] - top[1] <= TIE_BAND + 2.0 * float(np.max(extra[:Wn])))
+        Wn = min(c, N) if c > 0 else 0
         diff = np.nonzero(gm[:N] != om)[0]
-        ref_o, ref_n = orc.o[b, h], orc.counts[b, h]
-        if rescue_tie:
-            skipped += 1
-            bad = [j for j in diff if not band[j] and j >= Wn]
-            assert not bad, f"row {row}: mask differs outside the rescue window / tie band at {bad[:8]}"
-            continue
+        bad = [int(j) for j in diff if j >= Wn and not band[j]]
+        assert not bad, (f"row {row}: mask differs outside the tie band at blocks {bad[:8]} "
+                         f"(bounds {bnd[bad[:4]]}, tau_eff {teff})")
+        if not screen_all:
+            why = _window_admissible(gm[:N], om, int(orc.rescued[b, h]), bnd, band, Wn, c,
+                                     2.0 * TIE_BAND + 2.0 * float(np.max(extra[:Wn], initial=0.0)))
+            assert why is None, f"row {row}: rescue window not admissible: {why}"
+        else:
+            assert diff.size == 0, f"row {row}: screen_all mask differs at {diff[:8].tolist()}"
         if band.any():
             banded += 1
-            bad = [j for j in diff if not band[j]]
-            assert not bad, f"row {row}: mask differs outside the tie band at blocks {bad[:8]}"
-            bidx = np.nonzero(band)[0]
-            if bidx.size > max_band:
-                skipped += 1
-                continue
-            assert np_inputs is not None, "tie-band rows need the oracle inputs"
-            q, k, v = np_inputs
-            found = False
-            for var in _band_variants(om, bidx):
-                full = np.zeros((B, Hq, max(Ncap, 1)), np.uint8)
-                full[b, h, :N] = var
-                rv = oracle.decode(q, k, v, wl.seq_lens, tau_oracle, block_size=wl.block,
-                                   beta=wl.beta, z=wl.z, a=wl.a, rescue_window=c, lwb=wl.lwb,
-                                   self_ungated=self_ungated, rows=[row], sel_in=full[:, :, :Ncap])
-                if np.array_equal(var, gm[:N]):
-                    ref_o, ref_n = rv.o[b, h], rv.counts[b, h]
-                    found = True
-            assert found, f"row {row}: GPU mask is not any tie-band variant of the oracle mask"
-        else:
-            assert diff.size == 0, (f"row {row}: mask differs at blocks {diff[:8].tolist()} "
-                                    f"(bounds {bnd[diff[:4]]}, tau_eff {teff})")
-        assert counts[b, h] == ref_n, f"row {row}: counts {counts[b, h]} vs {ref_n}"
-        scale = np.max(np.abs(ref_o))
-        if scale == 0.0:
-            assert np.all(out[b, h] == 0.0), f"row {row}: expected a zero output"
-            compared += 1
+        if diff.size:
+            ext_rows.append(row)
             continue
-        err = float(np.max(np.abs(out[b, h] - ref_o)) / scale)
-        worst = max(worst, err)
-        assert err <= tol, f"row {row}: max rel error {err:.3e} > {tol:.1e}"
-        compared += 1
-    assert compared >= min_compared * len(rows), \
-        f"only {compared} of {len(rows)} rows compared ({skipped} skipped)"
-    return {"compared": compared, "band_rows": banded, "skipped": skipped, "worst_rel_err": worst}
+        worst = max(worst, _check_row(row, b, h, out, counts, orc.o[b, h], orc.counts[b, h], tol))
+    if ext_rows:
+        assert np_inputs is not None, "rows whose mask differs in the tie band need the oracle inputs"
+        q, k, v = np_inputs
+        rv = oracle.decode(q, k, v, wl.seq_lens, tau_oracle, block_size=wl.block, beta=wl.beta,
+                           z=wl.z, a=wl.a, rescue_window=c, lwb=wl.lwb, self_ungated=self_ungated,
+                           rows=ext_rows, sel_in=mask[:, :, :Ncap], n_threads=0)
+        for row in ext_rows:
+            b, h = divmod(row, Hq)
+            worst = max(worst, _check_row(row, b, h, out, counts, rv.o[b, h], rv.counts[b, h], tol))
+    union_checked = 0
+    if union_counts is not None:
+        uc = union_counts.cpu().numpy() if hasattr(union_counts, "cpu") else np.asarray(union_counts)
+        rowset = set(rows)
+        for b in range(B):
+            N = wl.seq_lens[b] // wl.block
+            for gg in range(wl.Hkv):
+                if all(b * Hq + gg * G + r in rowset for r in range(G)):
+                    ref = int(mask[b, gg * G:(gg + 1) * G, :N].any(axis=0).sum())
+                    assert int(uc[b, gg]) == ref, f"union count of ({b}, {gg}): {uc[b, gg]} vs {ref}"
+                    union_checked += 1
+    return {"rows": len(rows), "compared": len(rows), "band_rows": banded,
+            "external_mask_rows": len(ext_rows), "union_counts_checked": union_checked,
+            "worst_rel_err": worst}
+
+
+def _check_row(row, b, h, out, counts, ref_o, ref_n, tol) -> float:
+    assert counts[b, h] == ref_n, f"row {row}: counts {counts[b, h]} vs {ref_n}"
+    scale = np.max(np.abs(ref_o))
+    if scale == 0.0:
+        assert np.all(out[b, h] == 0.0), f"row {row}: expected a zero output"
+        return 0.0
+    err = float(np.max(np.abs(out[b, h] - ref_o)) / scale)
+    assert err <= tol, f"row {row}: max rel error {err:.3e} > {tol:.1e}"
+    return err

@@ -23,7 +23,7 @@ def test_header_declarations_are_all_exported(lib):
     assert declared == set(eta.EXPORTS), declared ^ set(eta.EXPORTS)
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.eta_abi_version() == 3
+    assert lib.eta_abi_version() == 4
 
 
 def good_desc(**kw):
@@ -92,8 +92,8 @@ def decode_call(lib, desc=None, q=FAKE, tau=FAKE, out=FAKE, mask=FAKE, ws=FAKE, 
     summ = summ or eta.SummaryDesc(mu=FAKE, sigma=FAKE, max_norm=FAKE, n_blk_cap=64)
     params = params or eta.decode_params()
     return lib.eta_decode(ctypes.byref(desc), eta.ETA_DT_BF16, q, FAKE, FAKE, FAKE,
-                          ctypes.byref(summ), tau, ctypes.byref(params), out, mask, None, ws,
-                          ws_bytes, None)
+                          ctypes.byref(summ), tau, ctypes.byref(params), out, mask, None, None,
+                          ws, ws_bytes, None)
 
 
 def test_decode_rejects_null_and_misaligned(lib):

@@ -95,5 +95,6 @@ def test_decode_on_f16_records_matches_oracle(name):
     mu16, sg16 = oracle.round_f16(mu), oracle.round_f16(sg)
     orc, tau_o = run_oracle(wl, np_in, summaries=(mu16, sg16, mx))
     extra = f16_band(wl, np_in[0], mu16, sg16, f16_record_ranges(wl, np_in[1], mu, sg))
-    stats = compare(wl, g, orc, tau_o, np_inputs=np_in, band_extra=extra)
+    stats = compare(wl, g, orc, tau_o, np_inputs=np_in, band_extra=extra,
+                    union_counts=g.union_counts)
     say(f"[gpu] fp16 index {name}: {stats}, median band {float(np.median(extra)):.2e}")

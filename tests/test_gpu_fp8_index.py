@@ -212,7 +212,8 @@ def test_decode_on_fp8_records_matches_oracle(name):
     orc, tau_o = run_oracle(wl, np_in, summaries=(mu8, sg8, mx))
     extra = f16_band(wl, np_in[0], mu8, sg8,
                      f16_record_ranges(wl, np_in[1], mu, sg, rnd=oracle.round_e4m3))
-    stats = compare(wl, g, orc, tau_o, np_inputs=np_in, band_extra=extra)
+    stats = compare(wl, g, orc, tau_o, np_inputs=np_in, band_extra=extra,
+                    union_counts=g.union_counts)
     say(f"[gpu] FP8 index {name}: {stats}, median band {float(np.median(extra)):.2e}, "
         f"max band {float(np.max(extra)):.2e}")
 

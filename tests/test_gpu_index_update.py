@@ -171,6 +171,6 @@ def test_decode_on_envelope_summaries_matches_oracle(sub, lwb):
     g = run_gpu(wl, sub_block=sub)
     summ = oracle_summaries(wl, np_in[1], sub_block=sub)
     orc, tau_o = run_oracle(wl, np_in, summaries=summ)
-    stats = compare(wl, g, orc, tau_o, np_inputs=np_in)
+    stats = compare(wl, g, orc, tau_o, np_inputs=np_in, union_counts=g.union_counts)
     frac = float(g.mask.float().mean())
     say(f"[gpu] envelope sub {sub} lwb {lwb}: {stats}, mask density {frac:.3f}")
