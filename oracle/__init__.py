@@ -46,6 +46,7 @@ class _Problem(ctypes.Structure):
         ("n_threads", ctypes.c_int32),
         ("o", _vp), ("sel", _vp), ("bounds", _vp), ("counts", _vp), ("lse", _vp),
         ("rescued", _vp),
+        ("blockmax", _vp), ("quality", _vp), ("missed", _vp),
     ]
 
 
@@ -104,6 +105,11 @@ def _load():
                                       ctypes.c_int64, ctypes.c_int, ctypes.c_int, _vp,
                                       ctypes.c_int, ctypes.c_double, ctypes.c_double,
                                       ctypes.c_int, ctypes.c_int, _vp, _vp, _vp]
+    lib.eta_oracle_screen_quality.restype = None
+    lib.eta_oracle_screen_quality.argtypes = [_vp, _vp, ctypes.c_int, ctypes.c_int64, ctypes.c_int64,
+                                              ctypes.c_int, ctypes.c_int, _vp, ctypes.c_double,
+                                              ctypes.c_double, ctypes.c_int, ctypes.c_int, _vp,
+                                              _vp, _vp]
     lib.eta_oracle_decode.restype = ctypes.c_int
     lib.eta_oracle_decode.argtypes = [ctypes.POINTER(_Problem)]
     _lib = lib
@@ -224,6 +230,53 @@ def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, b: int, sel: np.ndarray,
     return o, lse.value, cnt.value
 
 
+QUALITY_FIELDS = ("positive_blocks", "false_negative_blocks", "false_positive_blocks",
+                  "selected_blocks", "above_keys", "above_keys_attended")
+
+
+def screen_quality(q: np.ndarray, k: np.ndarray, b: int, sel: np.ndarray, *, tau_eff: float,
+                   beta: float = 4.0, self_ungated: bool = False, gate_off: bool = False) -> dict:
+    """Screening-quality diagnostics of one head over keys ``k[T][d]`` and a block
+    selection ``sel[N]`` (Tab. "index_quality"): brute-force block maxima, positive /
+    false-negative / false-positive / selected blocks, above-threshold keys of the full
+    blocks and how many are attended, and the missed gated softmax mass of the
+    rejected blocks (see eta_oracle_screen_quality)."""
+    q = _c(q, np.float64); k = _c(k)
+    T, d = k.shape
+    N = T // b
+    s = np.zeros(max(N, 1), np.uint8)
+    s[:N] = np.asarray(sel, np.uint8).reshape(-1)[:N]
+    bm = np.full(max(N, 1), np.nan)
+    qual = np.zeros(6, np.int64)
+    missed = ctypes.c_double()
+    _load().eta_oracle_screen_quality(_ptr(q), _ptr(k), _dtype_code(k), d, T, d, b, _ptr(s),
+                                      float(tau_eff), float(beta), int(self_ungated),
+                                      int(gate_off), _ptr(bm), _ptr(qual), ctypes.byref(missed))
+    out = dict(zip(QUALITY_FIELDS, (int(x) for x in qual)))
+    out["blockmax"] = bm[:N]
+    out["missed_mass"] = missed.value
+    return out
+
+
+def quality_rates(res: "DecodeResult", rows: Optional[Sequence[int]] = None) -> dict:
+    """Pooled screening-quality rates of a decode run with ``quality=True``:
+    block false-negative rate (false negatives / positive blocks), false-positive
+    rate (selected blocks that are not positive / selected blocks), token recall
+    (attended above-threshold keys / above-threshold keys) and the missed gated
+    mass (mean over rows and largest row)."""
+    B, Hq = res.missed.shape
+    rows = list(range(B * Hq)) if rows is None else list(rows)
+    qs = np.array([res.quality[r // Hq, r % Hq] for r in rows], np.int64).reshape(-1, 6)
+    mm = np.array([res.missed[r // Hq, r % Hq] for r in rows])
+    tot = qs.sum(axis=0)
+    ratio = lambda a, b: float(a) / float(b) if b else None
+    return {"rows": len(rows), "positive_blocks": int(tot[0]),
+            "false_negative_rate": ratio(tot[1], tot[0]), "false_positive_rate": ratio(tot[2], tot[3]),
+            "token_recall": ratio(tot[5], tot[4]), "missed_mass_mean": float(mm.mean()) if mm.size else None,
+            "missed_mass_max": float(mm.max()) if mm.size else None,
+            "rows_with_false_negatives": int(np.count_nonzero(qs[:, 1]))}
+
+
 # ------------------------------------------------------------------ batched
 
 @dataclass
@@ -234,6 +287,9 @@ class DecodeResult:
     counts: np.ndarray     # [B][Hq] int64
     lse: np.ndarray        # [B][Hq] float64
     rescued: np.ndarray    # [B][Hq] int64 (-1: no rescue)
+    blockmax: Optional[np.ndarray] = None   # [B][Hq][N_cap] (quality=True; NaN beyond N_b)
+    quality: Optional[np.ndarray] = None    # [B][Hq][6] QUALITY_FIELDS (quality=True)
+    missed: Optional[np.ndarray] = None     # [B][Hq] missed gated mass (quality=True)
 
 
 def block_index(k: np.ndarray, seq_lens: Sequence[int], block_size: int, n_threads: int = 0):
@@ -269,7 +325,7 @@ def decode(q: np.ndarray, k: np.ndarray, v: np.ndarray, seq_lens: Sequence[int],
            rescue_window: int = 128, lwb: int = 0, self_ungated: bool = False,
            screen_all: bool = False, gate_off: bool = False, bounds_only: bool = False,
            rows: Optional[Sequence[int]] = None, sel_in: Optional[np.ndarray] = None,
-           summaries=None, n_threads: int = 0) -> DecodeResult:
+           summaries=None, n_threads: int = 0, quality: bool = False) -> DecodeResult:
     """One ETA decode step for every (sequence, query head), or for ``rows``.
 
     q [B][Hq][d]; k, v [B][Hkv][T_cap][d]; seq_lens [B]; tau [B][Hq].
@@ -277,6 +333,8 @@ def decode(q: np.ndarray, k: np.ndarray, v: np.ndarray, seq_lens: Sequence[int],
     blocks plus the tail (Alg. "Hardware-Aligned Block-Sparse Decoding").
     Rows not requested are left zero.  ``bounds_only`` stops after the bounds.
     ``summaries`` = (mu, sigma, M) from ``block_index`` skips recomputing them.
+    ``quality`` also gives the screening-quality diagnostics of every requested row
+    (``screen_quality``) in ``blockmax``, ``quality`` and ``missed``.
     """
     q = _c(q); k = _c(k); v = _c(v)
     B, Hq, d = q.shape
@@ -298,6 +356,10 @@ def decode(q: np.ndarray, k: np.ndarray, v: np.ndarray, seq_lens: Sequence[int],
         lse=np.full((B, Hq), -np.inf),
         rescued=np.full((B, Hq), -1, np.int64),
     )
+    if quality:
+        res.blockmax = np.full((B, Hq, max(Ncap, 1)), np.nan)
+        res.quality = np.zeros((B, Hq, 6), np.int64)
+        res.missed = np.zeros((B, Hq))
     smu = ssg = smx = None
     if summaries is not None:
         smu = np.ascontiguousarray(summaries[0], np.float64)
@@ -318,12 +380,15 @@ def decode(q: np.ndarray, k: np.ndarray, v: np.ndarray, seq_lens: Sequence[int],
         n_threads=int(n_threads),
         o=_ptr(res.o), sel=_ptr(res.sel), bounds=_ptr(res.bounds), counts=_ptr(res.counts),
         lse=_ptr(res.lse), rescued=_ptr(res.rescued),
+        blockmax=_ptr(res.blockmax), quality=_ptr(res.quality), missed=_ptr(res.missed),
     )
     rc = _load().eta_oracle_decode(ctypes.byref(P))
     if rc != 0:
         raise ValueError(f"eta_oracle_decode rejected the problem (code {rc})")
     res.sel = res.sel[:, :, :Ncap]
     res.bounds = res.bounds[:, :, :Ncap]
+    if quality:
+        res.blockmax = res.blockmax[:, :, :Ncap]
     return res
 
 

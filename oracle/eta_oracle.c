@@ -314,6 +314,71 @@ void eta_oracle_attend(const double* q, const void* k, const void* v, int dt, in
   free(in);
 }
 
+/*
+ * Screening-quality diagnostics of one head (Tab. "index_quality" in App. "GQA
+ * Union Loading and Variance Dilution at Coarse Block Sizes"; the block false
+ * negatives and recall of above-threshold keys discussed in Sec. "Block
+ * Granularity and GQA Union Loading").  From the brute-force scores
+ * S_t = <q, k_t> / sqrt(d) of every key:
+ *   blockmax[j]  max over block j's keys of S_t (full blocks j < N)
+ *   qual[0]  positive blocks:  blockmax[j] >= tau_eff
+ *   qual[1]  false negatives:  positive and not selected
+ *   qual[2]  false positives:  selected and not positive
+ *   qual[3]  selected blocks
+ *   qual[4]  above-threshold keys of the full blocks: S_t >= tau_eff
+ *   qual[5]  those among them that are attended (their block is selected)
+ *   missed  the softmax mass of the rejected full blocks under gated attention
+ *           over every key (the no-screening distribution of Sec. "Elastic
+ *           Threshold Attention": sum over rejected keys of exp(S~_t) / sum over
+ *           all T keys), S~ gated with tau_eff as in eta_oracle_attend
+ * The tail [N b, T) is never screened, so it enters only the denominator of the
+ * missed mass.  blockmax may be NULL.
+ */
+void eta_oracle_screen_quality(const double* q, const void* k, int dt, int64_t row_stride,
+                               int64_t T, int d, int b, const uint8_t* sel, double tau_eff,
+                               double beta, int self_ungated, int gate_off, double* blockmax,
+                               int64_t* qual, double* missed) {
+  int64_t N = T / b;
+  double scale = 1.0 / sqrt((double)d);
+  for (int f = 0; f < 6; ++f) qual[f] = 0;
+  *missed = 0.0;
+  if (T <= 0) return;
+  double* sg = (double*)malloc(sizeof(double) * (size_t)T);
+  double m = -INFINITY;
+  for (int64_t j = 0; j <= N; ++j) {
+    int64_t t0 = j * b, t1 = j < N ? t0 + b : T;
+    double bmax = -INFINITY;
+    int64_t above = 0;
+    for (int64_t t = t0; t < t1; ++t) {
+      double S = 0.0;
+      for (int i = 0; i < d; ++i) S += q[i] * ld(k, dt, t * row_stride + i);
+      S *= scale;
+      if (S > bmax) bmax = S;
+      if (S >= tau_eff) ++above;
+      double Sg = (gate_off || (self_ungated && t == T - 1)) ? S : eta_oracle_gate(S, tau_eff, beta);
+      sg[t] = Sg;
+      if (Sg > m) m = Sg;
+    }
+    if (j == N) break;
+    int positive = bmax >= tau_eff;
+    if (blockmax) blockmax[j] = bmax;
+    qual[0] += positive;
+    qual[1] += positive && !sel[j];
+    qual[2] += !positive && sel[j];
+    qual[3] += sel[j] != 0;
+    qual[4] += above;
+    qual[5] += sel[j] ? above : 0;
+  }
+  double Z = 0.0, Zrej = 0.0;
+  for (int64_t t = 0; t < T; ++t) {
+    double w = exp(sg[t] - m);
+    Z += w;
+    if (t < N * b && !sel[t / b]) Zrej += w;
+  }
+  *missed = Z > 0.0 ? Zrej / Z : 0.0;
+  free(sg);
+}
+
 /* ---------------------------------------------------------------- batched */
 
 typedef struct {
@@ -349,6 +414,10 @@ typedef struct {
   int64_t* counts;             /* [B][Hq] attended tokens */
   double* lse;                 /* [B][Hq] */
   int64_t* rescued;            /* [B][Hq] rescued block or -1 */
+  /* optional screening-quality diagnostics (eta_oracle_screen_quality); NULL: skipped */
+  double* blockmax;            /* [B][Hq][N_cap] brute-force block maxima (NaN beyond N_b) */
+  int64_t* quality;            /* [B][Hq][6] */
+  double* missed;              /* [B][Hq] */
 } eta_oracle_problem;
 
 static const void* off(const void* p, int dt, int64_t elems) {
@@ -434,6 +503,14 @@ int eta_oracle_decode(const eta_oracle_problem* P) {
     if (P->sel) memcpy(P->sel + (int64_t)row * Ncap, sel, (size_t)Ncap);
     if (P->counts) P->counts[row] = cnt;
     if (P->lse) P->lse[row] = lse;
+    if (P->quality) {
+      double* bm = P->blockmax ? P->blockmax + (int64_t)row * Ncap : NULL;
+      if (bm)
+        for (int64_t j = 0; j < Ncap; ++j) bm[j] = NAN;
+      eta_oracle_screen_quality(qh, off(P->k, P->kv_dtype, kvoff), P->kv_dtype, d, T, d, P->b, sel,
+                                tau_eff, P->beta, P->self_ungated, P->gate_off, bm,
+                                P->quality + (int64_t)row * 6, P->missed + row);
+    }
     if (P->rescued) P->rescued[row] = resc;
     free(sel);
     free(qh);

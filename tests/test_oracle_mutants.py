@@ -56,6 +56,14 @@ MUTANTS = {
     "prefill_r_without_diagonal": ("    rsum += g;", "    if (j < i) rsum += g;"),
     "prefill_additive_sign": ("double Sg = additive ? S + C * g - C : S * g;", "double Sg = additive ? S - C * g + C : S * g;"),
     "prefill_lse_without_max": ("  *L_out = m + log(l);", "  *L_out = log(l);"),
+    "quality_strict_positive": ("int positive = bmax >= tau_eff;", "int positive = bmax > tau_eff;"),
+    "quality_missed_over_selected": ("if (t < N * b && !sel[t / b]) Zrej += w;",
+                                     "if (t < N * b && sel[t / b]) Zrej += w;"),
+    "quality_recall_counts_tail": ("    if (j == N) break;\n    int positive",
+                                   "    if (j == N) { qual[4] += above; break; }\n    int positive"),
+    "quality_blockmax_skips_last_key": ("      if (S > bmax) bmax = S;", "      if (S > bmax && t + 1 < t1) bmax = S;"),
+    "quality_missed_without_tail": ("    double w = exp(sg[t] - m);\n    Z += w;",
+                                    "    double w = exp(sg[t] - m);\n    if (t < N * b) Z += w;"),
     "calib_bisect_direction": ("if (eta_oracle_calib_g(hist, nb, lo, hi, beta, m) > target) a = m; else b = m;", "if (eta_oracle_calib_g(hist, nb, lo, hi, beta, m) < target) a = m; else b = m;"),
 }
 

@@ -644,3 +644,118 @@ def test_prefill_rows_are_the_full_rows():
         for n, (b, h, i) in enumerate(rows):
             np.testing.assert_array_equal(r.o[n], full.o[b, h, i])
             assert r.r[n] == full.r[b, h, i] and r.lse[n] == full.lse[b, h, i]
+
+
+# --------------------------------------------------------------------- screening quality
+#
+# The diagnostics of Tab. "index_quality": block false negatives / positives,
+# recall of above-threshold keys and the missed gated softmax mass.
+
+def _quality_keys():
+    """d = 4, b = 2 (scale 1/2 exact), q = (2, 0, 0, 0): each key's score is its first
+    coordinate exactly.  Block 0 = keys -1, 3 (maximum at its last key), block 1 =
+    keys 1, 0.2 (maximum exactly at tau = 1), tail = one key of score 1."""
+    k = np.zeros((5, 4), np.float32)
+    k[:, 0] = [-1.0, 3.0, 1.0, 0.2, 1.0]
+    return np.array([2.0, 0.0, 0.0, 0.0]), k
+
+
+def test_screen_quality_hand_worked_example():
+    q, k = _quality_keys()
+    S = [-1.0, 3.0, 1.0, float(np.float32(0.2)), 1.0]
+    g = [oracle.gate(s, 1.0, 4.0) for s in S]           # the gate is pinned above
+    m = max(g)
+    w = [math.exp(x - m) for x in g]
+    Z = sum(w)
+    # block 0 selected: block 1 (maximum 1 >= tau) is a false negative; of the two
+    # above-threshold keys of the full blocks (3 and 1; the tail's is not screened)
+    # one is attended; the missed mass is block 1's share of all five keys
+    r = oracle.screen_quality(q, k, 2, [1, 0], tau_eff=1.0, beta=4.0)
+    assert (r["positive_blocks"], r["false_negative_blocks"], r["false_positive_blocks"],
+            r["selected_blocks"], r["above_keys"], r["above_keys_attended"]) == (2, 1, 0, 1, 2, 1)
+    np.testing.assert_array_equal(r["blockmax"], [3.0, 1.0])
+    assert r["missed_mass"] == pytest.approx((w[2] + w[3]) / Z, rel=1e-14)
+    # block 1 selected instead: block 0 is the false negative
+    r = oracle.screen_quality(q, k, 2, [0, 1], tau_eff=1.0, beta=4.0)
+    assert (r["false_negative_blocks"], r["above_keys_attended"]) == (1, 1)
+    assert r["missed_mass"] == pytest.approx((w[0] + w[1]) / Z, rel=1e-14)
+    # nothing selected: both blocks missed, only the tail's mass kept
+    r = oracle.screen_quality(q, k, 2, [0, 0], tau_eff=1.0, beta=4.0)
+    assert (r["false_negative_blocks"], r["above_keys_attended"]) == (2, 0)
+    assert r["missed_mass"] == pytest.approx(1.0 - w[4] / Z, rel=1e-14)
+    # threshold above every score: no positive block, a selected block is a false positive
+    r = oracle.screen_quality(q, k, 2, [1, 1], tau_eff=3.5, beta=4.0)
+    assert (r["positive_blocks"], r["false_positive_blocks"], r["above_keys"]) == (0, 2, 0)
+    assert r["missed_mass"] == 0.0
+
+
+def _quality_workload(seed=3):
+    return make_workload(B=2, Hq=4, Hkv=2, d=32, block=16, seq_lens=[1000, 611], dtype=torch.float32,
+                         planted={"frac": 0.1}, predictor=False, tau_const=1.2, seed=seed)
+
+
+def test_blockmax_is_brute_force_maximum():
+    wl = _quality_workload()
+    q, k, v = (as_numpy(t) for t in (wl.q, wl.k, wl.v))
+    tau = np.full((2, 4), 1.2)
+    r = oracle.decode(q, k, v, wl.seq_lens, tau, block_size=16, z=1.0, quality=True)
+    for b in range(2):
+        N = wl.seq_lens[b] // 16
+        for h in range(4):
+            S = (k[b, h // 2, :N * 16].astype(np.float64) @ q[b, h].astype(np.float64)) / math.sqrt(32)
+            np.testing.assert_allclose(r.blockmax[b, h, :N], S.reshape(N, 16).max(axis=1), rtol=1e-13)
+            above = S >= 1.2
+            sel = np.repeat(r.sel[b, h, :N].astype(bool), 16)
+            assert r.quality[b, h, 4] == above.sum() and r.quality[b, h, 5] == (above & sel).sum()
+
+
+def test_missed_mass_is_the_log_sum_exp_gap():
+    """The attended set and the rejected blocks partition the keys, so the rejected
+    share of the dense gated mass is 1 - exp(lse_attended - lse_all) (the convex
+    decomposition of the output over a partition)."""
+    wl = _quality_workload(seed=5)
+    q, k, v = (as_numpy(t) for t in (wl.q, wl.k, wl.v))
+    tau = np.array([[1.0, 1.5, 2.0, 0.5], [1.2, 0.8, 2.5, 1.7]])
+    r = oracle.decode(q, k, v, wl.seq_lens, tau, block_size=16, z=1.0, quality=True)
+    full = oracle.decode(q, k, v, wl.seq_lens, tau, block_size=16, z=1.0, screen_all=True)
+    gap = 1.0 - np.exp(r.lse - full.lse)
+    np.testing.assert_allclose(r.missed, gap, rtol=1e-9, atol=1e-14)
+    assert np.all(r.missed > 0.0)
+
+
+@pytest.mark.parametrize("b,d", [(16, 32), (64, 64)])
+def test_no_false_negatives_at_the_certified_z(b, d):
+    """At z = sqrt((b - 1) d) the dual bound is at least every block's maximum score
+    (Samuelson + Cauchy-Schwarz), so every positive block is selected."""
+    wl = make_workload(B=1, Hq=4, Hkv=1, d=d, block=b, seq_lens=[b * 40], dtype=torch.float32,
+                       planted={"frac": 0.1}, predictor=False, tau_const=0.0, seed=b + d)
+    q, k, v = (as_numpy(t) for t in (wl.q, wl.k, wl.v))
+    r0 = oracle.decode(q, k, v, wl.seq_lens, np.zeros((1, 4)), block_size=b, z=1.0, quality=True,
+                       rescue_window=0)
+    tau = np.median(r0.blockmax[0], axis=1)[None, :]      # about half the blocks positive
+    zc = math.sqrt((b - 1) * d)
+    r = oracle.decode(q, k, v, wl.seq_lens, tau, block_size=b, z=zc, quality=True, rescue_window=0)
+    assert np.all(r.quality[0, :, 0] > 0)
+    assert np.all(r.quality[0, :, 1] == 0) and np.all(r.quality[0, :, 4] == r.quality[0, :, 5])
+    # not vacuous: without the z term the same blocks are missed
+    r = oracle.decode(q, k, v, wl.seq_lens, tau, block_size=b, z=0.0, quality=True, rescue_window=0)
+    assert r.quality[0, :, 1].sum() > 0
+
+
+def test_quality_of_screen_all_and_open_threshold():
+    wl = _quality_workload(seed=7)
+    q, k, v = (as_numpy(t) for t in (wl.q, wl.k, wl.v))
+    tau = np.full((2, 4), 1.2)
+    r = oracle.decode(q, k, v, wl.seq_lens, tau, block_size=16, z=1.0, quality=True, screen_all=True)
+    rates = oracle.quality_rates(r)
+    assert rates["false_negative_rate"] == 0.0 and rates["token_recall"] == 1.0
+    assert rates["missed_mass_max"] == 0.0
+    for b in range(2):
+        N = wl.seq_lens[b] // 16
+        assert np.all(r.quality[b, :, 2] == N - r.quality[b, :, 0])
+    r = oracle.decode(q, k, v, wl.seq_lens, np.full((2, 4), -np.inf), block_size=16, z=1.0,
+                      quality=True)
+    for b in range(2):
+        N = wl.seq_lens[b] // 16
+        assert np.all(r.quality[b, :, 0] == N) and np.all(r.quality[b, :, 1] == 0)
+    assert np.all(r.missed == 0.0)
