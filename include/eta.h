@@ -261,6 +261,38 @@ eta_status_t eta_decode_predicted(const eta_kv_desc_t* kv, int32_t q_dtype, cons
                                   void* stream);
 
 /*
+ * eta_decode_predicted_noalloc -- eta_decode_predicted for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same kernels and results, with the
+ * workspace taken from a scratch array the library holds on each GPU instead of
+ * a caller's buffer.  The call allocates nothing (no hipMalloc, hipFree or
+ * allocating library routine); the caller still passes inputs and outputs.
+ *   scratch      ETA_DECODE_NOALLOC_SCRATCH_BYTES (32 MiB) per GPU, a device array
+ *                in the library, held by each GPU the library runs on until the
+ *                process ends; its device address is looked up on the first call
+ *                on a device (with that device current)
+ *   size limit   a call whose eta_decode_workspace_size() exceeds that size is
+ *                rejected with ETA_ERR_WORKSPACE before anything is enqueued (e.g.
+ *                32 ragged 64K sequences at 32/8 heads need ~9.6 MB; 8 x 128K at
+ *                16/4 heads ~4.5 MB)
+ *   contents     no scratch entry needs to start at zero: every value a kernel reads
+ *                was written earlier in the same call
+ *   concurrency  every call on a GPU shares that GPU's scratch: calls that can
+ *                overlap (other streams, other host threads) race and give wrong
+ *                results; order them on one stream
+ * Every other argument and every result are as for eta_decode_predicted
+ * (bit-identical to it at the same arguments).
+ */
+#define ETA_DECODE_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+eta_status_t eta_decode_predicted_noalloc(const eta_kv_desc_t* kv, int32_t q_dtype,
+                                          const void* q, const void* k, const void* v,
+                                          const int32_t* seq_lens, const eta_summary_t* summ,
+                                          const float* W, const float* bias,
+                                          const eta_decode_params_t* p, void* out,
+                                          uint8_t* block_mask, int32_t* head_token_counts,
+                                          int32_t* union_counts, float* tau_out, void* stream);
+
+/*
  * Offline density-matched calibration of static per-head thresholds (App.
  * "Offline Threshold Calibration via 1/t-Weighted Histograms"; Alg.
  * "Density-Matched Offline Threshold Calibration"): the frozen constants that

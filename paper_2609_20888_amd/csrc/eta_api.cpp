@@ -242,6 +242,9 @@ size_t dense_ws_bytes(const Geom& g, int S, DecodeWs* c, void* base) {
 
 using namespace eta;
 
+static_assert(kScratchBytes == ETA_DECODE_NOALLOC_SCRATCH_BYTES,
+              "the header states the library scratch size");
+
 extern "C" {
 
 const char* eta_last_error_string(void) { return g_err.c_str(); }
@@ -325,7 +328,8 @@ static eta_status_t decode_impl(const eta_kv_desc_t* kv, int32_t q_dtype, const 
                                 const float* bias, float* tau_out,
                                 const eta_decode_params_t* p, void* out, uint8_t* block_mask,
                                 int32_t* head_token_counts, int32_t* union_counts,
-                                void* workspace, size_t workspace_bytes, void* stream) {
+                                void* workspace, size_t workspace_bytes, void* stream,
+                                bool library_scratch = false) {
   Geom g;
   eta_status_t st = check_kv(kv, &g);
   if (st) return st;
@@ -342,6 +346,18 @@ static eta_status_t decode_impl(const eta_kv_desc_t* kv, int32_t q_dtype, const 
   // the mask and the workspace are laid out with the summary capacity
   if ((st = check_summary(summ, &g))) return st;
   const int S = p->num_splits > 0 ? p->num_splits : default_splits(g);
+  if (library_scratch) {
+    // every check above is on the host; the scratch is looked up only for a valid call
+    const size_t need = decode_ws_bytes(g, S, nullptr, nullptr);
+    if (need > kScratchBytes)
+      return fail(ETA_ERR_WORKSPACE,
+                  "this call needs %zu bytes of scratch; the library's scratch holds %zu "
+                  "(use eta_decode_predicted with a workspace)", need, kScratchBytes);
+    hipError_t e = scratch_address((hipStream_t)stream, &workspace);
+    if (e != hipSuccess)
+      return fail(ETA_ERR_HIP, "library scratch lookup failed: %s", hipGetErrorString(e));
+    workspace_bytes = kScratchBytes;
+  }
   if (!workspace) return fail(ETA_ERR_WORKSPACE, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(workspace) & 255u)
     return fail(ETA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
@@ -380,6 +396,18 @@ eta_status_t eta_decode_predicted(const eta_kv_desc_t* kv, int32_t q_dtype, cons
   return decode_impl(kv, q_dtype, q, k, v, seq_lens, summ, nullptr, W, bias, tau_out, p, out,
                      block_mask, head_token_counts, union_counts, workspace, workspace_bytes,
                      stream);
+}
+
+eta_status_t eta_decode_predicted_noalloc(const eta_kv_desc_t* kv, int32_t q_dtype,
+                                          const void* q, const void* k, const void* v,
+                                          const int32_t* seq_lens, const eta_summary_t* summ,
+                                          const float* W, const float* bias,
+                                          const eta_decode_params_t* p, void* out,
+                                          uint8_t* block_mask, int32_t* head_token_counts,
+                                          int32_t* union_counts, float* tau_out, void* stream) {
+  if (!bias) return fail(ETA_ERR_INVALID_ARG, "bias must be non-NULL");
+  return decode_impl(kv, q_dtype, q, k, v, seq_lens, summ, nullptr, W, bias, tau_out, p, out,
+                     block_mask, head_token_counts, union_counts, nullptr, 0, stream, true);
 }
 
 static eta_status_t check_calib(const eta_calib_desc_t* cd, const eta_calib_state_t* st) {

@@ -88,6 +88,11 @@ hipError_t launch_prefill(const eta_prefill_desc_t& pd, const void* q, const voi
                           const float* tau, const int32_t* seq_lens, void* out, float* R, float* L,
                           hipStream_t stream, LaunchHook hook);
 
+// The library's own device scratch (eta_decode_predicted_noalloc): kScratchBytes
+// per GPU; scratch_address gives the address of the copy on the stream's device.
+constexpr size_t kScratchBytes = size_t(32) << 20;
+hipError_t scratch_address(hipStream_t stream, void** out);
+
 hipError_t launch_dense(const Geom& g, int S, int q_dtype, const void* q, const void* k,
                         const void* v, const int32_t* seq_lens, void* out, const DecodeWs& ws,
                         hipStream_t stream, LaunchHook hook);

@@ -25,6 +25,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "eta_device.h"
@@ -1876,6 +1877,43 @@ hipError_t launch_dense(const Geom& g, int S, int q_dtype, const void* q, const 
                  q_dtype, S};
   return with_hook(hook, ETA_KERNEL_DENSE_COMBINE, stream,
                    [&] { launch_combine_impl(g, ca, stream); });
+}
+
+// ---------------------------------------------------------------- library scratch
+//
+// Workspace of eta_decode_predicted_noalloc: a file-scope device array (each GPU
+// the library runs on holds its own copy, at its own address, until the
+// process ends).  Host code never uses the array's name as an address: the
+// device address of each GPU's copy is looked up once, with that GPU current,
+// and kept.
+
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+hipError_t scratch_address(hipStream_t stream, void** out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  hipDevice_t dev = 0;
+  hipError_t e = hipStreamGetDevice(stream, &dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(mu);
+  if (addr[dev] == nullptr) {
+    int cur = 0;
+    if ((e = hipGetDevice(&cur)) != hipSuccess) return e;
+    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) {
+      const hipError_t e2 = hipSetDevice(cur);
+      if (e == hipSuccess) e = e2;
+    }
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return hipSuccess;
 }
 
 }  // namespace eta

@@ -71,7 +71,7 @@ class KernelTime(ctypes.Structure):
 # Symbols include/eta.h declares (the CPU test checks the library exports each).
 EXPORTS = ("eta_build_block_summaries", "eta_build_block_summaries_envelope",
            "eta_update_block_summaries", "eta_predict_threshold", "eta_decode_workspace_size",
-           "eta_decode", "eta_decode_predicted", "eta_block_bounds", "eta_dense_workspace_size", "eta_dense_decode",
+           "eta_decode", "eta_decode_predicted", "eta_decode_predicted_noalloc", "eta_block_bounds", "eta_dense_workspace_size", "eta_dense_decode",
            "eta_calib_accumulate", "eta_calib_solve", "eta_gated_prefill",
            "eta_last_error_string", "eta_abi_version", "eta_profile_begin", "eta_profile_end")
 
@@ -111,6 +111,8 @@ def load_library(path: Optional[str] = None):
                        _vp, _vp, _vp, _vp, _vp, sz, _vp],
         "eta_decode_predicted": [P(KvDesc), i32, _vp, _vp, _vp, _vp, P(SummaryDesc), _vp, _vp,
                                  P(DecodeParams), _vp, _vp, _vp, _vp, _vp, _vp, sz, _vp],
+        "eta_decode_predicted_noalloc": [P(KvDesc), i32, _vp, _vp, _vp, _vp, P(SummaryDesc), _vp,
+                                         _vp, P(DecodeParams), _vp, _vp, _vp, _vp, _vp, _vp],
         "eta_block_bounds": [P(KvDesc), i32, _vp, _vp, P(SummaryDesc), f32, _vp, _vp],
         "eta_dense_workspace_size": [P(KvDesc), i32, P(sz)],
         "eta_dense_decode": [P(KvDesc), i32, _vp, _vp, _vp, _vp, _vp, i32, _vp, sz, _vp],
@@ -333,6 +335,31 @@ def decode_predicted(q, k, v, seq_lens, summ: Summaries, W, bias, *, block_size:
         ctypes.byref(sd), _ptr(W), _ptr(bias), ctypes.byref(p), _ptr(out), _ptr(mask),
         _ptr(counts), _ptr(union_counts), _ptr(tau_out), _ptr(workspace), workspace.numel(),
         _stream(stream)))
+    return DecodeOut(out=out, mask=mask, counts=counts, union_counts=union_counts)
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20   # ETA_DECODE_NOALLOC_SCRATCH_BYTES
+
+
+def decode_predicted_noalloc(q, k, v, seq_lens, summ: Summaries, W, bias, *, block_size: int,
+                             params: Optional[DecodeParams] = None, out=None, mask=None,
+                             counts=None, union_counts=None, tau_out=None,
+                             want_counts: bool = True, stream=None) -> DecodeOut:
+    """eta_decode_predicted_noalloc: eta_decode_predicted with the library's own scratch
+    as the workspace (the C call allocates nothing; output buffers not given are
+    allocated here, before the call)."""
+    B, Hq, d = q.shape
+    p = params if params is not None else decode_params()
+    desc = kv_desc(k, Hq, block_size)
+    if v.shape != k.shape or v.stride() != k.stride() or v.dtype != k.dtype:
+        raise ValueError("K and V must share shape, strides and dtype")
+    out, mask, counts, union_counts = _decode_outputs(q, k, summ, out, mask, counts, union_counts,
+                                                      want_counts)
+    sd = summ.desc()
+    _check(load_library().eta_decode_predicted_noalloc(
+        ctypes.byref(desc), _dtype_code(q), _ptr(q), _ptr(k), _ptr(v), _ptr(seq_lens),
+        ctypes.byref(sd), _ptr(W), _ptr(bias), ctypes.byref(p), _ptr(out), _ptr(mask),
+        _ptr(counts), _ptr(union_counts), _ptr(tau_out), _stream(stream)))
     return DecodeOut(out=out, mask=mask, counts=counts, union_counts=union_counts)
 
 
