@@ -121,7 +121,10 @@ typedef struct {
   int32_t pin_recent_blocks;    /* lwb: the last lwb full blocks are always selected; >= 0 */
   int32_t self_ungated;         /* 1: key seq_len-1 uses S~ = S (Eq. (mult_attn), M_tt = 1) */
   int32_t screen_all;           /* 1: every full block selected (dense gated attention) */
-  int32_t num_splits;           /* splits per (sequence, kv head); 0: library default; <= 1024 */
+  int32_t num_splits;           /* splits per (sequence, kv head), for several sequences their
+                                   average (the splits are dealt to the (sequence, kv head)
+                                   groups in proportion to their unions); 0: library default;
+                                   <= 1024 */
 } eta_decode_params_t;
 
 /*

@@ -197,8 +197,37 @@ int default_splits(const Geom& g) {
   return (int)S;
 }
 
-size_t decode_ws_bytes(const Geom& g, int S, DecodeWs* c, void* base) {
+// Split layout of a decode call.  One sequence (or a tile count table too large
+// for the split kernel's LDS): S splits per kv head, num_splits or the default
+// (one workgroup per compute unit for one sequence).  Several sequences: W =
+// num_splits x B x Hkv workgroups (num_splits 0: see below) dealt to the
+// (sequence, kv head) groups in proportion to their unions, so ragged lengths
+// and unequal unions finish together; num_splits is then the average per group
+// (8 x 128K at 18.6% union: 106 us per step at 512 in all against 143 with 64
+// uniform splits per group; 32 ragged 16K-64K sequences: 849 us at 2048 in all,
+// 1139 at 512).
+constexpr int kPropSplits = 512;
+constexpr int kPropMaxSplits = 4096;
+
+SplitPlan plan_splits(const Geom& g, int num_splits) {
+  const int64_t BG = (int64_t)g.B * g.Hkv;
+  if (g.B > 1 && BG <= kPropMaxGroups && BG * g.n_tiles <= kPropMaxCounts) {
+    // default: at least 8 per group on average (coarser shares leave some groups
+    // with one workgroup for up to twice the average work), at least 512 in all
+    // (2 per compute unit), at most 4096
+    int64_t W = 8 * BG;
+    W = W < kPropSplits ? kPropSplits : (W > kPropMaxSplits ? kPropMaxSplits : W);
+    if (W < BG) W = BG;
+    if (num_splits > 0) W = num_splits * BG;
+    return SplitPlan{0, (int)W};
+  }
+  const int S = num_splits > 0 ? num_splits : default_splits(g);
+  return SplitPlan{S, (int)(S * BG)};
+}
+
+size_t decode_ws_bytes(const Geom& g, const SplitPlan& sp, DecodeWs* c, void* base) {
   const size_t nb = (size_t)g.B * g.Hkv * g.ncap;
+  const size_t BG = (size_t)g.B * g.Hkv, BH = (size_t)g.B * g.Hq;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -206,11 +235,17 @@ size_t decode_ws_bytes(const Geom& g, int S, DecodeWs* c, void* base) {
     return o;
   };
   const size_t o_ids = take(nb * 4);
-  const size_t o_tc = take((size_t)g.B * g.Hkv * g.n_tiles * 4);
-  const size_t o_hc = take((size_t)g.B * g.Hq * g.n_tiles * 4);
-  const size_t o_ml = take((size_t)g.B * g.Hq * S * 8);
-  const size_t o_acc = take((size_t)g.B * g.Hq * S * g.D * 4);
-  const size_t o_tau = take((size_t)g.B * g.Hq * 4);
+  const size_t o_tc = take(BG * g.n_tiles * 4);
+  const size_t o_hc = take(BH * g.n_tiles * 4);
+  const size_t o_ml = take((size_t)sp.W * g.G * 8);
+  const size_t o_acc = take((size_t)sp.W * g.G * g.D * 4);
+  const size_t o_tau = take(BH * 4);
+  const size_t o_rb = take(BH * kRescueTiles * 4);
+  const size_t o_ri = take(BH * kRescueTiles * 4);
+  const size_t o_wb = take(BG * kMaxRescueWindow);
+  const size_t o_ro = take(BH * 4);
+  const size_t o_xu = take(BG * 4);
+  const size_t o_pl = take(BG * 8);
   if (c && base) {
     char* p = static_cast<char*>(base);
     c->tau = reinterpret_cast<float*>(p + o_tau);
@@ -219,6 +254,12 @@ size_t decode_ws_bytes(const Geom& g, int S, DecodeWs* c, void* base) {
     c->head_cnt = reinterpret_cast<int32_t*>(p + o_hc);
     c->part_ml = reinterpret_cast<float2*>(p + o_ml);
     c->part_acc = reinterpret_cast<float*>(p + o_acc);
+    c->resc_best = reinterpret_cast<float*>(p + o_rb);
+    c->resc_info = reinterpret_cast<int32_t*>(p + o_ri);
+    c->wbits = reinterpret_cast<uint8_t*>(p + o_wb);
+    c->resc_out = reinterpret_cast<int32_t*>(p + o_ro);
+    c->extra_union = reinterpret_cast<int32_t*>(p + o_xu);
+    c->plan = reinterpret_cast<int2*>(p + o_pl);
   }
   return off;
 }
@@ -317,8 +358,7 @@ eta_status_t eta_decode_workspace_size(const eta_kv_desc_t* kv, const eta_decode
   if (st) return st;
   if ((st = check_params(p))) return st;
   if (!bytes) return fail(ETA_ERR_INVALID_ARG, "bytes is NULL");
-  const int S = p->num_splits > 0 ? p->num_splits : default_splits(g);
-  *bytes = decode_ws_bytes(g, S, nullptr, nullptr);
+  *bytes = decode_ws_bytes(g, plan_splits(g, p->num_splits), nullptr, nullptr);
   return ok();
 }
 
@@ -345,10 +385,10 @@ static eta_status_t decode_impl(const eta_kv_desc_t* kv, int32_t q_dtype, const 
     return fail(ETA_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
   // the mask and the workspace are laid out with the summary capacity
   if ((st = check_summary(summ, &g))) return st;
-  const int S = p->num_splits > 0 ? p->num_splits : default_splits(g);
+  const SplitPlan plan = plan_splits(g, p->num_splits);
   if (library_scratch) {
     // every check above is on the host; the scratch is looked up only for a valid call
-    const size_t need = decode_ws_bytes(g, S, nullptr, nullptr);
+    const size_t need = decode_ws_bytes(g, plan, nullptr, nullptr);
     if (need > kScratchBytes)
       return fail(ETA_ERR_WORKSPACE,
                   "this call needs %zu bytes of scratch; the library's scratch holds %zu "
@@ -362,11 +402,11 @@ static eta_status_t decode_impl(const eta_kv_desc_t* kv, int32_t q_dtype, const 
   if (reinterpret_cast<uintptr_t>(workspace) & 255u)
     return fail(ETA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
   DecodeWs ws;
-  const size_t need = decode_ws_bytes(g, S, &ws, workspace);
+  const size_t need = decode_ws_bytes(g, plan, &ws, workspace);
   if (workspace_bytes < need)
     return fail(ETA_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
   DecodeCfg c{p->beta, p->z, p->offset_a, p->rescue_window_blocks, p->pin_recent_blocks,
-              p->self_ungated ? 1 : 0, p->screen_all ? 1 : 0, S};
+              p->self_ungated ? 1 : 0, p->screen_all ? 1 : 0, plan};
   hipError_t e = launch_decode(g, c, q_dtype, q, k, v, seq_lens, *summ, tau, W, bias, tau_out,
                                out, block_mask, head_token_counts, union_counts, ws,
                                (hipStream_t)stream, active_hook());

@@ -13,6 +13,9 @@ namespace eta {
 // rescue window (rescue_window_blocks <= kMaxRescueWindow).
 constexpr int kScreenTile = 64;
 constexpr int kMaxRescueWindow = 256;
+constexpr int kRescueTiles = kMaxRescueWindow / kScreenTile;
+constexpr int kRescueAny = -2;     // a block of the tile's window part is selected
+constexpr int kRescueNone = -1;    // no block of the tile's window part has a bound
 constexpr int kMaxSplits = 1024;
 // Upper bound on screening tiles per (sequence, kv head): the split-decode
 // kernel keeps their prefix sum in LDS.
@@ -32,24 +35,42 @@ struct Geom {
 
 // Workspace carve-up of eta_decode.
 struct DecodeWs {
+  float* resc_best;          // [B][Hq][kRescueTiles] top-1 rescue: window part of each tile
+  int32_t* resc_info;        // [B][Hq][kRescueTiles]
+  uint8_t* wbits;            // [B][Hkv][kMaxRescueWindow] union head bits of the window blocks
+  int32_t* resc_out;         // [B][Hq] rescued block per head, or -1
+  int32_t* extra_union;      // [B][Hkv] rescued blocks outside the union
+  int2* plan;                // [B][Hkv] (first split workgroup, splits)
   int32_t* ids;              // [B][Hkv][ncap]   union block ids | head bits << 24, compacted
                              //                  per screening tile (tile t's ids start at
                              //                  t * kScreenTile)
   int32_t* tile_cnt;         // [B][Hkv][n_tiles] union blocks per tile
   int32_t* head_cnt;         // [B][Hq][n_tiles]  selected blocks per head per tile
-  float2* part_ml;           // [B][Hq][S]        (running max, running sum) per split
-  float* part_acc;           // [B][Hq][S][D]     unnormalised output per split
+  float2* part_ml;           // [W][G]            (running max, running sum) per split and head
+  float* part_acc;           // [W][G][D]         unnormalised output per split and head
   float* tau;                // [B][Hq]           thresholds predicted by the screening kernel
 };
 
-size_t decode_ws_bytes(const Geom& g, int S, DecodeWs* carve, void* base);
+// How split decode is laid out: S splits per (sequence, kv head) (uniform), or
+// W workgroups dealt to the groups in proportion to their unions (proportional,
+// several sequences; every split workgroup then reads all B Hkv n_tiles tile
+// counts, which must fit in LDS).
+constexpr int kPropMaxGroups = 1024;
+constexpr int kPropMaxCounts = 4096;
+struct SplitPlan {
+  int S;                     // uniform splits per group (0 when proportional)
+  int W;                     // split workgroups in all
+};
+SplitPlan plan_splits(const Geom& g, int num_splits);
+
+size_t decode_ws_bytes(const Geom& g, const SplitPlan& sp, DecodeWs* carve, void* base);
 size_t dense_ws_bytes(const Geom& g, int S, DecodeWs* carve, void* base);
 int default_splits(const Geom& g);
 
 struct DecodeCfg {
   float beta, z, offset_a;
   int rescue_window, lwb, self_ungated, screen_all;
-  int S;                     // splits per (sequence, kv head)
+  SplitPlan plan;
 };
 
 // Launchers: validated arguments in, one or more kernels enqueued on `stream`.

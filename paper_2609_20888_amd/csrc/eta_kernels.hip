@@ -599,6 +599,9 @@ struct ScreenArgs {
   int32_t* tile_cnt;
   int32_t* head_cnt;
   float* bounds;
+  float* resc_best;          // [B][Hq][kRescueTiles] window part of each tile: largest bound
+  int32_t* resc_info;        //   its block, kRescueNone, or kRescueAny (a window block selected)
+  uint8_t* wbits;            // [B][Hkv][kMaxRescueWindow] union head bits of the window blocks
   Geom g;
   int q_dtype;
   int predict;
@@ -804,42 +807,29 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
 #pragma unroll
     for (int h = 0; h < G; ++h) bits |= (uint32_t)selected(j, bnd[h], h) << h;
 
-    // top-1 rescue over the window [0, min(c, N))
+    if (w != 0) return;
+    // top-1 rescue over the window [0, min(c, N)): this tile's part of it, per
+    // head whether any of its window blocks is selected and the first of its
+    // largest non-NaN bounds, and the union head bits of its window blocks; the
+    // split kernel combines the window's tiles and attends the rescued block
     const int64_t Wn = (int64_t)a.c < N ? (int64_t)a.c : N;
     if (a.c > 0 && (int64_t)tile * kScreenTile < Wn) {
-      bool any[G];
-      float best[G];
-      int64_t arg[G];
+      const bool inw = j < Wn;
 #pragma unroll
-      for (int h = 0; h < G; ++h) { any[h] = false; best[h] = kNegInf; arg[h] = -1; }
-      for (int64_t jb = 0; jb < Wn; jb += kScreenTile) {
-        float wb[G];
-        if (jb == (int64_t)tile * kScreenTile) {
-#pragma unroll
-          for (int h = 0; h < G; ++h) wb[h] = bnd[h];
-        } else {
-          float m1[DQ], sd1[DQ], M1;
-          issue(jb, m1, sd1, M1);
-          finish(jb, m1, sd1, M1, wb);
-        }
-        const int64_t jj = jb + lane;
-        const bool inw = jj < Wn;
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-          any[h] = any[h] || (__ballot(inw && selected(jj, wb[h], h)) != 0ull);
-          // first index of the chunk's largest non-NaN bound
-          const bool ok = inw && !isnan(wb[h]);
-          float bv = ok ? wb[h] : kNegInf;
-          int bi = ok ? (int)jj : 0x7fffffff;
-          wave_argmax(bv, bi);
-          if (bi != 0x7fffffff && (arg[h] < 0 || bv > best[h])) { best[h] = bv; arg[h] = bi; }
+      for (int h = 0; h < G; ++h) {
+        const bool any = __ballot(inw && selected(j, bnd[h], h)) != 0ull;
+        const bool ok = inw && !isnan(bnd[h]);
+        float bv = ok ? bnd[h] : kNegInf;
+        int bi = ok ? (int)j : 0x7fffffff;
+        wave_argmax(bv, bi);
+        if (lane == 0) {
+          const int64_t e = (hq0 + h) * kRescueTiles + tile;
+          a.resc_best[e] = bv;
+          a.resc_info[e] = any ? kRescueAny : (bi == 0x7fffffff ? kRescueNone : bi);
         }
       }
-#pragma unroll
-      for (int h = 0; h < G; ++h)
-        if (!any[h] && arg[h] == j) bits |= 1u << h;
+      if (inw) a.wbits[bg * kMaxRescueWindow + j] = (uint8_t)bits;
     }
-    if (w != 0) return;
     if (j < g.ncap) {
 #pragma unroll
       for (int h = 0; h < G; ++h) a.mask[(hq0 + h) * g.ncap + j] = (uint8_t)((bits >> h) & 1u);
@@ -903,13 +893,23 @@ struct SplitArgs {
   const float* tau;
   const int32_t* ids;
   const int32_t* tile_cnt;
-  float2* part_ml;
-  float* part_acc;
+  float2* part_ml;           // [splits][G] (max, sum) per split workgroup and head
+  float* part_acc;           // [splits][G][D]
+  const float* resc_best;    // screening's window parts (see ScreenArgs)
+  const int32_t* resc_info;
+  const uint8_t* wbits;
+  uint8_t* mask;             // the rescued blocks' mask bits are set here
+  int32_t* resc_out;         // [B][Hq] rescued block per head, or -1 (for the combine)
+  int32_t* extra_union;      // [B][Hkv] rescued blocks outside the union (for the combine)
+  int2* plan;                // [B][Hkv] (first split workgroup, splits) of each group
   Geom g;
   int q_dtype;
   float beta, offset_a;
   int self_ungated;
+  int c;                     // rescue window (blocks)
+  int S_uniform;             // > 0: S splits per group, grid (S, Hkv, B); 0: proportional, 1-D grid
 };
+
 
 // Gated score S~ = S sigmoid(beta (S - tau_eff)); -inf when the head does not
 // attend the token.
@@ -1218,8 +1218,6 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
   constexpr int GQ = 4 * NQ;
   constexpr int DC = D / 8;
   const Geom& g = a.g;
-  const int s = blockIdx.x, gh = blockIdx.y, b = blockIdx.z;
-  const int S = gridDim.x;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   __shared__ float qf_s[BF ? 1 : D][G];                  // fp32 path: scaled q
   __shared__ bf16x8 qa_s[BF ? NQ * 2 * 4 * DC : 1];      // bf16 path: q chunks (hi, lo)
@@ -1232,17 +1230,106 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
   __shared__ int32_t item_j[kItemChunk];
   __shared__ uint8_t item_bits[kItemChunk];
   __shared__ uint8_t item_sub[kItemChunk];
+  __shared__ int grp_s[DENSE ? 1 : kPropMaxGroups + 1];  // proportional: first split of each group
+  __shared__ int cnt_s[DENSE ? 1 : kPropMaxCounts];      // proportional: every tile count
+  __shared__ int who_s[2];                               // proportional: group, split index
+  __shared__ float rbest_s[DENSE ? 1 : G][kRescueTiles];
+  __shared__ int rinfo_s[DENSE ? 1 : G][kRescueTiles];
+  __shared__ int resc_s[G];                              // rescued block per head, or -1
+  __shared__ int rx_s[G][2];                             // distinct rescued blocks: (block, heads)
+  __shared__ int rxw_s[G];                               // union bits at each head's rescued block
+  __shared__ int nrx_s;
 
+  // ---- which (sequence, kv head) and split.  Uniform: S splits per group, grid
+  // (S, Hkv, B).  Proportional (several sequences): a 1-D grid whose workgroups are
+  // dealt to the groups in proportion to their union's 64-token tiles (at least
+  // one each), so short and long unions finish together in one round.
+  constexpr int SPB = BF ? BS / 64 : 1;
+  const bool uniform = DENSE || a.S_uniform > 0;
+  int b, gh, s, S, first;
+  const int32_t* tc;
+  if (uniform) {
+    s = blockIdx.x;
+    gh = blockIdx.y;
+    b = blockIdx.z;
+    S = gridDim.x;
+    first = (b * g.Hkv + gh) * S;
+    tc = a.tile_cnt + ((int64_t)b * g.Hkv + gh) * g.n_tiles;
+  } else {
+    const int BG = g.B * g.Hkv, nc = BG * g.n_tiles, W = gridDim.x;
+    for (int i = tid; i < nc; i += NT) cnt_s[i] = a.tile_cnt[i];
+    __syncthreads();
+    // each group's work: its union's tiles, plus one for a tail
+    int64_t mine = 0;
+    for (int x = tid; x < BG; x += NT) {
+      int u = 0;
+      for (int t = 0; t < g.n_tiles; ++t) u += cnt_s[x * g.n_tiles + t];
+      const int64_t T_b = clamp_len(a.seq_lens, x / g.Hkv, g.cap);
+      const int work = u * SPB + ((T_b % BS) != 0 ? 1 : 0);
+      grp_s[x] = work;
+      mine += work;
+    }
+    // total work (integer sums: any order)
+    for (int o = 32; o > 0; o >>= 1) mine += __shfl_xor(mine, o, 64);
+    if (lane == 0) wsum_s[w] = (int)mine;
+    __syncthreads();
+    int64_t UT = 0;
+#pragma unroll
+    for (int k = 0; k < NW; ++k) UT += wsum_s[k];
+    __syncthreads();
+    // splits per group, then their exclusive prefix (one thread: BG <= 1024)
+    for (int x = tid; x < BG; x += NT)
+      grp_s[x] = 1 + (UT > 0 ? (int)((int64_t)(W - BG) * grp_s[x] / UT) : 0);
+    __syncthreads();
+    if (tid == 0) {
+      int acc = 0;
+      for (int x = 0; x < BG; ++x) {
+        const int n = grp_s[x];
+        grp_s[x] = acc;
+        acc += n;
+      }
+      grp_s[BG] = acc;
+      // this workgroup's group: the last one starting at or before it
+      int lo = 0, hi = BG;
+      const int me = (int)blockIdx.x;
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (grp_s[mid] <= me) lo = mid; else hi = mid;
+      }
+      who_s[0] = me < acc ? lo : -1;
+      who_s[1] = me - grp_s[lo];
+    }
+    __syncthreads();
+    const int bgi = who_s[0];
+    if (bgi < 0) return;             // workgroups past the allocation (uniform exit)
+    b = bgi / g.Hkv;
+    gh = bgi % g.Hkv;
+    s = who_s[1];
+    first = grp_s[bgi];
+    S = grp_s[bgi + 1] - first;
+    tc = cnt_s + (int64_t)bgi * g.n_tiles;
+  }
   const int64_t hq0 = (int64_t)b * g.Hq + (int64_t)gh * G;
   const int64_t bg = (int64_t)b * g.Hkv + gh;
   const float scale = 1.0f / sqrtf((float)D);
   // The independent loads go out together: length, the first 256 tile counts,
-  // thresholds and the query elements (as raw bits, converted afterwards, so
-  // that no conversion waits on its own load).
+  // thresholds, the rescue window's parts and the query elements (as raw bits,
+  // converted afterwards, so that no conversion waits on its own load).
   const int64_t T = clamp_len(a.seq_lens, b, g.cap);
-  const int32_t* tc = a.tile_cnt + bg * g.n_tiles;
   const int tc0 = (!DENSE && tid < g.n_tiles) ? tc[tid] : 0;
   const float tau_in = (!DENSE && tid < G) ? a.tau[hq0 + tid] : 0.f;
+  const int64_t N = T / BS;
+  const int64_t Wn = (int64_t)a.c < N ? (int64_t)a.c : N;
+  const int nwt = (int)((Wn + kScreenTile - 1) / kScreenTile);    // window tiles
+  if constexpr (!DENSE) {
+    if (tid < G * kRescueTiles) {
+      const int h = tid / kRescueTiles, t = tid % kRescueTiles;
+      if (t < nwt) {
+        rbest_s[h][t] = a.resc_best[(hq0 + h) * kRescueTiles + t];
+        rinfo_s[h][t] = a.resc_info[(hq0 + h) * kRescueTiles + t];
+      }
+    }
+  }
   constexpr int QE = BF ? NQ * 4 * D : G * D;          // staged query elements
   constexpr int QR = (QE + NT - 1) / NT;
   uint32_t qraw[QR];
@@ -1254,7 +1341,6 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
     qraw[r] = a.q_dtype == ETA_DT_F32 ? reinterpret_cast<const uint32_t*>(a.q)[src]
                                       : (uint32_t)reinterpret_cast<const uint16_t*>(a.q)[src];
   }
-  const int64_t N = T / BS;
   const int ntail = (int)(T - N * BS);
 #pragma unroll
   for (int r = 0; r < QR; ++r) {
@@ -1285,7 +1371,6 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
   // (shares differ by at most one tile and each spreads over the whole list,
   // which measured faster than contiguous ranges); on the fp32 path the
   // contiguous range of whole blocks [lo, hi).
-  constexpr int SPB = BF ? BS / 64 : 1;
   int64_t UI;                // items (blocks) in the list
   if constexpr (DENSE) {
     UI = N;
@@ -1316,6 +1401,59 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
     if (tid == 0) pref_s[g.n_tiles] = carry;
     UI = carry;
   }
+  // top-1 rescue (App. "Top-1 Rescue, Tail Handling, and Kernel Validation"):
+  // for each head, when no block of the window [0, Wn) is selected, the first of
+  // the window's largest bounds (tiles in order, strict >, each tile's own first
+  // largest) is attended as well.  Each distinct rescued block becomes one more
+  // item of the list, after the union's, carrying the heads that rescued it (a
+  // rescued head attends it only there, also when the block is in the union for
+  // other heads, which then reads it once more).
+  uint32_t wb_rescued = 1u;
+  if constexpr (!DENSE) {
+    if (tid < G) {
+      int jr = -1;
+      if (a.c > 0 && Wn > 0) {
+        bool any = false;
+        float best = kNegInf;
+        int arg = -1;
+        for (int t = 0; t < nwt; ++t) {
+          const int inf = rinfo_s[tid][t];
+          if (inf == kRescueAny) {
+            any = true;
+          } else if (inf >= 0 && (arg < 0 || rbest_s[tid][t] > best)) {
+            best = rbest_s[tid][t];
+            arg = inf;
+          }
+        }
+        if (!any) jr = arg;
+      }
+      resc_s[tid] = jr;
+      // whether the rescued block is in the union: for the union count only (the
+      // last split writes it after streaming)
+      if (s == S - 1 && jr >= 0) wb_rescued = a.wbits[bg * kMaxRescueWindow + jr];
+    }
+    if (s == 0 && tid == 0) a.plan[bg] = make_int2(first, S);
+    __syncthreads();
+    if (tid == 0) {
+      int nb = 0;
+      for (int h = 0; h < G; ++h) {
+        const int j = resc_s[h];
+        if (j < 0) continue;
+        int k = 0;
+        while (k < nb && rx_s[k][0] != j) ++k;
+        if (k == nb) {
+          rx_s[nb][0] = j;
+          rx_s[nb][1] = 0;
+          ++nb;
+        }
+        rx_s[k][1] |= 1 << h;
+      }
+      nrx_s = nb;
+    }
+    __syncthreads();
+  }
+  const int64_t UI_union = UI;
+  if constexpr (!DENSE) UI += nrx_s;
   const int64_t lo = (UI * s) / S, hi = (UI * (s + 1)) / S;
   __syncthreads();
 
@@ -1349,6 +1487,9 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
     if constexpr (DENSE) {
       jo = (int32_t)it;
       bo = (uint8_t)all_bits;
+    } else if (it >= UI_union) {        // rescued block: the heads that rescued it
+      jo = rx_s[it - UI_union][0];
+      bo = (uint8_t)rx_s[it - UI_union][1];
     } else {
       int tl = 0, th = g.n_tiles;       // pref_s[tl] <= it < pref_s[th]
       while (th - tl > 1) {
@@ -1394,7 +1535,28 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
       __syncthreads();
     }
   }
-  if (s == S - 1 && ntail > 0 && w == 0) attend(N * BS, ntail, all_bits);
+  if constexpr (!DENSE) {
+    if (s == S - 1) {
+      // the rescued blocks' mask bits, and (for the combine) each head's rescued
+      // block and how many rescued blocks are outside the union
+      if (tid < G) rxw_s[tid] = (int)wb_rescued;        // union bits at the rescued block
+      __syncthreads();
+      if (tid == 0) {
+        int extra = 0;
+        for (int k = 0; k < nrx_s; ++k) {
+          int in_union = 0;
+          for (int h = 0; h < G; ++h) in_union |= (resc_s[h] == rx_s[k][0] && rxw_s[h] != 0);
+          extra += !in_union;
+        }
+        a.extra_union[bg] = extra;
+      }
+      if (tid < G) {
+        a.resc_out[hq0 + tid] = resc_s[tid];
+        if (resc_s[tid] >= 0) a.mask[(hq0 + tid) * g.ncap + resc_s[tid]] = 1;
+      }
+    }
+  }
+  if (s == S - 1 && ntail > 0 && w == NW - 1) attend(N * BS, ntail, all_bits);
 
   // merge the four wavefront states
   if (lane == 0) {
@@ -1422,9 +1584,9 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
         o = fmaf(mrg_acc[k][h][i], wk, o);
       }
     }
-    const int64_t row = (hq0 + h) * S + s;
-    a.part_acc[row * D + i] = o;
-    if (i == 0) a.part_ml[row] = make_float2(ms, L);
+    const int64_t pidx = (int64_t)(first + s) * G + h;
+    a.part_acc[pidx * D + i] = o;
+    if (i == 0) a.part_ml[pidx] = make_float2(ms, L);
   }
 }
 
@@ -1588,17 +1750,20 @@ __global__ __launch_bounds__(256) void calib_solve_kernel(CalibSolveArgs a) {
 // ---------------------------------------------------------------- combine
 
 struct CombineArgs {
-  const float2* part_ml;
-  const float* part_acc;
+  const float2* part_ml;     // [splits][G]
+  const float* part_acc;     // [splits][G][D]
   const int32_t* head_cnt;
   const int32_t* tile_cnt;
   const int32_t* seq_lens;
+  const int32_t* resc_out;   // rescued block per head or -1 (nullptr: dense)
+  const int32_t* extra_union;
+  const int2* plan;          // (first split, splits) per group; nullptr: uniform S
   int32_t* counts;
   int32_t* union_counts;
   void* out;
   Geom g;
   int q_dtype;
-  int S;
+  int S;                     // uniform splits per group (plan == nullptr)
 };
 
 // One workgroup of 512 threads per (sequence, query head).  Thread (i, part)
@@ -1632,31 +1797,43 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
   const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int i = tid % D, part = tid / D;
   const int64_t row = (int64_t)b * g.Hq + h;
-  const float2* ml = a.part_ml + row * a.S;
-  const float* accp = a.part_acc + row * a.S * D + i;
+  const int64_t bg = (int64_t)b * g.Hkv + h / g.G;
+  const int hh = h % g.G;
   // per-head selected blocks: wavefront 0 sums the head's tile counts; the
   // union blocks of the (sequence, kv head): wavefront 1 of the group's first
-  // head sums the union's tile counts (both issued first)
+  // head sums the union's tile counts (both issued first, with the rescue
+  // results and the group's split range)
   int cnt = 0;
   if (a.counts != nullptr && tid < 64)
     for (int t = tid; t < g.n_tiles; t += 64) cnt += a.head_cnt[row * g.n_tiles + t];
-  const bool do_union = a.union_counts != nullptr && h % g.G == 0 && tid >= 64 && tid < 128;
-  const int64_t bg = (int64_t)b * g.Hkv + h / g.G;
+  const bool do_union = a.union_counts != nullptr && hh == 0 && tid >= 64 && tid < 128;
   int ucnt = 0;
   if (do_union)
     for (int t = tid - 64; t < g.n_tiles; t += 64) ucnt += a.tile_cnt[bg * g.n_tiles + t];
+  const int rescued = (a.resc_out != nullptr && tid == 0) ? a.resc_out[row] : -1;
+  const int extra = (a.extra_union != nullptr && tid == 64 && do_union) ? a.extra_union[bg] : 0;
+  int first = (int)bg * a.S, S = a.S;
+  if (a.plan != nullptr) {
+    const int2 pl = a.plan[bg];
+    first = pl.x;
+    S = pl.y;
+  }
+  // split s's partial of this head: (first + s) G + hh
+  const float2* ml = a.part_ml + (int64_t)first * g.G + hh;
+  const float* accp = a.part_acc + ((int64_t)first * g.G + hh) * D + i;
+  const int64_t st = g.G;          // partials between consecutive splits
   float2 mv[kCombPrefetch];
   float av[kCombPrefetch];
   float mloc = kNegInf;
 #pragma unroll
   for (int k = 0; k < kCombPrefetch; ++k) {
     const int sidx = part + P * k;
-    const bool in = sidx < a.S;
-    mv[k] = in ? ml[sidx] : make_float2(kNegInf, 0.f);
-    av[k] = in ? accp[(int64_t)sidx * D] : 0.f;
+    const bool in = sidx < S;
+    mv[k] = in ? ml[sidx * st] : make_float2(kNegInf, 0.f);
+    av[k] = in ? accp[sidx * st * D] : 0.f;
     mloc = fmaxf(mloc, mv[k].x);
   }
-  for (int sidx = part + P * kCombPrefetch; sidx < a.S; sidx += P) mloc = fmaxf(mloc, ml[sidx].x);
+  for (int sidx = part + P * kCombPrefetch; sidx < S; sidx += P) mloc = fmaxf(mloc, ml[sidx * st].x);
   const float ms = block_reduce(mloc, true, red);
   float o = 0.f, L = 0.f;
   if (ms != kNegInf) {
@@ -1666,10 +1843,10 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
       o = fmaf(wk, av[k], o);
       L = fmaf(mv[k].y, wk, L);
     }
-    for (int sidx = part + P * kCombPrefetch; sidx < a.S; sidx += P) {
-      const float2 e = ml[sidx];
+    for (int sidx = part + P * kCombPrefetch; sidx < S; sidx += P) {
+      const float2 e = ml[sidx * st];
       const float wk = e.x == kNegInf ? 0.f : __expf(e.x - ms);
-      o = fmaf(wk, accp[(int64_t)sidx * D], o);
+      o = fmaf(wk, accp[sidx * st * D], o);
       L = fmaf(e.y, wk, L);
     }
   }
@@ -1691,13 +1868,13 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
     if (tid == 0) {
       const int64_t T = clamp_len(a.seq_lens, b, g.cap);
       const int64_t N = T / g.BS;
-      a.counts[row] = (int32_t)((int64_t)cnt * g.BS + (T - N * g.BS));
+      a.counts[row] = (int32_t)(((int64_t)cnt + (rescued >= 0 ? 1 : 0)) * g.BS + (T - N * g.BS));
     }
   }
   if (do_union) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) ucnt += __shfl_xor(ucnt, o, 64);
-    if (tid == 64) a.union_counts[bg] = ucnt;
+    if (tid == 64) a.union_counts[bg] = ucnt + extra;
   }
 }
 
@@ -1767,8 +1944,8 @@ void launch_screen_impl(const Geom& g, const ScreenArgs& sa, hipStream_t stream)
 }
 
 template <bool DENSE>
-void launch_split_impl(const Geom& g, int S, const SplitArgs& sp, hipStream_t stream) {
-  dim3 grid(S, g.Hkv, g.B);
+void launch_split_impl(const Geom& g, const SplitPlan& pl, const SplitArgs& sp, hipStream_t stream) {
+  const dim3 grid = pl.S > 0 ? dim3(pl.S, g.Hkv, g.B) : dim3(pl.W);
 #define ETA_SPL(D_, BS_, G_, T_)                                                                \
   if (g.D == D_ && g.BS == BS_ && g.G == G_)                                                    \
     hipLaunchKernelGGL((split_kernel<D_, BS_, G_, T_, DENSE>), grid, dim3(64 * kSplitWaves), 0, stream, sp);
@@ -1815,19 +1992,22 @@ hipError_t launch_decode(const Geom& g, const DecodeCfg& c, int q_dtype, const v
     if (e0 != hipSuccess) return e0;
   }
   ScreenArgs sa{q, seq_lens, separate ? ws.tau : tau, W, bias, ws.tau, tau_out, s.mu, s.sigma,
-                s.max_norm, mask, ws.ids, ws.tile_cnt, ws.head_cnt, nullptr, g, q_dtype,
-                (predict && !separate) ? 1 : 0, c.z, c.offset_a, c.rescue_window, c.lwb,
-                c.screen_all};
+                s.max_norm, mask, ws.ids, ws.tile_cnt, ws.head_cnt, nullptr, ws.resc_best,
+                ws.resc_info, ws.wbits, g, q_dtype, (predict && !separate) ? 1 : 0, c.z,
+                c.offset_a, c.rescue_window, c.lwb, c.screen_all};
   hipError_t e = with_hook(hook, ETA_KERNEL_SCREEN, stream,
                            [&] { launch_screen_impl<false>(g, sa, stream); });
   if (e != hipSuccess) return e;
   SplitArgs sp{q, k, v, seq_lens, predict ? ws.tau : tau, ws.ids, ws.tile_cnt, ws.part_ml,
-               ws.part_acc, g, q_dtype, c.beta, c.offset_a, c.self_ungated};
+               ws.part_acc, ws.resc_best, ws.resc_info, ws.wbits, mask, ws.resc_out,
+               ws.extra_union, ws.plan, g, q_dtype, c.beta, c.offset_a, c.self_ungated,
+               c.rescue_window, c.plan.S};
   e = with_hook(hook, ETA_KERNEL_SPLIT_DECODE, stream,
-                [&] { launch_split_impl<false>(g, c.S, sp, stream); });
+                [&] { launch_split_impl<false>(g, c.plan, sp, stream); });
   if (e != hipSuccess) return e;
-  CombineArgs ca{ws.part_ml, ws.part_acc, ws.head_cnt, ws.tile_cnt, seq_lens, counts,
-                 union_counts, out, g, q_dtype, c.S};
+  CombineArgs ca{ws.part_ml, ws.part_acc, ws.head_cnt, ws.tile_cnt, seq_lens, ws.resc_out,
+                 ws.extra_union, c.plan.S > 0 ? nullptr : ws.plan, counts, union_counts, out, g,
+                 q_dtype, c.plan.S};
   return with_hook(hook, ETA_KERNEL_COMBINE, stream, [&] { launch_combine_impl(g, ca, stream); });
 }
 
@@ -1835,8 +2015,8 @@ hipError_t launch_bounds(const Geom& g, int q_dtype, const void* q, const int32_
                          const eta_summary_t& s, float z, float* bounds, hipStream_t stream,
                          LaunchHook hook) {
   ScreenArgs sa{q, seq_lens, nullptr, nullptr, nullptr, nullptr, nullptr, s.mu, s.sigma,
-                s.max_norm, nullptr, nullptr, nullptr, nullptr, bounds, g, q_dtype, 0, z, 0.f,
-                0, 0, 0};
+                s.max_norm, nullptr, nullptr, nullptr, nullptr, bounds, nullptr, nullptr, nullptr,
+                g, q_dtype, 0, z, 0.f, 0, 0, 0};
   return with_hook(hook, ETA_KERNEL_BOUNDS, stream,
                    [&] { launch_screen_impl<true>(g, sa, stream); });
 }
@@ -1869,12 +2049,13 @@ hipError_t launch_dense(const Geom& g, int S, int q_dtype, const void* q, const 
                         const void* v, const int32_t* seq_lens, void* out, const DecodeWs& ws,
                         hipStream_t stream, LaunchHook hook) {
   SplitArgs sp{q, k, v, seq_lens, nullptr, nullptr, nullptr, ws.part_ml, ws.part_acc,
-               g, q_dtype, 0.f, 0.f, 0};
+               nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, g, q_dtype, 0.f,
+               0.f, 0, 0, S};
   hipError_t e = with_hook(hook, ETA_KERNEL_DENSE_SPLIT, stream,
-                           [&] { launch_split_impl<true>(g, S, sp, stream); });
+                           [&] { launch_split_impl<true>(g, SplitPlan{S, S * g.B * g.Hkv}, sp, stream); });
   if (e != hipSuccess) return e;
-  CombineArgs ca{ws.part_ml, ws.part_acc, nullptr, nullptr, seq_lens, nullptr, nullptr, out, g,
-                 q_dtype, S};
+  CombineArgs ca{ws.part_ml, ws.part_acc, nullptr, nullptr, seq_lens, nullptr, nullptr, nullptr,
+                 nullptr, nullptr, out, g, q_dtype, S};
   return with_hook(hook, ETA_KERNEL_DENSE_COMBINE, stream,
                    [&] { launch_combine_impl(g, ca, stream); });
 }
