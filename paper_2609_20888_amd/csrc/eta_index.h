@@ -1,0 +1,87 @@
+// Index arithmetic of the split-decode kernel: the proportional split plan, the
+// union list's tile prefix and item lookup, and the splits' shares.  Every
+// function is host + device code and touches only the arrays it is given, so
+// the CPU bounds harness (tests/cpu_tier) runs the kernels' own arithmetic on
+// edge geometries under the address and undefined-behaviour sanitizers.
+#pragma once
+
+#include <stdint.h>
+
+#if defined(__HIPCC__)
+#define ETA_HD __host__ __device__ __forceinline__
+#else
+#define ETA_HD inline
+#endif
+
+namespace eta {
+
+// Work of one (sequence, kv head) group for the proportional plan, in 64-token
+// tiles: its union blocks' tiles, plus one when the sequence has a partial tail.
+ETA_HD int group_work(int union_blocks, int tiles_per_block, int64_t seq_len, int block) {
+  return union_blocks * tiles_per_block + ((seq_len % block) != 0 ? 1 : 0);
+}
+
+// Splits of a group under the proportional plan: one each, and the remaining
+// W - BG dealt in proportion to the groups' work (rounded down), so the sum over
+// the groups never exceeds W.  W >= BG >= 1.
+ETA_HD int group_splits(int work, int64_t total_work, int W, int BG) {
+  return 1 + (total_work > 0 ? (int)((int64_t)(W - BG) * work / total_work) : 0);
+}
+
+// In place: v[0..n) -> exclusive prefix sums; returns the total (callers keep it
+// in v[n]).
+ETA_HD int exclusive_prefix(int* v, int n) {
+  int acc = 0;
+  for (int x = 0; x < n; ++x) {
+    const int k = v[x];
+    v[x] = acc;
+    acc += k;
+  }
+  return acc;
+}
+
+// The group of split workgroup `me`: the last g with first[g] <= me; -1 when me
+// is past the allocation (first[n] = the number of split workgroups used).
+ETA_HD int find_group(const int* first, int n, int me) {
+  if (me >= first[n]) return -1;
+  int lo = 0, hi = n;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (first[mid] <= me) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+// Union list item `it` (pref = exclusive prefix of the per-tile union counts,
+// pref[n_tiles] = their total, it < that total) -> the screening tile holding it
+// and its slot among that tile's compacted ids: pref[tile] <= it < pref[tile + 1].
+ETA_HD void resolve_item(const int* pref, int n_tiles, int64_t it, int* tile, int* slot) {
+  int tl = 0, th = n_tiles;
+  while (th - tl > 1) {
+    const int mid = (tl + th) >> 1;
+    if (pref[mid] <= it) tl = mid; else th = mid;
+  }
+  *tile = tl;
+  *slot = (int)(it - pref[tl]);
+}
+
+// Number of 64-token tiles of split s of S under the strided share (tiles s,
+// s + S, s + 2 S, ... of total_tiles).
+ETA_HD int strided_share(int64_t total_tiles, int s, int S) {
+  return total_tiles > s ? (int)((total_tiles - s + S - 1) / S) : 0;
+}
+
+// Contiguous share [lo, hi) of `items` for split s of S (the fp32 path).
+ETA_HD void contiguous_share(int64_t items, int s, int S, int64_t* lo, int64_t* hi) {
+  *lo = (items * s) / S;
+  *hi = (items * (s + 1)) / S;
+}
+
+// Position of a compacted union id: tile t of a group whose ids start at
+// group_base, lane l with ballot bal of the tile's union blocks.
+ETA_HD int64_t union_slot(int64_t group_base, int tile, uint64_t bal, int lane) {
+  const uint64_t below = lane == 0 ? 0ull : (bal & ((~0ull) >> (64 - lane)));
+  return group_base + (int64_t)tile * 64 + __builtin_popcountll(below);
+}
+
+}  // namespace eta

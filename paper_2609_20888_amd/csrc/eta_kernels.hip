@@ -29,6 +29,7 @@
 #include <type_traits>
 
 #include "eta_device.h"
+#include "eta_index.h"
 #include "eta_internal.h"
 
 namespace eta {
@@ -836,9 +837,7 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
     }
     // ordered compaction of the tile's union ids and the per-head counts
     const unsigned long long bal = __ballot(bits != 0);
-    if (bits != 0)
-      a.ids[bg * g.ncap + (int64_t)tile * kScreenTile + __popcll(bal & ((1ull << lane) - 1ull))] =
-          (int32_t)((uint32_t)j | (bits << 24));
+    if (bits != 0) a.ids[union_slot(bg * g.ncap, tile, bal, lane)] = (int32_t)((uint32_t)j | (bits << 24));
     if (lane == 0) a.tile_cnt[bg * g.n_tiles + tile] = __popcll(bal);
 #pragma unroll
     for (int h = 0; h < G; ++h) {
@@ -1264,8 +1263,7 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
     for (int x = tid; x < BG; x += NT) {
       int u = 0;
       for (int t = 0; t < g.n_tiles; ++t) u += cnt_s[x * g.n_tiles + t];
-      const int64_t T_b = clamp_len(a.seq_lens, x / g.Hkv, g.cap);
-      const int work = u * SPB + ((T_b % BS) != 0 ? 1 : 0);
+      const int work = group_work(u, SPB, clamp_len(a.seq_lens, x / g.Hkv, g.cap), BS);
       grp_s[x] = work;
       mine += work;
     }
@@ -1278,26 +1276,14 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
     for (int k = 0; k < NW; ++k) UT += wsum_s[k];
     __syncthreads();
     // splits per group, then their exclusive prefix (one thread: BG <= 1024)
-    for (int x = tid; x < BG; x += NT)
-      grp_s[x] = 1 + (UT > 0 ? (int)((int64_t)(W - BG) * grp_s[x] / UT) : 0);
+    for (int x = tid; x < BG; x += NT) grp_s[x] = group_splits(grp_s[x], UT, W, BG);
     __syncthreads();
     if (tid == 0) {
-      int acc = 0;
-      for (int x = 0; x < BG; ++x) {
-        const int n = grp_s[x];
-        grp_s[x] = acc;
-        acc += n;
-      }
-      grp_s[BG] = acc;
+      grp_s[BG] = exclusive_prefix(grp_s, BG);
       // this workgroup's group: the last one starting at or before it
-      int lo = 0, hi = BG;
-      const int me = (int)blockIdx.x;
-      while (hi - lo > 1) {
-        const int mid = (lo + hi) >> 1;
-        if (grp_s[mid] <= me) lo = mid; else hi = mid;
-      }
-      who_s[0] = me < acc ? lo : -1;
-      who_s[1] = me - grp_s[lo];
+      const int me = (int)blockIdx.x, gi = find_group(grp_s, BG, me);
+      who_s[0] = gi;
+      who_s[1] = gi >= 0 ? me - grp_s[gi] : 0;
     }
     __syncthreads();
     const int bgi = who_s[0];
@@ -1454,7 +1440,8 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
   }
   const int64_t UI_union = UI;
   if constexpr (!DENSE) UI += nrx_s;
-  const int64_t lo = (UI * s) / S, hi = (UI * (s + 1)) / S;
+  int64_t lo, hi;
+  contiguous_share(UI, s, S, &lo, &hi);
   __syncthreads();
 
   const KVT* kb = reinterpret_cast<const KVT*>(a.k) + (int64_t)b * g.sb + (int64_t)gh * g.sh;
@@ -1491,12 +1478,9 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
       jo = rx_s[it - UI_union][0];
       bo = (uint8_t)rx_s[it - UI_union][1];
     } else {
-      int tl = 0, th = g.n_tiles;       // pref_s[tl] <= it < pref_s[th]
-      while (th - tl > 1) {
-        const int mid = (tl + th) >> 1;
-        if (pref_s[mid] <= it) tl = mid; else th = mid;
-      }
-      const uint32_t id = (uint32_t)a.ids[bg * g.ncap + (int64_t)tl * kScreenTile + (it - pref_s[tl])];
+      int tl, slot;
+      resolve_item(pref_s, g.n_tiles, it, &tl, &slot);
+      const uint32_t id = (uint32_t)a.ids[bg * g.ncap + (int64_t)tl * kScreenTile + slot];
       jo = (int32_t)(id & kIdMask);
       bo = (uint8_t)(id >> 24);
     }
@@ -1505,8 +1489,7 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
     // kItemChunk of the share's tiles at a time, resolved by all threads at once;
     // wavefront w takes the chunk's tiles w, w + NW, ... so the wavefronts finish
     // within one tile
-    const int64_t UT = UI * SPB;
-    const int nt = UT > s ? (int)((UT - s + S - 1) / S) : 0;
+    const int nt = strided_share(UI * SPB, s, S);
     for (int k0 = 0; k0 < nt; k0 += kItemChunk) {
       const int n = nt - k0 < kItemChunk ? nt - k0 : kItemChunk;
       if (tid < n) {
