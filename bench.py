@@ -103,14 +103,8 @@ def measure_prefill(torch, eta, dev):
     psl = torch.full((pB,), pT, dtype=torch.int32, device=dev)
     pout, pR, pL = eta.gated_prefill(pq, pk, pv, ptau, psl, beta=4.0)
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    reps = 5
-    e0.record()
-    for _ in range(reps):
-        eta.gated_prefill(pq, pk, pv, ptau, psl, beta=4.0, out=pout, R=pR, L=pL)
-    e1.record()
-    torch.cuda.synchronize()
-    pms = e0.elapsed_time(e1) / reps
+    pms = batch_median_ms(torch, lambda: eta.gated_prefill(pq, pk, pv, ptau, psl, beta=4.0, out=pout,
+                                                           R=pR, L=pL), reps=5)
     pflops = 4.0 * pd * pHq * pT * (pT + 1) / 2      # QK^T and p.V over the causal pairs
     prefill = {"workload": f"B={pB}, {pT} tokens, {pHq}/{pHkv} heads, d={pd}, bf16, causal",
                "ms": round(pms, 3), "tflops": round(pflops / pms / 1e9, 1),
@@ -141,6 +135,22 @@ def time_cold(torch, run, steps, flush):
     d = sorted(a.elapsed_time(b) * 1e3 for a, b in evs)
     pick = lambda f: round(d[min(len(d) - 1, int(f * len(d)))], 2)
     return round(sum(d) / len(d), 2), pick(0.1), pick(0.5), pick(0.9)
+
+
+def batch_median_ms(torch, fn, reps=10, batches=3):
+    """Milliseconds per call: events around `reps` back-to-back calls, the median of
+    `batches` such batches (after one untimed call)."""
+    fn()
+    out = []
+    for _ in range(batches):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        out.append(a.elapsed_time(b) / reps)
+    return sorted(out)[len(out) // 2]
 
 
 def time_warm(torch, run, steps, warmup=5):
@@ -266,13 +276,7 @@ def main():
     summ = eta.build_block_summaries(k, sl, bs, num_q_heads=Hq)
     torch.cuda.synchronize()
     s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    reps = 5
-    s0.record()
-    for _ in range(reps):
-        eta.build_block_summaries(k, sl, bs, num_q_heads=Hq, out=summ)
-    s1.record()
-    torch.cuda.synchronize()
-    sum_ms = s0.elapsed_time(s1) / reps
+    sum_ms = batch_median_ms(torch, lambda: eta.build_block_summaries(k, sl, bs, num_q_heads=Hq, out=summ))
     sum_bytes = B * Hkv * wl.seq_lens[0] * d * e + B * Hkv * (wl.seq_lens[0] // bs) * (2 * d * 4 + 4)
     log(f"[bench] summary build {sum_ms * 1e3:.1f} us ({sum_bytes / sum_ms / 1e6:.0f} GB/s)")
 
@@ -282,12 +286,8 @@ def main():
     env_sub = bs // 16
     env = eta.build_block_summaries(k, sl, bs, num_q_heads=Hq, sub_block=env_sub)
     torch.cuda.synchronize()
-    s0.record()
-    for _ in range(reps):
-        eta.build_block_summaries(k, sl, bs, num_q_heads=Hq, sub_block=env_sub, out=env)
-    s1.record()
-    torch.cuda.synchronize()
-    env_ms = s0.elapsed_time(s1) / reps
+    env_ms = batch_median_ms(torch, lambda: eta.build_block_summaries(k, sl, bs, num_q_heads=Hq,
+                                                                      sub_block=env_sub, out=env))
     prev = sl - 1
     upd_reps = 50
     s0.record()
