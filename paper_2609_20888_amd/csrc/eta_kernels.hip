@@ -290,6 +290,10 @@ __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ 
   constexpr int CH = NI * 4 <= 128 ? NI : 16;  // loads held at once (VGPR budget)
   constexpr int NCH = NI / CH;
   static_assert(LPR >= 8 && LPR <= 32 && NI % CH == 0, "unsupported summary shape");
+  // the envelope's sub-block sums over four row groups of 16 lanes (bf16 rows
+  // of 128) take the transposed route below when a sub-block spans all four
+  constexpr bool TR = ENV && LPR == 16 && EPL == 8;
+  const bool tr_on = TR && (1 << sub_log2) >= R;
   __shared__ float mu_s[D][kSumBlocks + 1];
   __shared__ float sg_s[D][kSumBlocks + 1];
   __shared__ float mx_s[kSumBlocks];
@@ -347,6 +351,7 @@ __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ 
       mean[e] = row_group_reduce<LPR>(s[e], [](float a, float c) { return a + c; }) * inv_bs;
       s[e] = 0.f;   // pass two keeps the envelope here
     }
+    float tr_s[2] = {0.f, 0.f};
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
       if constexpr (NCH > 1) {
@@ -371,28 +376,60 @@ __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ 
           const int ng = sub < R ? sub : R, kl = sub > R ? sub / R : 1;
           if (((c * CH + i + 1) & (kl - 1)) == 0) {
             const float inv_sub = 1.0f / (float)sub;
+            if (TR && ng == 4) {
+              // the eight coordinates' sums over the four row groups at once:
+              // each row swap exchanges two coordinates' rows, so the pairwise
+              // adds are those of partial_group_sum (same operands, same
+              // order) and coordinate 4 m + r ends in row r of tr_s[m]
+              float u[4];
 #pragma unroll
-            for (int e = 0; e < EPL; ++e) {
-              // the largest mean square deviation; its root is taken once at
-              // the end (the root is monotone, so this is the largest root)
-              const float t = partial_group_sum<LPR>(v[e], ng);
-              s[e] = fmaxf(s[e], t * inv_sub);
-              v[e] = 0.f;
+              for (int p = 0; p < 4; ++p) {
+                const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[2 * p]),
+                                                                __float_as_uint(v[2 * p + 1]), false, false);
+                u[p] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+              }
+#pragma unroll
+              for (int m = 0; m < 2; ++m) {
+                const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(u[2 * m]),
+                                                                __float_as_uint(u[2 * m + 1]), false, false);
+                tr_s[m] = fmaxf(tr_s[m], (__uint_as_float(r[0]) + __uint_as_float(r[1])) * inv_sub);
+              }
+#pragma unroll
+              for (int e = 0; e < EPL; ++e) v[e] = 0.f;
+            } else {
+#pragma unroll
+              for (int e = 0; e < EPL; ++e) {
+                // the largest mean square deviation; its root is taken once at
+                // the end (the root is monotone, so this is the largest root)
+                const float t = partial_group_sum<LPR>(v[e], ng);
+                s[e] = fmaxf(s[e], t * inv_sub);
+                v[e] = 0.f;
+              }
             }
           }
         }
       }
     }
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) {
-      float sd;
-      if constexpr (ENV)
-        sd = sqrtf(row_group_reduce<LPR>(s[e], [](float a, float c) { return fmaxf(a, c); }));
-      else
-        sd = sqrtf(row_group_reduce<LPR>(v[e], [](float a, float c) { return a + c; }) * inv_bs);
+    if (TR && tr_on) {
+      // row group rg holds coordinates rg and 4 + rg of its lane's eight
       if (rg == 0) {
-        mu_s[cl * EPL + e][jj] = mean[e];
-        sg_s[cl * EPL + e][jj] = sd;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) mu_s[cl * EPL + e][jj] = mean[e];
+      }
+      sg_s[cl * EPL + rg][jj] = sqrtf(tr_s[0]);
+      sg_s[cl * EPL + 4 + rg][jj] = sqrtf(tr_s[1]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) {
+        float sd;
+        if constexpr (ENV)
+          sd = sqrtf(row_group_reduce<LPR>(s[e], [](float a, float c) { return fmaxf(a, c); }));
+        else
+          sd = sqrtf(row_group_reduce<LPR>(v[e], [](float a, float c) { return a + c; }) * inv_bs);
+        if (rg == 0) {
+          mu_s[cl * EPL + e][jj] = mean[e];
+          sg_s[cl * EPL + e][jj] = sd;
+        }
       }
     }
     n2max = row_group_reduce<LPR>(n2max, [](float a, float c) { return fmaxf(a, c); });
