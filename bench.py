@@ -181,11 +181,41 @@ def step_bytes(wl, union_blocks, predictor: bool, stat_bytes: int = 4):
     return kv, kv + records + small
 
 
-def measure_config(torch, np, eta, dev, wl, steps, flush):
+def measure_compact(torch, np, eta, dev, wl, steps, flush, stat_dtype):
+    """The same workload screened on half-precision (or FP8) records: thresholds
+    placed from that index's own bounds (the same head survival), cold and warm
+    step and per-kernel times."""
+    from synth import place_bias
+    sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
+    summ = eta.build_block_summaries(wl.k, sl, wl.block, num_q_heads=wl.Hq, stat_dtype=stat_dtype)
+    nblk = [t // wl.block for t in wl.seq_lens]
+    if wl.W is not None:
+        bounds = eta.block_bounds(wl.q, sl, summ, wl.k, block_size=wl.block, z=wl.z).cpu().numpy()
+        qW = eta.predict_threshold(wl.q, wl.W, torch.zeros(wl.Hq, device=dev)).cpu().numpy()
+        bias = torch.as_tensor(place_bias(bounds, nblk, qW.astype(np.float64), wl.target_survival,
+                                          wl.a), device=dev)
+    else:
+        bias = wl.bias.to(dev)
+    p = eta.decode_params(beta=wl.beta, z=wl.z, offset_a=wl.a, rescue_window=wl.rescue_window,
+                          lwb=wl.lwb)
+    st = eta.DecodeStep(wl.q, wl.k, wl.v, sl, summ, wl.W, bias, block_size=wl.block, params=p)
+    warm = time_warm(torch, st.run, steps, warmup=10)
+    cold = time_cold(torch, st.run, max(10, steps // 2), flush)[0]
+    torch.cuda.synchronize()
+    eta.profile_begin()
+    for _ in range(20):
+        st.run()
+    torch.cuda.synchronize()
+    kt = {name: round(t / n * 1e3, 2) for name, (t, n) in eta.profile_end().items() if n}
+    return {"us_per_step_cold": cold, "us_per_step_warm": warm,
+            "union_blocks": int(st.union_counts.sum()), "kernel_avg_us_warm": kt}
+
+
+def measure_config(torch, np, eta, dev, wl, steps, flush, compact=False):
     """One workload at the library defaults: the prepared decode step (predicted or
     constant thresholds, the predictor bias placed from the GPU's own bounds) warm
     and cold, its union and algorithmic bytes, and the dense decode baseline at the
-    same shape (cold and warm)."""
+    same shape (cold and warm); with `compact`, also the step on fp16 records."""
     from synth import place_bias
     sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
     summ = eta.build_block_summaries(wl.k, sl, wl.block, num_q_heads=wl.Hq)
@@ -227,6 +257,10 @@ def measure_config(torch, np, eta, dev, wl, steps, flush):
          "dense_us_per_step_cold": dense_cold, "dense_us_per_step_warm": dense_warm,
          "speedup_vs_dense_cold": round(dense_cold / cold, 3),
          "speedup_vs_dense_warm": round(dense_warm / warm, 3), "kernel_avg_us_warm": kt}
+    if compact:
+        del st, summ
+        torch.cuda.empty_cache()
+        r["fp16_records"] = measure_compact(torch, np, eta, dev, wl, steps, flush, torch.float16)
     log(f"[bench] {wl.name}: {r}")
     return r
 
@@ -259,7 +293,8 @@ def main():
         mk = {"4k": lambda: config1(device=dev), "32k": lambda: config2(device=dev),
               "128k": lambda: config3(device=dev), "ragged": lambda: config5(device=dev),
               "ragged_pred": lambda: config5(device=dev, predictor=True)}[args.only_config]
-        r = measure_config(torch, np, eta, dev, mk(), args.steps, flush_buffer(torch, dev))
+        r = measure_config(torch, np, eta, dev, mk(), args.steps, flush_buffer(torch, dev),
+                           compact=args.only_config in ("128k", "ragged_pred"))
         print(json.dumps({args.only_config: r}), flush=True)
         return
 
@@ -494,14 +529,15 @@ def main():
     if not args.no_other_configs and not args.only_primary:
         from synth import config1, config2, config3, config5
         others = {}
-        for name, mk in (("b1_4k_mha4_d64_blk64_fp32_constant", lambda: config1(device=dev)),
-                         ("b1_32k_gqa16x4_d128_blk64_predictor", lambda: config2(device=dev)),
-                         ("b8_128k_gqa16x4_d128_blk64_predictor", lambda: config3(device=dev)),
-                         ("b32_ragged_16k_64k_gqa32x8_d128_blk64_constants", lambda: config5(device=dev)),
-                         ("b32_ragged_16k_64k_gqa32x8_d128_blk64_predictor",
-                          lambda: config5(device=dev, predictor=True))):
+        for name, mk, compact in (
+                ("b1_4k_mha4_d64_blk64_fp32_constant", lambda: config1(device=dev), False),
+                ("b1_32k_gqa16x4_d128_blk64_predictor", lambda: config2(device=dev), False),
+                ("b8_128k_gqa16x4_d128_blk64_predictor", lambda: config3(device=dev), True),
+                ("b32_ragged_16k_64k_gqa32x8_d128_blk64_constants", lambda: config5(device=dev), False),
+                ("b32_ragged_16k_64k_gqa32x8_d128_blk64_predictor",
+                 lambda: config5(device=dev, predictor=True), True)):
             owl = mk()
-            others[name] = measure_config(torch, np, eta, dev, owl, 50, flush)
+            others[name] = measure_config(torch, np, eta, dev, owl, 50, flush, compact)
             del owl
             torch.cuda.empty_cache()
 
