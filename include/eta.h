@@ -124,7 +124,10 @@ typedef struct {
   int32_t num_splits;           /* splits per (sequence, kv head), for several sequences their
                                    average (the splits are dealt to the (sequence, kv head)
                                    groups in proportion to their unions); 0: library default;
-                                   <= 1024 */
+                                   <= 1024; 1 with one sequence (or a uniform split layout):
+                                   each (sequence, kv head) is decoded by one workgroup that
+                                   writes the results itself, with no merge launch (App.
+                                   "Chunked Decoding and Two-Stage Reduction", one chunk) */
 } eta_decode_params_t;
 
 /*

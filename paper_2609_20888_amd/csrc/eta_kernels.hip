@@ -938,6 +938,12 @@ struct SplitArgs {
   int32_t* resc_out;         // [B][Hq] rescued block per head, or -1 (for the combine)
   int32_t* extra_union;      // [B][Hkv] rescued blocks outside the union (for the combine)
   int2* plan;                // [B][Hkv] (first split workgroup, splits) of each group
+  // one split per group (uniform plan, S = 1): the split writes the final
+  // results itself and no combine runs
+  const int32_t* head_cnt;   // [B][Hq][n_tiles] selected blocks per head per tile
+  void* out;                 // [B][Hq][D] in q's type
+  int32_t* counts;           // [B][Hq] attended tokens (may be nullptr)
+  int32_t* union_counts;     // [B][Hkv] union blocks (may be nullptr)
   Geom g;
   int q_dtype;
   float beta, offset_a;
@@ -1334,6 +1340,7 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
   }
   const int64_t hq0 = (int64_t)b * g.Hq + (int64_t)gh * G;
   const int64_t bg = (int64_t)b * g.Hkv + gh;
+  const bool single = uniform && S == 1;             // no partials, no combine
   const float scale = 1.0f / sqrtf((float)D);
   // The independent loads go out together: length, the first 256 tile counts,
   // thresholds, the rescue window's parts and the query elements (as raw bits,
@@ -1568,10 +1575,13 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
           for (int h = 0; h < G; ++h) in_union |= (resc_s[h] == rx_s[k][0] && rxw_s[h] != 0);
           extra += !in_union;
         }
-        a.extra_union[bg] = extra;
+        if (!single)
+          a.extra_union[bg] = extra;
+        else if (a.union_counts != nullptr)
+          a.union_counts[bg] = (int32_t)(UI_union + extra);
       }
       if (tid < G) {
-        a.resc_out[hq0 + tid] = resc_s[tid];
+        if (!single) a.resc_out[hq0 + tid] = resc_s[tid];
         if (resc_s[tid] >= 0) a.mask[(hq0 + tid) * g.ncap + resc_s[tid]] = 1;
       }
     }
@@ -1604,9 +1614,27 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
         o = fmaf(mrg_acc[k][h][i], wk, o);
       }
     }
-    const int64_t pidx = (int64_t)(first + s) * G + h;
-    a.part_acc[pidx * D + i] = o;
-    if (i == 0) a.part_ml[pidx] = make_float2(ms, L);
+    if (single) {          // the combine's result for one partial: acc / l
+      store_out(a.out, a.q_dtype, (hq0 + h) * D + i, L > 0.f ? o / L : 0.f);
+    } else {
+      const int64_t pidx = (int64_t)(first + s) * G + h;
+      a.part_acc[pidx * D + i] = o;
+      if (i == 0) a.part_ml[pidx] = make_float2(ms, L);
+    }
+  }
+  if constexpr (!DENSE) {
+    if (single && a.counts != nullptr) {
+      // attended tokens per head: its selected blocks (tile counts), its
+      // rescued block, the tail
+      for (int h = w; h < G; h += NW) {
+        int cnt = 0;
+        for (int t = lane; t < g.n_tiles; t += 64) cnt += a.head_cnt[(hq0 + h) * g.n_tiles + t];
+#pragma unroll
+        for (int o2 = 32; o2 > 0; o2 >>= 1) cnt += __shfl_xor(cnt, o2, 64);
+        if (lane == 0)
+          a.counts[hq0 + h] = (int32_t)(((int64_t)cnt + (resc_s[h] >= 0 ? 1 : 0)) * BS + ntail);
+      }
+    }
   }
 }
 
@@ -2020,11 +2048,12 @@ hipError_t launch_decode(const Geom& g, const DecodeCfg& c, int q_dtype, const v
   if (e != hipSuccess) return e;
   SplitArgs sp{q, k, v, seq_lens, predict ? ws.tau : tau, ws.ids, ws.tile_cnt, ws.part_ml,
                ws.part_acc, ws.resc_best, ws.resc_info, ws.wbits, mask, ws.resc_out,
-               ws.extra_union, ws.plan, g, q_dtype, c.beta, c.offset_a, c.self_ungated,
-               c.rescue_window, c.plan.S};
+               ws.extra_union, ws.plan, ws.head_cnt, out, counts, union_counts, g, q_dtype,
+               c.beta, c.offset_a, c.self_ungated, c.rescue_window, c.plan.S};
   e = with_hook(hook, ETA_KERNEL_SPLIT_DECODE, stream,
                 [&] { launch_split_impl<false>(g, c.plan, sp, stream); });
   if (e != hipSuccess) return e;
+  if (c.plan.S == 1) return hipSuccess;     // one split per group wrote the results
   CombineArgs ca{ws.part_ml, ws.part_acc, ws.head_cnt, ws.tile_cnt, seq_lens, ws.resc_out,
                  ws.extra_union, c.plan.S > 0 ? nullptr : ws.plan, counts, union_counts, out, g,
                  q_dtype, c.plan.S};
@@ -2069,11 +2098,11 @@ hipError_t launch_dense(const Geom& g, int S, int q_dtype, const void* q, const 
                         const void* v, const int32_t* seq_lens, void* out, const DecodeWs& ws,
                         hipStream_t stream, LaunchHook hook) {
   SplitArgs sp{q, k, v, seq_lens, nullptr, nullptr, nullptr, ws.part_ml, ws.part_acc,
-               nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, g, q_dtype, 0.f,
-               0.f, 0, 0, S};
+               nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, out,
+               nullptr, nullptr, g, q_dtype, 0.f, 0.f, 0, 0, S};
   hipError_t e = with_hook(hook, ETA_KERNEL_DENSE_SPLIT, stream,
                            [&] { launch_split_impl<true>(g, SplitPlan{S, S * g.B * g.Hkv}, sp, stream); });
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || S == 1) return e;     // one split per group wrote the output
   CombineArgs ca{ws.part_ml, ws.part_acc, nullptr, nullptr, seq_lens, nullptr, nullptr, nullptr,
                  nullptr, nullptr, out, g, q_dtype, S};
   return with_hook(hook, ETA_KERNEL_DENSE_COMBINE, stream,
