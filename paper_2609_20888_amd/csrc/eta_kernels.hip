@@ -1881,6 +1881,9 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
     av[k] = in ? accp[sidx * st * D] : 0.f;
     mloc = fmaxf(mloc, mv[k].x);
   }
+  // splits past the prefetched ones (more than 16 per thread): unrolled so that
+  // eight loads are in flight at a time instead of one round trip per split
+#pragma unroll 8
   for (int sidx = part + P * kCombPrefetch; sidx < S; sidx += P) mloc = fmaxf(mloc, ml[sidx * st].x);
   const float ms = block_reduce(mloc, true, red);
   float o = 0.f, L = 0.f;
@@ -1891,6 +1894,7 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
       o = fmaf(wk, av[k], o);
       L = fmaf(mv[k].y, wk, L);
     }
+#pragma unroll 8
     for (int sidx = part + P * kCombPrefetch; sidx < S; sidx += P) {
       const float2 e = ml[sidx * st];
       const float wk = e.x == kNegInf ? 0.f : __expf(e.x - ms);
