@@ -139,6 +139,15 @@ DECODE_CASES = {
     "splits_1": (dict(B=2, Hq=8, Hkv=2, d=128, block=64, seq_lens=[20000, 640],
                       planted={"frac": 0.05}, predictor=True, target_survival=0.15, seed=24),
                  dict(num_splits=1)),
+    # one sequence, one split per kv head: the split workgroup writes the output,
+    # counts and union counts itself (no combine); bf16 with a tail, and fp32 with
+    # every head rescued
+    "single_split_bf16_tail": (dict(B=1, Hq=8, Hkv=2, d=128, block=64, seq_lens=[20000],
+                                    planted={"frac": 0.05}, predictor=True, target_survival=0.15,
+                                    seed=26), dict(num_splits=1)),
+    "single_split_fp32_rescue": (dict(B=1, Hq=4, Hkv=1, d=64, block=64, seq_lens=[4000],
+                                      dtype=torch.float32, predictor=False, tau_const=50.0,
+                                      seed=27), dict(num_splits=1)),
     "splits_1024": (dict(B=1, Hq=8, Hkv=2, d=128, block=64, seq_lens=[20000],
                          planted={"frac": 0.05}, predictor=True, target_survival=0.15, seed=25),
                     dict(num_splits=1024)),
@@ -256,17 +265,21 @@ def test_dense_decode_matches_oracle():
                            predictor=False, tau_const=0.0, seed=d)
         dev = torch.device("cuda")
         sl = torch.tensor(lens, dtype=torch.int32, device=dev)
-        out = eta.dense_decode(wl.q.to(dev), wl.k.to(dev), wl.v.to(dev), sl, block_size=b)
-        torch.cuda.synchronize()
         q, k, v = oracle_inputs(wl)
         r = oracle.decode(q, k, v, lens, np.zeros((wl.B, 8)), block_size=b, screen_all=True,
                           gate_off=True)
-        o = out.float().cpu().numpy()
         tol = 2e-2 if dt == torch.bfloat16 else 1e-4
-        for bb in range(wl.B):
-            for h in range(8):
-                ref = r.o[bb, h]
-                assert np.max(np.abs(o[bb, h] - ref)) / np.max(np.abs(ref)) <= tol
+        # the library's split count, and one split per (sequence, kv head), where
+        # the split workgroup writes the output and no combine runs
+        for splits in (0, 1):
+            out = eta.dense_decode(wl.q.to(dev), wl.k.to(dev), wl.v.to(dev), sl, block_size=b,
+                                   num_splits=splits)
+            torch.cuda.synchronize()
+            o = out.float().cpu().numpy()
+            for bb in range(wl.B):
+                for h in range(8):
+                    ref = r.o[bb, h]
+                    assert np.max(np.abs(o[bb, h] - ref)) / np.max(np.abs(ref)) <= tol, (splits, bb, h)
 
 
 # ------------------------------------------------------------------ full-size workloads
