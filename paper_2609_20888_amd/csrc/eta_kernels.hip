@@ -150,29 +150,44 @@ __device__ __forceinline__ float wave_reduce(float x, Op op) {
 }
 
 // (largest value, smallest index among its lanes) over the wavefront, in every
-// lane: the max / min-index order is a total order, so the same steps as
-// wave_reduce pair every lane with every other
-__device__ __forceinline__ void wave_argmax(float& v, int& i) {
-  auto take = [&](float ov, int oi) {
-    if (ov > v || (ov == v && oi < i)) { v = ov; i = oi; }
+// lane, for N independent pairs: the max / min-index order is a total order, so
+// the same steps as wave_reduce pair every lane with every other; the N
+// butterflies run stage by stage, interleaved, instead of one after another.
+template <int N>
+__device__ __forceinline__ void wave_argmax_n(float (&v)[N], int (&i)[N]) {
+  auto take = [](float& cv, int& ci, float ov, int oi) {
+    if (ov > cv || (ov == cv && oi < ci)) { cv = ov; ci = oi; }
   };
-  take(dpp_mov<0xB1>(v), __float_as_int(dpp_mov<0xB1>(__int_as_float(i))));
-  take(dpp_mov<0x4E>(v), __float_as_int(dpp_mov<0x4E>(__int_as_float(i))));
-  take(dpp_mov<0x141>(v), __float_as_int(dpp_mov<0x141>(__int_as_float(i))));
-  take(dpp_mov<0x140>(v), __float_as_int(dpp_mov<0x140>(__int_as_float(i))));
-  {
-    const auto rv = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    const auto ri = __builtin_amdgcn_permlane16_swap((uint32_t)i, (uint32_t)i, false, false);
-    v = __uint_as_float(rv[0]);
-    i = (int)ri[0];
-    take(__uint_as_float(rv[1]), (int)ri[1]);
+#define ETA_ARGMAX_DPP(CTRL)                                                                    \
+  {                                                                                             \
+    float ov[N];                                                                                \
+    int oi[N];                                                                                  \
+    _Pragma("unroll") for (int n = 0; n < N; ++n) {                                             \
+      ov[n] = dpp_mov<CTRL>(v[n]);                                                              \
+      oi[n] = __float_as_int(dpp_mov<CTRL>(__int_as_float(i[n])));                              \
+    }                                                                                           \
+    _Pragma("unroll") for (int n = 0; n < N; ++n) take(v[n], i[n], ov[n], oi[n]);               \
   }
-  {
-    const auto rv = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    const auto ri = __builtin_amdgcn_permlane32_swap((uint32_t)i, (uint32_t)i, false, false);
-    v = __uint_as_float(rv[0]);
-    i = (int)ri[0];
-    take(__uint_as_float(rv[1]), (int)ri[1]);
+  ETA_ARGMAX_DPP(0xB1)
+  ETA_ARGMAX_DPP(0x4E)
+  ETA_ARGMAX_DPP(0x141)
+  ETA_ARGMAX_DPP(0x140)
+#undef ETA_ARGMAX_DPP
+#pragma unroll
+  for (int n = 0; n < N; ++n) {
+    const auto rv = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[n]), __float_as_uint(v[n]), false, false);
+    const auto ri = __builtin_amdgcn_permlane16_swap((uint32_t)i[n], (uint32_t)i[n], false, false);
+    v[n] = __uint_as_float(rv[0]);
+    i[n] = (int)ri[0];
+    take(v[n], i[n], __uint_as_float(rv[1]), (int)ri[1]);
+  }
+#pragma unroll
+  for (int n = 0; n < N; ++n) {
+    const auto rv = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[n]), __float_as_uint(v[n]), false, false);
+    const auto ri = __builtin_amdgcn_permlane32_swap((uint32_t)i[n], (uint32_t)i[n], false, false);
+    v[n] = __uint_as_float(rv[0]);
+    i[n] = (int)ri[0];
+    take(v[n], i[n], __uint_as_float(rv[1]), (int)ri[1]);
   }
 }
 
@@ -853,17 +868,23 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
     const int64_t Wn = (int64_t)a.c < N ? (int64_t)a.c : N;
     if (a.c > 0 && (int64_t)tile * kScreenTile < Wn) {
       const bool inw = j < Wn;
+      float bv[G];
+      int bi[G];
+      bool any[G];
 #pragma unroll
       for (int h = 0; h < G; ++h) {
-        const bool any = __ballot(inw && selected(j, bnd[h], h)) != 0ull;
+        any[h] = __ballot(inw && ((bits >> h) & 1u)) != 0ull;
         const bool ok = inw && !isnan(bnd[h]);
-        float bv = ok ? bnd[h] : kNegInf;
-        int bi = ok ? (int)j : 0x7fffffff;
-        wave_argmax(bv, bi);
-        if (lane == 0) {
+        bv[h] = ok ? bnd[h] : kNegInf;
+        bi[h] = ok ? (int)j : 0x7fffffff;
+      }
+      wave_argmax_n<G>(bv, bi);
+      if (lane == 0) {
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
           const int64_t e = (hq0 + h) * kRescueTiles + tile;
-          a.resc_best[e] = bv;
-          a.resc_info[e] = any ? kRescueAny : (bi == 0x7fffffff ? kRescueNone : bi);
+          a.resc_best[e] = bv[h];
+          a.resc_info[e] = any[h] ? kRescueAny : (bi[h] == 0x7fffffff ? kRescueNone : bi[h]);
         }
       }
       if (inw) a.wbits[bg * kMaxRescueWindow + j] = (uint8_t)bits;
