@@ -201,9 +201,17 @@ eta_status_t eta_predict_threshold(int32_t batch, int32_t num_q_heads, int32_t h
                                    int32_t q_dtype, const void* q, const float* W,
                                    const float* bias, float* tau_out, void* stream);
 
-/* Bytes of workspace eta_decode needs for this geometry and these params. */
-eta_status_t eta_decode_workspace_size(const eta_kv_desc_t* kv, const eta_decode_params_t* p,
-                                       size_t* bytes);
+/*
+ * Bytes of workspace eta_decode / eta_decode_predicted need for this geometry,
+ * these params and a summary of block capacity n_blk_cap (the n_blk_cap of the
+ * eta_summary_t the decode will read: the workspace holds per-block id lists
+ * and per-tile counts laid out with that capacity, and the default split count
+ * depends on it).  n_blk_cap is checked as eta_summary_t states
+ * (>= capacity_tokens / block_size, <= 131072): ETA_ERR_INVALID_ARG /
+ * ETA_ERR_UNSUPPORTED otherwise.  *bytes is host memory, written on success.
+ */
+eta_status_t eta_decode_workspace_size(const eta_kv_desc_t* kv, int64_t n_blk_cap,
+                                       const eta_decode_params_t* p, size_t* bytes);
 
 /*
  * eta_decode -- one ETA decode step (Alg. "Hardware-Aligned Block-Sparse
@@ -416,9 +424,10 @@ eta_status_t eta_dense_decode(const eta_kv_desc_t* kv, int32_t q_dtype, const vo
 /* Human-readable detail of the last failure on this host thread ("" if none). */
 const char* eta_last_error_string(void);
 
-/* ABI version of this header: 4 (2: eta_summary_t carries the record type;
+/* ABI version of this header: 5 (2: eta_summary_t carries the record type;
  * 3: ETA_DT_FP8 records; 4: eta_decode / eta_decode_predicted return the
- * per-(sequence, kv head) union counts). */
+ * per-(sequence, kv head) union counts; 5: eta_decode_workspace_size takes the
+ * summary's n_blk_cap). */
 int32_t eta_abi_version(void);
 
 /*

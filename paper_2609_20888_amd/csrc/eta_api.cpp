@@ -94,6 +94,22 @@ eta_status_t check_kv(const eta_kv_desc_t* kv, Geom* g) {
   return ETA_OK;
 }
 
+// The block capacity of the summary a call reads: the stride of the summary and
+// mask arrays, and what the decode workspace is laid out for (its id lists and
+// tile counts), so the workspace query and the decode take it from here alike.
+eta_status_t set_blk_cap(int64_t n_blk_cap, Geom* g) {
+  if (n_blk_cap < g->cap / g->BS)
+    return fail(ETA_ERR_INVALID_ARG, "n_blk_cap (%lld) < capacity_tokens / block_size (%lld)",
+                (long long)n_blk_cap, (long long)(g->cap / g->BS));
+  g->ncap = n_blk_cap;
+  g->n_tiles = (int)((g->ncap + kScreenTile - 1) / kScreenTile);
+  if (g->n_tiles < 1) g->n_tiles = 1;
+  if (g->n_tiles > kMaxTiles || n_blk_cap >= kMaxBlocks)
+    return fail(ETA_ERR_UNSUPPORTED, "n_blk_cap %lld exceeds %d screening tiles of %d blocks",
+                (long long)n_blk_cap, kMaxTiles, kScreenTile);
+  return ETA_OK;
+}
+
 eta_status_t check_summary(const eta_summary_t* s, Geom* g) {
   if (s == nullptr) return fail(ETA_ERR_INVALID_ARG, "summary descriptor is NULL");
   if (!s->mu || !s->sigma || !s->max_norm)
@@ -104,16 +120,7 @@ eta_status_t check_summary(const eta_summary_t* s, Geom* g) {
     return fail(ETA_ERR_INVALID_ARG,
                 "stat_dtype %d: summaries are ETA_DT_F32, ETA_DT_F16 or ETA_DT_FP8", s->stat_dtype);
   g->stat_dtype = s->stat_dtype;
-  if (s->n_blk_cap < g->cap / g->BS)
-    return fail(ETA_ERR_INVALID_ARG, "n_blk_cap (%lld) < capacity_tokens / block_size (%lld)",
-                (long long)s->n_blk_cap, (long long)(g->cap / g->BS));
-  g->ncap = s->n_blk_cap;
-  g->n_tiles = (int)((g->ncap + kScreenTile - 1) / kScreenTile);
-  if (g->n_tiles < 1) g->n_tiles = 1;
-  if (g->n_tiles > kMaxTiles || s->n_blk_cap >= kMaxBlocks)
-    return fail(ETA_ERR_UNSUPPORTED, "n_blk_cap %lld exceeds %d screening tiles of %d blocks",
-                (long long)s->n_blk_cap, kMaxTiles, kScreenTile);
-  return ETA_OK;
+  return set_blk_cap(s->n_blk_cap, g);
 }
 
 eta_status_t check_params(const eta_decode_params_t* p) {
@@ -290,7 +297,7 @@ extern "C" {
 
 const char* eta_last_error_string(void) { return g_err.c_str(); }
 
-int32_t eta_abi_version(void) { return 4; }
+int32_t eta_abi_version(void) { return 5; }
 
 static eta_status_t summaries_impl(const eta_kv_desc_t* kv, const void* k,
                                    const int32_t* prev_lens, const int32_t* seq_lens,
@@ -351,11 +358,12 @@ eta_status_t eta_predict_threshold(int32_t batch, int32_t num_q_heads, int32_t h
   return ok();
 }
 
-eta_status_t eta_decode_workspace_size(const eta_kv_desc_t* kv, const eta_decode_params_t* p,
-                                       size_t* bytes) {
+eta_status_t eta_decode_workspace_size(const eta_kv_desc_t* kv, int64_t n_blk_cap,
+                                       const eta_decode_params_t* p, size_t* bytes) {
   Geom g;
   eta_status_t st = check_kv(kv, &g);
   if (st) return st;
+  if ((st = set_blk_cap(n_blk_cap, &g))) return st;
   if ((st = check_params(p))) return st;
   if (!bytes) return fail(ETA_ERR_INVALID_ARG, "bytes is NULL");
   *bytes = decode_ws_bytes(g, plan_splits(g, p->num_splits), nullptr, nullptr);

@@ -106,7 +106,7 @@ def load_library(path: Optional[str] = None):
         "eta_build_block_summaries_envelope": [P(KvDesc), _vp, _vp, i32, P(SummaryDesc), _vp],
         "eta_update_block_summaries": [P(KvDesc), _vp, _vp, _vp, i32, i32, P(SummaryDesc), _vp],
         "eta_predict_threshold": [i32, i32, i32, i32, _vp, _vp, _vp, _vp, _vp],
-        "eta_decode_workspace_size": [P(KvDesc), P(DecodeParams), P(sz)],
+        "eta_decode_workspace_size": [P(KvDesc), ctypes.c_int64, P(DecodeParams), P(sz)],
         "eta_decode": [P(KvDesc), i32, _vp, _vp, _vp, _vp, P(SummaryDesc), _vp, P(DecodeParams),
                        _vp, _vp, _vp, _vp, _vp, sz, _vp],
         "eta_decode_predicted": [P(KvDesc), i32, _vp, _vp, _vp, _vp, P(SummaryDesc), _vp, _vp,
@@ -255,10 +255,11 @@ def predict_threshold(q: torch.Tensor, W: Optional[torch.Tensor], bias: torch.Te
     return out
 
 
-def decode_workspace_size(desc: KvDesc, params: DecodeParams) -> int:
+def decode_workspace_size(desc: KvDesc, n_blk_cap: int, params: DecodeParams) -> int:
+    """eta_decode_workspace_size for a summary of block capacity n_blk_cap."""
     n = ctypes.c_size_t()
-    _check(load_library().eta_decode_workspace_size(ctypes.byref(desc), ctypes.byref(params),
-                                                    ctypes.byref(n)))
+    _check(load_library().eta_decode_workspace_size(ctypes.byref(desc), int(n_blk_cap),
+                                                    ctypes.byref(params), ctypes.byref(n)))
     return n.value
 
 
@@ -303,7 +304,7 @@ def decode(q, k, v, seq_lens, summ: Summaries, tau, *, block_size: int,
         raise ValueError("K and V must share shape, strides and dtype")
     out, mask, counts, union_counts = _decode_outputs(q, k, summ, out, mask, counts, union_counts,
                                                       want_counts)
-    nbytes = decode_workspace_size(desc, p)
+    nbytes = decode_workspace_size(desc, summ.n_blk_cap, p)
     if workspace is None or workspace.numel() < nbytes:
         workspace = alloc_workspace(nbytes, q.device)
     sd = summ.desc()
@@ -326,7 +327,7 @@ def decode_predicted(q, k, v, seq_lens, summ: Summaries, W, bias, *, block_size:
         raise ValueError("K and V must share shape, strides and dtype")
     out, mask, counts, union_counts = _decode_outputs(q, k, summ, out, mask, counts, union_counts,
                                                       want_counts)
-    nbytes = decode_workspace_size(desc, p)
+    nbytes = decode_workspace_size(desc, summ.n_blk_cap, p)
     if workspace is None or workspace.numel() < nbytes:
         workspace = alloc_workspace(nbytes, q.device)
     sd = summ.desc()
@@ -383,7 +384,8 @@ class DecodeStep:
         self.union_counts = (torch.empty(B, k.shape[1], dtype=torch.int32, device=q.device)
                              if want_counts else None)
         self.tau = torch.empty(B, Hq, dtype=torch.float32, device=q.device)
-        self.workspace = alloc_workspace(decode_workspace_size(self.desc, self.params), q.device)
+        self.workspace = alloc_workspace(decode_workspace_size(self.desc, summ.n_blk_cap, self.params),
+                                         q.device)
         self._fn = load_library().eta_decode_predicted
         self._args = (ctypes.byref(self.desc), _dtype_code(q), _ptr(q), _ptr(k), _ptr(v),
                       _ptr(seq_lens), ctypes.byref(self.sdesc), _ptr(W), _ptr(bias),

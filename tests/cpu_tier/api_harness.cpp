@@ -217,22 +217,27 @@ static eta_summary_t summ(const eta_kv_desc_t& k, int st = ETA_DT_F32) {
   return s;
 }
 
-static void decode_geometry(int B, int Hq, int Hkv, int d, int b, int64_t cap, int splits) {
+// blk_extra: a summary holding that many blocks more than capacity_tokens /
+// block_size (n_blk_cap only has a lower bound).
+static void decode_geometry(int B, int Hq, int Hkv, int d, int b, int64_t cap, int splits,
+                            int64_t blk_extra = 0) {
   eta_kv_desc_t k = desc(B, Hq, Hkv, d, b, cap);
   eta_decode_params_t p = params(splits);
+  eta_summary_t s = summ(k);
+  s.n_blk_cap += blk_extra;
   size_t need = 0;
-  eta_status_t st = eta_decode_workspace_size(&k, &p, &need);
+  eta_status_t st = eta_decode_workspace_size(&k, s.n_blk_cap, &p, &need);
   CHECK(st == ETA_OK, "workspace size: %s", eta_last_error_string());
   if (st != ETA_OK) return;
   void* ws = std::aligned_alloc(256, (need + 255) / 256 * 256);
   g_ws = static_cast<const unsigned char*>(ws);
   g_ws_bytes = need;
-  eta_summary_t s = summ(k);
   const int before = launches;
   st = eta_decode(&k, ETA_DT_BF16, FAKE, FAKE, FAKE, (const int32_t*)FAKE, &s, (const float*)FAKE,
                   &p, FAKE, (uint8_t*)FAKE, nullptr, nullptr, ws, need, nullptr);
-  CHECK(st == ETA_OK && launches == before + 1, "decode B=%d %d/%d d=%d b=%d cap=%lld S=%d: %s", B,
-        Hq, Hkv, d, b, (long long)cap, splits, eta_last_error_string());
+  CHECK(st == ETA_OK && launches == before + 1,
+        "decode B=%d %d/%d d=%d b=%d cap=%lld +%lld blocks S=%d: %s", B, Hq, Hkv, d, b,
+        (long long)cap, (long long)blk_extra, splits, eta_last_error_string());
   st = eta_decode_predicted(&k, ETA_DT_BF16, FAKE, FAKE, FAKE, (const int32_t*)FAKE, &s,
                             (const float*)FAKE, (const float*)FAKE, &p, FAKE, (uint8_t*)FAKE,
                             nullptr, nullptr, nullptr, ws, need, nullptr);
@@ -273,7 +278,11 @@ static void invalid_calls() {
   eta_decode_params_t p = params();
   eta_summary_t s = summ(k);
   size_t need = 0;
-  eta_decode_workspace_size(&k, &p, &need);
+  eta_decode_workspace_size(&k, s.n_blk_cap, &p, &need);
+  // a block capacity below capacity_tokens / block_size is refused by the query too
+  size_t none = 0;
+  CHECK(eta_decode_workspace_size(&k, s.n_blk_cap - 1, &p, &none) == ETA_ERR_INVALID_ARG &&
+            none == 0, "workspace query took n_blk_cap < capacity / block_size");
   void* ws = std::aligned_alloc(256, (need + 255) / 256 * 256);
   const int before = launches;
   auto dec = [&](const eta_kv_desc_t& kk, const eta_decode_params_t& pp, const eta_summary_t& ss,
@@ -347,7 +356,7 @@ static void other_entry_points() {
   eta_build_block_summaries(&k, FAKE, (const int32_t*)FAKE, &s, nullptr);
   eta_kernel_time_t t[ETA_KERNEL_KINDS];
   CHECK(eta_profile_end(t) == ETA_OK && t[ETA_KERNEL_SUMMARIES].launches == 1, "profile end");
-  CHECK(eta_abi_version() >= 4, "abi version");
+  CHECK(eta_abi_version() == 5, "abi version");
 }
 
 int main() {
@@ -366,6 +375,12 @@ int main() {
   decode_geometry(1, 16, 4, 128, 64, (int64_t)2048 * 64 * 64, 0);   // 2048 screening tiles
   decode_geometry(256, 32, 8, 128, 64, 65536, 0);                   // 2048 groups: uniform plan
   decode_geometry(32, 32, 8, 128, 64, 65536, 0);                    // proportional, 4096 counts
+  // summaries larger than the cache: one block past, a tile past, and T < b with a
+  // one-block summary (capacity_tokens / block_size = 0)
+  for (int B : {1, 8})
+    for (int64_t cap : {1, 63, 64, 4097})
+      for (int S : {0, 1})
+        for (int64_t extra : {1, 65}) decode_geometry(B, 16, 4, 128, 64, cap, S, extra);
   invalid_calls();
   other_entry_points();
   if (failures) {

@@ -23,7 +23,7 @@ def test_header_declarations_are_all_exported(lib):
     assert declared == set(eta.EXPORTS), declared ^ set(eta.EXPORTS)
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.eta_abi_version() == 4
+    assert lib.eta_abi_version() == 5
 
 
 def good_desc(**kw):
@@ -34,9 +34,12 @@ def good_desc(**kw):
     return eta.KvDesc(**d)
 
 
-def ws_size(lib, desc, params):
+def ws_size(lib, desc, params, n_blk_cap=None):
+    if n_blk_cap is None:
+        n_blk_cap = max(desc.capacity_tokens, 0) // max(desc.block_size, 1)
     n = ctypes.c_size_t()
-    st = lib.eta_decode_workspace_size(ctypes.byref(desc), ctypes.byref(params), ctypes.byref(n))
+    st = lib.eta_decode_workspace_size(ctypes.byref(desc), n_blk_cap, ctypes.byref(params),
+                                       ctypes.byref(n))
     return st, n.value
 
 
@@ -48,6 +51,14 @@ def test_workspace_size_valid_and_monotone(lib):
     assert st == eta.ETA_OK and n2 > n1
     st, n3 = ws_size(lib, good_desc(), eta.decode_params(num_splits=512))
     assert st == eta.ETA_OK and n3 > n1
+    # the workspace follows the summary's block capacity, which may exceed the cache's
+    st, n4 = ws_size(lib, good_desc(), p, n_blk_cap=4096 // 64 + 64)
+    assert st == eta.ETA_OK and n4 > n1
+    st, n5 = ws_size(lib, good_desc(capacity_tokens=52), p, n_blk_cap=1)
+    st0, n6 = ws_size(lib, good_desc(capacity_tokens=52), p, n_blk_cap=0)
+    assert st == st0 == eta.ETA_OK and n5 > n6
+    assert ws_size(lib, good_desc(), p, n_blk_cap=4096 // 64 - 1)[0] == eta.ETA_ERR_INVALID_ARG
+    assert ws_size(lib, good_desc(), p, n_blk_cap=131073)[0] == eta.ETA_ERR_UNSUPPORTED
 
 
 @pytest.mark.parametrize("kw,code", [

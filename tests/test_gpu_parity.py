@@ -450,3 +450,44 @@ def test_decode_step_replays_in_a_hip_graph_like_eager(predictor):
         for name, x, y in zip(("out", "mask", "counts", "tau"), got, ref):
             assert torch.equal(x, y), (r, name)
     say(f"[gpu] graph replays of the decode step match eager (predictor={predictor})")
+
+
+# ------------------------------------------------------------------ seeded random geometries
+
+def _random_geometry(seed: int):
+    """One seeded small geometry: group size, head dim, block size, K/V type, ragged
+    lengths (some below one block, some with a tail), predictor or constant
+    thresholds, rescue window, pinned blocks, split count."""
+    rng = np.random.default_rng(1000 + seed)
+    G = int(rng.choice([1, 2, 4, 8]))
+    Hkv = int(rng.choice([1, 2])) if G < 8 else 1
+    d = int(rng.choice([64, 128]))
+    block = int(rng.choice([64, 128]))
+    B = int(rng.integers(1, 4))
+    lens = [int(rng.integers(0, 40 * block)) for _ in range(B)]
+    if rng.random() < 0.3:
+        lens[0] = int(rng.integers(0, block))               # shorter than one block
+    dtype = torch.float32 if rng.random() < 0.25 else torch.bfloat16
+    predictor = bool(rng.random() < 0.6)
+    wkw = dict(B=B, Hq=G * Hkv, Hkv=Hkv, d=d, block=block, seq_lens=lens, dtype=dtype,
+               planted={"frac": 0.05}, predictor=predictor, seed=2000 + seed,
+               rescue_window=int(rng.choice([0, 3, 64, 256])), lwb=int(rng.choice([0, 0, 2])))
+    if predictor:
+        wkw["target_survival"] = float(rng.choice([0.02, 0.1, 0.3]))
+    else:
+        wkw["tau_const"] = float(rng.choice([0.5, 1.5, 3.0]))
+    rkw = dict(num_splits=int(rng.choice([0, 0, 1, 3, 17])))
+    return wkw, rkw
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_decode_random_geometries(seed):
+    wkw, rkw = _random_geometry(seed)
+    say(f"[gpu] random geometry {seed}: {wkw} {rkw}")
+    wl = make_workload(**wkw)
+    np_in = oracle_inputs(wl)
+    calibrate_bias(wl, np_in)
+    g = run_gpu(wl, **rkw)
+    orc, tau_o = run_oracle(wl, np_in)
+    stats = compare(wl, g, orc, tau_o, np_inputs=np_in, union_counts=g.union_counts)
+    assert stats["compared"] == wl.B * wl.Hq

@@ -68,7 +68,7 @@ def test_noalloc_rejects_calls_beyond_the_scratch():
                       stride_h=4096 * 128, stride_t=128)
     summ = eta.SummaryDesc(mu=FAKE, sigma=FAKE, max_norm=FAKE, n_blk_cap=64)
     p = eta.decode_params(num_splits=1024)
-    need = eta.decode_workspace_size(desc, p)
+    need = eta.decode_workspace_size(desc, summ.n_blk_cap, p)
     assert need > eta.NOALLOC_SCRATCH_BYTES
     st = lib.eta_decode_predicted_noalloc(ctypes.byref(desc), eta.ETA_DT_BF16, FAKE, FAKE, FAKE,
                                           FAKE, ctypes.byref(summ), FAKE, FAKE, ctypes.byref(p),
