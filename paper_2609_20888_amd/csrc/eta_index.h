@@ -29,7 +29,8 @@ ETA_HD int group_splits(int work, int64_t total_work, int W, int BG) {
 }
 
 // In place: v[0..n) -> exclusive prefix sums; returns the total (callers keep it
-// in v[n]).
+// in v[n]).  The split kernel computes the same prefixes with block-wide scans
+// (integer sums, so equal whatever the order); this is their definition.
 ETA_HD int exclusive_prefix(int* v, int n) {
   int acc = 0;
   for (int x = 0; x < n; ++x) {

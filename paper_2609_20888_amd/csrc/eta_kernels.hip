@@ -1294,8 +1294,8 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
   __shared__ uint8_t item_bits[kItemChunk];
   __shared__ uint8_t item_sub[kItemChunk];
   __shared__ int grp_s[DENSE ? 1 : kPropMaxGroups + 1];  // proportional: first split of each group
-  __shared__ int cnt_s[DENSE ? 1 : kPropMaxCounts];      // proportional: every tile count
-  __shared__ int who_s[2];                               // proportional: group, split index
+  __shared__ int cnt_s[DENSE ? 1 : kPropMaxCounts + 1];  // proportional: prefix of every tile count
+  __shared__ int wtail_s[NW];
   __shared__ float rbest_s[DENSE ? 1 : G][kRescueTiles];
   __shared__ int rinfo_s[DENSE ? 1 : G][kRescueTiles];
   __shared__ int resc_s[G];                              // rescued block per head, or -1
@@ -1310,7 +1310,9 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
   constexpr int SPB = BF ? BS / 64 : 1;
   const bool uniform = DENSE || a.S_uniform > 0;
   int b, gh, s, S, first;
-  const int32_t* tc;
+  const int32_t* tc = nullptr;     // uniform: the group's tile counts
+  const int* pref = pref_s;        // exclusive prefix of the group's tile counts ...
+  int pbase = 0;                   // ... offset by pbase
   if (uniform) {
     s = blockIdx.x;
     gh = blockIdx.y;
@@ -1318,46 +1320,111 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
     S = gridDim.x;
     first = (b * g.Hkv + gh) * S;
     tc = a.tile_cnt + ((int64_t)b * g.Hkv + gh) * g.n_tiles;
-  } else {
-    const int BG = g.B * g.Hkv, nc = BG * g.n_tiles, W = gridDim.x;
-    for (int i = tid; i < nc; i += NT) cnt_s[i] = a.tile_cnt[i];
-    __syncthreads();
-    // each group's work: its union's tiles, plus one for a tail
-    int64_t mine = 0;
-    for (int x = tid; x < BG; x += NT) {
-      int u = 0;
-      for (int t = 0; t < g.n_tiles; ++t) u += cnt_s[x * g.n_tiles + t];
-      const int work = group_work(u, SPB, clamp_len(a.seq_lens, x / g.Hkv, g.cap), BS);
-      grp_s[x] = work;
-      mine += work;
-    }
-    // total work (integer sums: any order)
-    for (int o = 32; o > 0; o >>= 1) mine += __shfl_xor(mine, o, 64);
-    if (lane == 0) wsum_s[w] = (int)mine;
-    __syncthreads();
-    int64_t UT = 0;
+  } else if constexpr (!DENSE) {
+    // Every tile count and every length in one round trip.  One block scan of
+    // the counts (groups in order, each group's tiles in order) gives each
+    // group's union tiles and, offset by the group's start, its own tile prefix;
+    // a second scan over the groups' split counts gives each group's first split.
+    const int BG = g.B * g.Hkv, nct = g.n_tiles, nc = BG * nct, W = gridDim.x;
+    constexpr int CPT = kPropMaxCounts / NT;   // counts per thread, contiguous
+    constexpr int GPT = kPropMaxGroups / NT;   // groups per thread, contiguous
+    static_assert(CPT * NT == kPropMaxCounts && GPT * NT == kPropMaxGroups, "whole shares");
+    // (unconditional loads from clamped indexes, masked afterwards: a load under a
+    // branch is waited for inside the branch, one round trip each)
+    int cv[CPT], tails[GPT];
 #pragma unroll
-    for (int k = 0; k < NW; ++k) UT += wsum_s[k];
-    __syncthreads();
-    // splits per group, then their exclusive prefix (one thread: BG <= 1024)
-    for (int x = tid; x < BG; x += NT) grp_s[x] = group_splits(grp_s[x], UT, W, BG);
-    __syncthreads();
-    if (tid == 0) {
-      grp_s[BG] = exclusive_prefix(grp_s, BG);
-      // this workgroup's group: the last one starting at or before it
-      const int me = (int)blockIdx.x, gi = find_group(grp_s, BG, me);
-      who_s[0] = gi;
-      who_s[1] = gi >= 0 ? me - grp_s[gi] : 0;
+    for (int k = 0; k < CPT; ++k) {
+      const int i = tid * CPT + k;
+      cv[k] = a.tile_cnt[i < nc ? i : 0];
     }
+#pragma unroll
+    for (int r = 0; r < GPT; ++r) {
+      const int x = tid * GPT + r;
+      tails[r] = a.seq_lens[(x < BG ? x : 0) / g.Hkv];
+    }
+    // every value is needed here, so none of the loads is moved into a branch
+#pragma unroll
+    for (int r = 0; r < GPT; ++r) asm volatile("" ::"v"(tails[r]));
+#pragma unroll
+    for (int k = 0; k < CPT; ++k)
+      if (tid * CPT + k >= nc) cv[k] = 0;
+    int ntl = 0;
+#pragma unroll
+    for (int r = 0; r < GPT; ++r) {
+      const int x = tid * GPT + r;
+      const int64_t len = tails[r] < 0 ? 0 : (tails[r] > g.cap ? g.cap : tails[r]);
+      // a group's work is its union's tiles plus one for a partial tail
+      tails[r] = x < BG ? group_work(0, SPB, len, BS) : 0;
+      ntl += tails[r];
+    }
+    int run = 0;
+#pragma unroll
+    for (int k = 0; k < CPT; ++k) {
+      const int v = cv[k];
+      cv[k] = run;
+      run += v;
+    }
+    int incl = run;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += y;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) ntl += __shfl_xor(ntl, o, 64);
+    if (lane == 63) wsum_s[w] = incl;
+    if (lane == 0) wtail_s[w] = ntl;
     __syncthreads();
-    const int bgi = who_s[0];
+    int woff = 0, tot = 0, ntails = 0;
+#pragma unroll
+    for (int k = 0; k < NW; ++k) {
+      woff += k < w ? wsum_s[k] : 0;
+      tot += wsum_s[k];
+      ntails += wtail_s[k];
+    }
+    const int ex = woff + incl - run;
+#pragma unroll
+    for (int k = 0; k < CPT; ++k) cnt_s[tid * CPT + k] = ex + cv[k];
+    if (tid == NT - 1) cnt_s[kPropMaxCounts] = ex + run;
+    __syncthreads();
+    // splits per group (integer work: the total does not depend on the order)
+    const int64_t UT = (int64_t)tot * SPB + ntails;
+    int sp[GPT], run2 = 0;
+#pragma unroll
+    for (int r = 0; r < GPT; ++r) {
+      const int x = tid * GPT + r;
+      const int v = x < BG ? group_splits((cnt_s[(x + 1) * nct] - cnt_s[x * nct]) * SPB + tails[r],
+                                          UT, W, BG)
+                           : 0;
+      sp[r] = run2;
+      run2 += v;
+    }
+    int incl2 = run2;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl2, o, 64);
+      if (lane >= o) incl2 += y;
+    }
+    if (lane == 63) wsum_s[w] = incl2;     // every read of the first scan's sums is done
+    __syncthreads();
+    int woff2 = 0;
+#pragma unroll
+    for (int k = 0; k < NW; ++k) woff2 += k < w ? wsum_s[k] : 0;
+    const int ex2 = woff2 + incl2 - run2;
+#pragma unroll
+    for (int r = 0; r < GPT; ++r) grp_s[tid * GPT + r] = ex2 + sp[r];
+    if (tid == NT - 1) grp_s[kPropMaxGroups] = ex2 + run2;
+    __syncthreads();
+    // this workgroup's group: the last one starting at or before it
+    const int me = (int)blockIdx.x, bgi = find_group(grp_s, BG, me);
     if (bgi < 0) return;             // workgroups past the allocation (uniform exit)
     b = bgi / g.Hkv;
     gh = bgi % g.Hkv;
-    s = who_s[1];
     first = grp_s[bgi];
+    s = me - first;
     S = grp_s[bgi + 1] - first;
-    tc = cnt_s + (int64_t)bgi * g.n_tiles;
+    pref = cnt_s + bgi * nct;
+    pbase = pref[0];
   }
   const int64_t hq0 = (int64_t)b * g.Hq + (int64_t)gh * G;
   const int64_t bg = (int64_t)b * g.Hkv + gh;
@@ -1365,21 +1432,18 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
   const float scale = 1.0f / sqrtf((float)D);
   // The independent loads go out together: length, the first 256 tile counts,
   // thresholds, the rescue window's parts and the query elements (as raw bits,
-  // converted afterwards, so that no conversion waits on its own load).
-  const int64_t T = clamp_len(a.seq_lens, b, g.cap);
-  const int tc0 = (!DENSE && tid < g.n_tiles) ? tc[tid] : 0;
+  // converted afterwards, so that no conversion waits on its own load).  The
+  // rescue parts of every window tile are read (those past the window are never
+  // used), so that no load waits for the length.
+  int32_t t_raw = a.seq_lens[b];
+  const int tc0 = (!DENSE && uniform && tid < g.n_tiles) ? tc[tid] : 0;
   const float tau_in = (!DENSE && tid < G) ? a.tau[hq0 + tid] : 0.f;
-  const int64_t N = T / BS;
-  const int64_t Wn = (int64_t)a.c < N ? (int64_t)a.c : N;
-  const int nwt = (int)((Wn + kScreenTile - 1) / kScreenTile);    // window tiles
+  float rb_in = 0.f;
+  int ri_in = 0;
   if constexpr (!DENSE) {
-    if (tid < G * kRescueTiles) {
-      const int h = tid / kRescueTiles, t = tid % kRescueTiles;
-      if (t < nwt) {
-        rbest_s[h][t] = a.resc_best[(hq0 + h) * kRescueTiles + t];
-        rinfo_s[h][t] = a.resc_info[(hq0 + h) * kRescueTiles + t];
-      }
-    }
+    const int e = tid < G * kRescueTiles ? tid : 0;
+    rb_in = a.resc_best[hq0 * kRescueTiles + e];
+    ri_in = a.resc_info[hq0 * kRescueTiles + e];
   }
   constexpr int QE = BF ? NQ * 4 * D : G * D;          // staged query elements
   constexpr int QR = (QE + NT - 1) / NT;
@@ -1391,6 +1455,21 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
     const int64_t src = (hq0 + ((idx < QE && hh < G) ? hh : 0)) * D + i;
     qraw[r] = a.q_dtype == ETA_DT_F32 ? reinterpret_cast<const uint32_t*>(a.q)[src]
                                       : (uint32_t)reinterpret_cast<const uint16_t*>(a.q)[src];
+  }
+  // the length and the rescue parts are taken here, after every load has been
+  // issued (a uniform load is otherwise moved to a scalar register, with its
+  // wait, right where it is issued)
+  asm volatile("" : "+v"(t_raw) : "v"(rb_in), "v"(ri_in));
+  t_raw = __builtin_amdgcn_readfirstlane(t_raw);
+  const int64_t T = t_raw < 0 ? 0 : (t_raw > g.cap ? g.cap : (int64_t)t_raw);
+  const int64_t N = T / BS;
+  const int64_t Wn = (int64_t)a.c < N ? (int64_t)a.c : N;
+  const int nwt = (int)((Wn + kScreenTile - 1) / kScreenTile);    // window tiles
+  if constexpr (!DENSE) {
+    if (tid < G * kRescueTiles) {
+      rbest_s[tid / kRescueTiles][tid % kRescueTiles] = rb_in;
+      rinfo_s[tid / kRescueTiles][tid % kRescueTiles] = ri_in;
+    }
   }
   const int ntail = (int)(T - N * BS);
 #pragma unroll
@@ -1425,6 +1504,8 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
   int64_t UI;                // items (blocks) in the list
   if constexpr (DENSE) {
     UI = N;
+  } else if (!uniform) {
+    UI = pref[g.n_tiles] - pbase;   // the plan's scan holds the group's prefix
   } else {
     // exclusive prefix sum of the per-tile union counts, NT tiles at a time
     int carry = 0;
@@ -1544,7 +1625,7 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
       bo = (uint8_t)rx_s[it - UI_union][1];
     } else {
       int tl, slot;
-      resolve_item(pref_s, g.n_tiles, it, &tl, &slot);
+      resolve_item(pref, g.n_tiles, it + pbase, &tl, &slot);
       const uint32_t id = (uint32_t)a.ids[bg * g.ncap + (int64_t)tl * kScreenTile + slot];
       jo = (int32_t)(id & kIdMask);
       bo = (uint8_t)(id >> 24);
