@@ -189,16 +189,17 @@ def measure_compact(torch, np, eta, dev, wl, steps, flush, stat_dtype):
     sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
     summ = eta.build_block_summaries(wl.k, sl, wl.block, num_q_heads=wl.Hq, stat_dtype=stat_dtype)
     nblk = [t // wl.block for t in wl.seq_lens]
+    W_h = wl.W_heads                    # head-major, as the library takes it
     if wl.W is not None:
         bounds = eta.block_bounds(wl.q, sl, summ, wl.k, block_size=wl.block, z=wl.z).cpu().numpy()
-        qW = eta.predict_threshold(wl.q, wl.W, torch.zeros(wl.Hq, device=dev)).cpu().numpy()
+        qW = eta.predict_threshold(wl.q, W_h, torch.zeros(wl.Hq, device=dev)).cpu().numpy()
         bias = torch.as_tensor(place_bias(bounds, nblk, qW.astype(np.float64), wl.target_survival,
                                           wl.a), device=dev)
     else:
         bias = wl.bias.to(dev)
     p = eta.decode_params(beta=wl.beta, z=wl.z, offset_a=wl.a, rescue_window=wl.rescue_window,
                           lwb=wl.lwb)
-    st = eta.DecodeStep(wl.q, wl.k, wl.v, sl, summ, wl.W, bias, block_size=wl.block, params=p)
+    st = eta.DecodeStep(wl.q, wl.k, wl.v, sl, summ, W_h, bias, block_size=wl.block, params=p)
     warm = time_warm(torch, st.run, steps, warmup=10)
     cold = time_cold(torch, st.run, max(10, steps // 2), flush)[0]
     torch.cuda.synchronize()
@@ -220,16 +221,17 @@ def measure_config(torch, np, eta, dev, wl, steps, flush, compact=False):
     sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
     summ = eta.build_block_summaries(wl.k, sl, wl.block, num_q_heads=wl.Hq)
     nblk = [t // wl.block for t in wl.seq_lens]
+    W_h = wl.W_heads                    # head-major, as the library takes it
     if wl.W is not None:
         bounds = eta.block_bounds(wl.q, sl, summ, wl.k, block_size=wl.block, z=wl.z).cpu().numpy()
-        qW = eta.predict_threshold(wl.q, wl.W, torch.zeros(wl.Hq, device=dev)).cpu().numpy()
+        qW = eta.predict_threshold(wl.q, W_h, torch.zeros(wl.Hq, device=dev)).cpu().numpy()
         bias = torch.as_tensor(place_bias(bounds, nblk, qW.astype(np.float64), wl.target_survival,
                                           wl.a), device=dev)
     else:
         bias = wl.bias.to(dev)
     p = eta.decode_params(beta=wl.beta, z=wl.z, offset_a=wl.a, rescue_window=wl.rescue_window,
                           lwb=wl.lwb)
-    st = eta.DecodeStep(wl.q, wl.k, wl.v, sl, summ, wl.W, bias, block_size=wl.block, params=p)
+    st = eta.DecodeStep(wl.q, wl.k, wl.v, sl, summ, W_h, bias, block_size=wl.block, params=p)
     warm = time_warm(torch, st.run, steps, warmup=10)
     cold, c10, c50, c90 = time_cold(torch, st.run, max(10, steps // 2), flush)
     union = int(st.union_counts.sum())
@@ -302,7 +304,7 @@ def main():
     wl = config4(device=dev, survival=PRIMARY_SURVIVAL)
     B, Hq, Hkv, d, bs = wl.B, wl.Hq, wl.Hkv, wl.d, wl.block
     sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
-    q, k, v, W = wl.q, wl.k, wl.v, wl.W
+    q, k, v, W = wl.q, wl.k, wl.v, wl.W_heads   # W head-major, as the library takes it
     e = 2  # bf16 bytes
     Ncap = wl.n_blk_cap
     torch.cuda.synchronize()

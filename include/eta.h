@@ -100,8 +100,10 @@ typedef struct {
  * ETA_DT_FP8 stores mu and sigma as 8-bit E4M3 codes (the FP8 metadata of Sec.
  * "Limitations and Conclusion"): nearest-even rounding of the fp32 statistic,
  * magnitudes from 464 saturated to 448; a quarter of the fp32 record bytes.
- * n_blk_cap >= capacity_tokens / block_size, n_blk_cap < 2^24 and
- * n_blk_cap <= 131072 (2048 screening tiles of 64 blocks).
+ * n_blk_cap >= max(1, capacity_tokens / block_size), n_blk_cap < 2^24 and
+ * n_blk_cap <= 131072 (2048 screening tiles of 64 blocks).  A multiple of 4
+ * lets screening read four blocks' records per load (any other value is
+ * accepted and read one record at a time).
  */
 typedef struct {
   void* mu;
@@ -186,13 +188,16 @@ eta_status_t eta_update_block_summaries(const eta_kv_desc_t* kv, const void* k,
                                         const eta_summary_t* out, void* stream);
 
 /*
- * eta_predict_threshold -- Eq. (tau_pred): tau[b][h] = sum_j qbar[b][j] W[j][h] + bias[h],
+ * eta_predict_threshold -- Eq. (tau_pred): tau[b][h] = sum_j qbar[b][j] W[h][j] + bias[h],
  * qbar[b] the concatenation of the num_q_heads query heads of sequence b
  * (post-RoPE queries).  W == NULL gives frozen per-head constants tau[b][h] =
  * bias[h] (Sec. "Runtime Contextuality and Domain-Specific Offline
  * Calibration").
  *   q        [batch][num_q_heads][head_dim], q_dtype (eta_dtype_t)
- *   W        fp32 [num_q_heads*head_dim][num_q_heads] row-major, or NULL
+ *   W        fp32 [num_q_heads][num_q_heads*head_dim] row-major (head-major: row h holds
+ *            the weights of head h's threshold, i.e. the (H d) x H matrix of Eq.
+ *            (tau_pred) transposed, so that a workgroup predicting a few heads reads
+ *            only their rows), or NULL
  *   bias     fp32 [num_q_heads] (required)
  *   tau_out  fp32 [batch][num_q_heads]
  * fp32 accumulation.  head_dim here may be any value in [1, 1024].
@@ -207,7 +212,7 @@ eta_status_t eta_predict_threshold(int32_t batch, int32_t num_q_heads, int32_t h
  * eta_summary_t the decode will read: the workspace holds per-block id lists
  * and per-tile counts laid out with that capacity, and the default split count
  * depends on it).  n_blk_cap is checked as eta_summary_t states
- * (>= capacity_tokens / block_size, <= 131072): ETA_ERR_INVALID_ARG /
+ * (>= max(1, capacity_tokens / block_size), <= 131072): ETA_ERR_INVALID_ARG /
  * ETA_ERR_UNSUPPORTED otherwise.  *bytes is host memory, written on success.
  */
 eta_status_t eta_decode_workspace_size(const eta_kv_desc_t* kv, int64_t n_blk_cap,
@@ -427,7 +432,7 @@ const char* eta_last_error_string(void);
 /* ABI version of this header: 5 (2: eta_summary_t carries the record type;
  * 3: ETA_DT_FP8 records; 4: eta_decode / eta_decode_predicted return the
  * per-(sequence, kv head) union counts; 5: eta_decode_workspace_size takes the
- * summary's n_blk_cap). */
+ * summary's n_blk_cap, which is at least 1). */
 int32_t eta_abi_version(void);
 
 /*

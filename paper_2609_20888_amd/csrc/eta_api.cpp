@@ -98,6 +98,7 @@ eta_status_t check_kv(const eta_kv_desc_t* kv, Geom* g) {
 // mask arrays, and what the decode workspace is laid out for (its id lists and
 // tile counts), so the workspace query and the decode take it from here alike.
 eta_status_t set_blk_cap(int64_t n_blk_cap, Geom* g) {
+  if (n_blk_cap < 1) return fail(ETA_ERR_INVALID_ARG, "n_blk_cap must be >= 1 (got %lld)", (long long)n_blk_cap);
   if (n_blk_cap < g->cap / g->BS)
     return fail(ETA_ERR_INVALID_ARG, "n_blk_cap (%lld) < capacity_tokens / block_size (%lld)",
                 (long long)n_blk_cap, (long long)(g->cap / g->BS));

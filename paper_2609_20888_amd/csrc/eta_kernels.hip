@@ -71,6 +71,26 @@ __device__ __forceinline__ float stat_f32(uint8_t x) {
   return __builtin_amdgcn_cvt_f32_fp8((int)x, 0);
 }
 
+// Four consecutive records of one coordinate row (one 16-, 8- or 4-byte load),
+// and their fp32 values (the same conversions as stat_f32).
+template <typename ST>
+struct alignas(4 * sizeof(ST)) Rec4 {
+  ST v[4];
+};
+template <typename ST>
+__device__ __forceinline__ void rec4_f32(const Rec4<ST>& r, float (&f)[4]) {
+  if constexpr (sizeof(ST) == 1) {
+    const int word = (int)__builtin_bit_cast(uint32_t, r);
+    f[0] = __builtin_amdgcn_cvt_f32_fp8(word, 0);
+    f[1] = __builtin_amdgcn_cvt_f32_fp8(word, 1);
+    f[2] = __builtin_amdgcn_cvt_f32_fp8(word, 2);
+    f[3] = __builtin_amdgcn_cvt_f32_fp8(word, 3);
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) f[e] = stat_f32(r.v[e]);
+  }
+}
+
 // Element access for the two storage types: float and bf16 (raw uint16 bits).
 template <typename T>
 struct Elem;
@@ -476,90 +496,104 @@ __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ 
 
 // ---------------------------------------------------------------- predictor
 //
-// tau[b][h] = sum_j qbar[b][j] W[j][h] + bias[h] with one fixed summation
-// order shared by the stand-alone predictor and the screening kernel's fused
-// prediction, so both give bit-identical thresholds: thread t of a 256-thread
-// workgroup accumulates rows j = t, t + 256, ... (independent loads, all in
-// flight); each wavefront reduces by butterfly; the four wavefront sums are
+// tau[b][h] = sum_j qbar[b][j] W[h][j] + bias[h].  W is head-major: row h holds
+// the Hq d weights of head h's threshold (the predictor's (Hq d) x Hq matrix
+// transposed), so a workgroup that predicts a few heads reads those heads' rows
+// and nothing else.  One fixed summation order is shared by the stand-alone
+// predictor and the screening kernel's fused prediction, so both give
+// bit-identical thresholds: thread t of a 256-thread workgroup accumulates rows
+// j = 1024 p + 4 t + e (passes p = 0, 1, ..., e = 0..3 within each, in that
+// order); each wavefront reduces by butterfly; the four wavefront sums are
 // added in order; the bias is added last.
 
 constexpr int kPredThreads = 256;
-constexpr int kPredCols = 4;     // columns per stand-alone predictor workgroup
-
-// Per-thread partial sums of columns h0 .. h0 + ncols - 1 (ncols <= NC).
-// The first kPredRows rows of each thread are loaded into registers by
+constexpr int kPredCols = 4;                    // heads per stand-alone predictor workgroup
+constexpr int kPredStep = 4 * kPredThreads;     // rows per pass
+// The first kPredPass passes of each thread are loaded into registers by
 // pred_load (so a caller can issue them ahead of other loads) and consumed by
 // pred_sum, which then continues over any further rows in the same order.
-constexpr int kPredRows = 8;
+constexpr int kPredPass = 2;
 
 template <int NC>
 struct PredRows {
-  uint32_t x[kPredRows];     // raw query bits (fp32, or bf16 in the low half)
-  float w[kPredRows][NC];
+  uint32_t x[kPredPass][4];   // raw query bits (fp32, or bf16 in the low half)
+  float w[kPredPass][NC][4];
 };
 
 __device__ __forceinline__ float pred_x(uint32_t raw, int q_dtype) {
   return q_dtype == ETA_DT_F32 ? __uint_as_float(raw) : __uint_as_float(raw << 16);
 }
 
-// Loads rows j0 + threadIdx.x + kPredThreads k (k < kPredRows), all
-// unconditional (indexes clamped, the unused values zeroed in pred_fma) so that
-// they are in flight together; the query is kept as raw bits until pred_fma so
-// that no conversion waits for its load.  VEC: the NC columns are whole,
-// 16-byte aligned groups of four (ncols == NC, h0 and Hq multiples of 4).
+// Loads passes p0 .. p0 + kPredPass - 1 of this thread: rows 1024 p + 4 t + e of
+// the query and of heads h0 .. h0 + ncols - 1 (ncols <= NC), all unconditional
+// (indexes clamped, the unused values zeroed in pred_fma) so that they are in
+// flight together; the query is kept as raw bits until pred_fma so that no
+// conversion waits for its load.  VEC: J a multiple of 4, so each thread's four
+// rows are one 8- or 16-byte query load and one 16-byte load per head.
 template <int NC, bool VEC>
 __device__ __forceinline__ void pred_load(const void* __restrict__ q, int q_dtype, int64_t qoff,
-                                          const float* __restrict__ W, int Hq, int J, int h0,
-                                          int ncols, int j0, PredRows<NC>& r) {
+                                          const float* __restrict__ W, int J, int h0, int ncols,
+                                          int p0, PredRows<NC>& r) {
 #pragma unroll
-  for (int k = 0; k < kPredRows; ++k) {
-    const int j = j0 + (int)threadIdx.x + kPredThreads * k;
-    const int jc = j < J ? j : 0;
-    r.x[k] = q_dtype == ETA_DT_F32 ? reinterpret_cast<const uint32_t*>(q)[qoff + jc]
-                                   : (uint32_t)reinterpret_cast<const uint16_t*>(q)[qoff + jc];
-    const float* wr = W + (int64_t)jc * Hq + h0;
+  for (int p = 0; p < kPredPass; ++p) {
+    const int j = (p0 + p) * kPredStep + 4 * (int)threadIdx.x;
     if constexpr (VEC) {
+      const int jc = j < J ? j : 0;
+      if (q_dtype == ETA_DT_F32) {
+        const uint4 u = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint32_t*>(q) + qoff + jc);
+        r.x[p][0] = u.x; r.x[p][1] = u.y; r.x[p][2] = u.z; r.x[p][3] = u.w;
+      } else {
+        const uint2 u = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(q) + qoff + jc);
+        r.x[p][0] = u.x & 0xffffu; r.x[p][1] = u.x >> 16; r.x[p][2] = u.y & 0xffffu; r.x[p][3] = u.y >> 16;
+      }
 #pragma unroll
-      for (int c = 0; c < NC; c += 4) {
-        const float4 w4 = *reinterpret_cast<const float4*>(wr + c);
-        r.w[k][c] = w4.x;
-        r.w[k][c + 1] = w4.y;
-        r.w[k][c + 2] = w4.z;
-        r.w[k][c + 3] = w4.w;
+      for (int c = 0; c < NC; ++c) {
+        const int hc = h0 + (c < ncols ? c : 0);
+        const float4 w4 = *reinterpret_cast<const float4*>(W + (int64_t)hc * J + jc);
+        r.w[p][c][0] = w4.x; r.w[p][c][1] = w4.y; r.w[p][c][2] = w4.z; r.w[p][c][3] = w4.w;
       }
     } else {
 #pragma unroll
-      for (int c = 0; c < NC; ++c) r.w[k][c] = wr[c < ncols ? c : 0];
+      for (int e = 0; e < 4; ++e) {
+        const int jc = j + e < J ? j + e : 0;
+        r.x[p][e] = q_dtype == ETA_DT_F32 ? reinterpret_cast<const uint32_t*>(q)[qoff + jc]
+                                          : (uint32_t)reinterpret_cast<const uint16_t*>(q)[qoff + jc];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) r.w[p][c][e] = W[(int64_t)(h0 + (c < ncols ? c : 0)) * J + jc];
+      }
     }
   }
 }
 
 template <int NC>
-__device__ __forceinline__ void pred_fma(int q_dtype, int J, int ncols, int j0,
+__device__ __forceinline__ void pred_fma(int q_dtype, int J, int ncols, int p0,
                                          const PredRows<NC>& r, float (&acc)[NC]) {
 #pragma unroll
-  for (int k = 0; k < kPredRows; ++k) {
-    const bool in = j0 + (int)threadIdx.x + kPredThreads * k < J;
-    const float x = in ? pred_x(r.x[k], q_dtype) : 0.f;
+  for (int p = 0; p < kPredPass; ++p) {
 #pragma unroll
-    for (int c = 0; c < NC; ++c) acc[c] = fmaf(x, (in && c < ncols) ? r.w[k][c] : 0.f, acc[c]);
+    for (int e = 0; e < 4; ++e) {
+      const bool in = (p0 + p) * kPredStep + 4 * (int)threadIdx.x + e < J;
+      const float x = in ? pred_x(r.x[p][e], q_dtype) : 0.f;
+#pragma unroll
+      for (int c = 0; c < NC; ++c) acc[c] = fmaf(x, (in && c < ncols) ? r.w[p][c][e] : 0.f, acc[c]);
+    }
   }
 }
 
-// Thread t's partial sums over rows t, t + kPredThreads, ... in that order: the
-// first kPredRows from r (loaded by pred_load at j0 = 0), the rest loaded
-// kPredRows at a time.
+// Thread t's partial sums over its rows in the order above: the first
+// kPredPass passes from r (loaded by pred_load at pass 0), the rest loaded
+// kPredPass passes at a time.
 template <int NC, bool VEC>
 __device__ __forceinline__ void pred_sum(const void* __restrict__ q, int q_dtype, int64_t qoff,
-                                         const float* __restrict__ W, int Hq, int J, int h0,
-                                         int ncols, const PredRows<NC>& r, float (&acc)[NC]) {
+                                         const float* __restrict__ W, int J, int h0, int ncols,
+                                         const PredRows<NC>& r, float (&acc)[NC]) {
 #pragma unroll
   for (int c = 0; c < NC; ++c) acc[c] = 0.f;
   pred_fma<NC>(q_dtype, J, ncols, 0, r, acc);
-  for (int j0 = kPredThreads * kPredRows; j0 < J; j0 += kPredThreads * kPredRows) {
+  for (int p0 = kPredPass; p0 * kPredStep < J; p0 += kPredPass) {
     PredRows<NC> r2;
-    pred_load<NC, VEC>(q, q_dtype, qoff, W, Hq, J, h0, ncols, j0, r2);
-    pred_fma<NC>(q_dtype, J, ncols, j0, r2, acc);
+    pred_load<NC, VEC>(q, q_dtype, qoff, W, J, h0, ncols, p0, r2);
+    pred_fma<NC>(q_dtype, J, ncols, p0, r2, acc);
   }
 }
 
@@ -595,14 +629,14 @@ __global__ __launch_bounds__(kPredThreads) void predict_kernel(const void* __res
   const int ncols = Hq - h0 < kPredCols ? Hq - h0 : kPredCols;
   const int64_t J = (int64_t)Hq * D;
   float acc[kPredCols];
-  if (W != nullptr && ncols == kPredCols && Hq % 4 == 0) {
+  if (W != nullptr && J % 4 == 0) {
     PredRows<kPredCols> rows;
-    pred_load<kPredCols, true>(q, q_dtype, (int64_t)b * J, W, Hq, (int)J, h0, ncols, 0, rows);
-    pred_sum<kPredCols, true>(q, q_dtype, (int64_t)b * J, W, Hq, (int)J, h0, ncols, rows, acc);
+    pred_load<kPredCols, true>(q, q_dtype, (int64_t)b * J, W, (int)J, h0, ncols, 0, rows);
+    pred_sum<kPredCols, true>(q, q_dtype, (int64_t)b * J, W, (int)J, h0, ncols, rows, acc);
   } else if (W != nullptr) {
     PredRows<kPredCols> rows;
-    pred_load<kPredCols, false>(q, q_dtype, (int64_t)b * J, W, Hq, (int)J, h0, ncols, 0, rows);
-    pred_sum<kPredCols, false>(q, q_dtype, (int64_t)b * J, W, Hq, (int)J, h0, ncols, rows, acc);
+    pred_load<kPredCols, false>(q, q_dtype, (int64_t)b * J, W, (int)J, h0, ncols, 0, rows);
+    pred_sum<kPredCols, false>(q, q_dtype, (int64_t)b * J, W, (int)J, h0, ncols, rows, acc);
   } else {
 #pragma unroll
     for (int c = 0; c < kPredCols; ++c) acc[c] = 0.f;
@@ -679,7 +713,7 @@ __device__ __forceinline__ int screen_tile(int k) {
   return k;
 }
 
-template <int D, int G, bool BOUNDS_ONLY, typename ST>
+template <int D, int G, bool BOUNDS_ONLY, typename ST, bool VEC>
 __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
   constexpr int DQ = D / 4;            // dimensions per quarter
   const Geom& g = a.g;
@@ -689,7 +723,7 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
   __shared__ float q2_s[D][G];
   __shared__ float qn_s[G];
   __shared__ float teff_s[G];
-  __shared__ float part_s[3][2 * G][kScreenTile];
+  __shared__ float part_s[4][2 * G][kScreenTile];
   __shared__ float pred_red[4 * G];
 
   const int64_t hq0 = (int64_t)b * g.Hq + (int64_t)gh * G;   // first query head row of the group
@@ -697,19 +731,41 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
   const float scale = 1.0f / sqrtf((float)D);
   const float z = a.z;
 
-  // this lane's summary loads for blocks jb + lane (indexes clamped into the
-  // buffers; values of blocks that are not full are discarded later)
-  auto issue = [&](int64_t jb, float (&m)[DQ], float (&sd)[DQ], float& M) {
-    int64_t jc = jb + lane;
-    jc = jc < g.ncap ? jc : g.ncap - 1;
-    const ST* mup = reinterpret_cast<const ST*>(a.mu) + (bg * D + w * DQ) * g.ncap + jc;
-    const ST* sgp = reinterpret_cast<const ST*>(a.sigma) + (bg * D + w * DQ) * g.ncap + jc;
+  // This lane's summary loads: coordinate w DQ + 4 k + cg (cg = lane / 16) of the
+  // four consecutive blocks jb + 4 qd .. + 3 (qd = lane % 16), one load per
+  // record array and k when the rows are four-record aligned (VEC: n_blk_cap a
+  // multiple of 4), else four; indexes clamped into the buffers (records of
+  // blocks that are not full are discarded later; n_blk_cap >= 1).  Wavefront 0
+  // uses the largest norm of block jb + lane.
+  constexpr int NK = DQ / 4;
+  const int cg = lane >> 4, qd = lane & 15;
+  auto issue = [&](int64_t jb, Rec4<ST> (&m)[NK], Rec4<ST> (&sd)[NK], float& M) {
+    const int64_t row0 = bg * D + w * DQ + cg;
+    if constexpr (VEC) {             // n_blk_cap >= 4, a multiple of 4
+      int64_t j4 = jb + 4 * qd;
+      j4 = j4 < g.ncap ? j4 : g.ncap - 4;
 #pragma unroll
-    for (int i = 0; i < DQ; ++i) {
-      m[i] = stat_f32(mup[(int64_t)i * g.ncap]);
-      sd[i] = stat_f32(sgp[(int64_t)i * g.ncap]);
+      for (int k = 0; k < NK; ++k) {
+        const int64_t o = (row0 + 4 * k) * g.ncap + j4;
+        m[k] = *reinterpret_cast<const Rec4<ST>*>(reinterpret_cast<const ST*>(a.mu) + o);
+        sd[k] = *reinterpret_cast<const Rec4<ST>*>(reinterpret_cast<const ST*>(a.sigma) + o);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < NK; ++k) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          int64_t jc = jb + 4 * qd + e;
+          jc = jc < g.ncap ? jc : g.ncap - 1;
+          const int64_t o = (row0 + 4 * k) * g.ncap + jc;
+          m[k].v[e] = reinterpret_cast<const ST*>(a.mu)[o];
+          sd[k].v[e] = reinterpret_cast<const ST*>(a.sigma)[o];
+        }
+      }
     }
-    M = a.mx[bg * g.ncap + jc];
+    int64_t jm = jb + lane;
+    jm = jm < g.ncap ? jm : g.ncap - 1;
+    M = a.mx[bg * g.ncap + jm];       // (used by wavefront 0)
   };
   // the bias (or given threshold) and the predictor rows first, then this
   // tile's summaries: each is consumed in that order, so no wait for a later
@@ -733,10 +789,10 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
   const bool predict = !BOUNDS_ONLY && a.predict && a.W != nullptr;
   const int64_t Jq = (int64_t)g.Hq * D;
   PredRows<G> prow;
-  // the group's G columns: whole 16-byte groups when G is a multiple of 4
-  constexpr bool PVEC = G % 4 == 0;
-  if (predict) pred_load<G, PVEC>(a.q, a.q_dtype, (int64_t)b * Jq, a.W, g.Hq, (int)Jq, gh * G, G, 0, prow);
-  float m0[DQ], sd0[DQ], M0;
+  // the group's G rows of W (Hq d is a multiple of 4 here: d is 64 or 128)
+  if (predict) pred_load<G, true>(a.q, a.q_dtype, (int64_t)b * Jq, a.W, (int)Jq, gh * G, G, 0, prow);
+  Rec4<ST> m0[NK], sd0[NK];
+  float M0;
   issue((int64_t)tile * kScreenTile, m0, sd0, M0);
 
   // the group's queries, their norms (one wavefront per head), thresholds
@@ -763,7 +819,7 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
   if constexpr (!BOUNDS_ONLY) {
     if (predict) {
       float acc[G];
-      pred_sum<G, PVEC>(a.q, a.q_dtype, (int64_t)b * Jq, a.W, g.Hq, (int)Jq, gh * G, G, prow, acc);
+      pred_sum<G, true>(a.q, a.q_dtype, (int64_t)b * Jq, a.W, (int)Jq, gh * G, G, prow, acc);
 #pragma unroll
       for (int h = 0; h < G; ++h) {
         const float x = wave_sum(acc[h]);
@@ -797,31 +853,52 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
   const int64_t N = T / g.BS;
 
   // Bounds of blocks jb + lane from loads issued by `issue` (all four
-  // wavefronts take part); valid in wavefront 0, NaN for blocks not full.
-  auto finish = [&](int64_t jb, const float (&m)[DQ], const float (&sd)[DQ], float M,
+  // wavefronts take part); valid in wavefront 0, NaN for blocks not full.  Each
+  // lane sums its coordinates in order; the four coordinate groups of a block
+  // are added by row swaps (two registers per swap: block 4 qd + r of the quad
+  // ends in row r, as partial sums (rows 0 + 1) + (rows 2 + 3)); wavefront 0
+  // adds the four wavefronts' partials in order.
+  auto finish = [&](int64_t jb, const Rec4<ST> (&m)[NK], const Rec4<ST> (&sd)[NK], float M,
                     float (&bnd)[G]) {
     const int64_t j = jb + lane;
-    float dot[G], var[G];
+    float dot[G][4], var[G][4];
 #pragma unroll
-    for (int h = 0; h < G; ++h) { dot[h] = 0.f; var[h] = 0.f; }
+    for (int h = 0; h < G; ++h)
 #pragma unroll
-    for (int i = 0; i < DQ; ++i) {
-      // keep the query's LDS reads inside the loop: hoisted out of the rescue
-      // window's loop they held ~30 registers and cost a wavefront per SIMD
+      for (int e = 0; e < 4; ++e) { dot[h][e] = 0.f; var[h][e] = 0.f; }
+#pragma unroll
+    for (int k = 0; k < NK; ++k) {
+      // keep the query's LDS reads inside the loop (hoisted they hold registers)
       asm volatile("" ::: "memory");
-      const float s2 = sd[i] * sd[i];
+      const int i = w * DQ + 4 * k + cg;
+      float mv[4], sv[4];
+      rec4_f32(m[k], mv);
+      rec4_f32(sd[k], sv);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sv[e] *= sv[e];
 #pragma unroll
       for (int h = 0; h < G; ++h) {
-        dot[h] = fmaf(q_s[w * DQ + i][h], m[i], dot[h]);
-        var[h] = fmaf(q2_s[w * DQ + i][h], s2, var[h]);
+        const float qh = q_s[i][h], q2 = q2_s[i][h];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          dot[h][e] = fmaf(qh, mv[e], dot[h][e]);
+          var[h][e] = fmaf(q2, sv[e], var[h][e]);
+        }
       }
     }
-    if (w > 0) {
+    auto sum16 = [](float x, float y) {
+      const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(y), false, false);
+      return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    };
+    auto sum32 = [](float x, float y) {
+      const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(y), false, false);
+      return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    };
+    const int jq = 4 * qd + cg;       // the block whose sums this lane ends with
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
-        part_s[w - 1][h][lane] = dot[h];
-        part_s[w - 1][G + h][lane] = var[h];
-      }
+    for (int h = 0; h < G; ++h) {
+      part_s[w][h][jq] = sum32(sum16(dot[h][0], dot[h][1]), sum16(dot[h][2], dot[h][3]));
+      part_s[w][G + h][jq] = sum32(sum16(var[h][0], var[h][1]), sum16(var[h][2], var[h][3]));
     }
     __syncthreads();
 #pragma unroll
@@ -829,9 +906,10 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
     if (w == 0 && j < N) {
 #pragma unroll
       for (int h = 0; h < G; ++h) {
-        const float dt = ((dot[h] + part_s[0][h][lane]) + part_s[1][h][lane]) + part_s[2][h][lane];
-        const float vr =
-            ((var[h] + part_s[0][G + h][lane]) + part_s[1][G + h][lane]) + part_s[2][G + h][lane];
+        const float dt = ((part_s[0][h][lane] + part_s[1][h][lane]) + part_s[2][h][lane]) +
+                         part_s[3][h][lane];
+        const float vr = ((part_s[0][G + h][lane] + part_s[1][G + h][lane]) +
+                          part_s[2][G + h][lane]) + part_s[3][G + h][lane];
         const float gauss = fmaf(z, sqrtf(vr), dt);
         const float spher = qn_s[h] * M;
         float lo = gauss < spher ? gauss : spher;
@@ -2080,21 +2158,29 @@ namespace {
 template <bool BOUNDS_ONLY>
 void launch_screen_impl(const Geom& g, const ScreenArgs& sa, hipStream_t stream) {
   dim3 grid(g.n_tiles, g.Hkv, g.B);
+  // four-record loads need rows that start on a multiple of 4 records
+  const bool vec = g.ncap >= 4 && (g.ncap & 3) == 0;
+#define ETA_SCR_T(D_, G_, ST_)                                                                  \
+  if (vec)                                                                                      \
+    hipLaunchKernelGGL((screen_kernel<D_, G_, BOUNDS_ONLY, ST_, true>), grid,                   \
+                       dim3(kScreenThreads), 0, stream, sa);                                    \
+  else                                                                                          \
+    hipLaunchKernelGGL((screen_kernel<D_, G_, BOUNDS_ONLY, ST_, false>), grid,                  \
+                       dim3(kScreenThreads), 0, stream, sa);
 #define ETA_SCR(D_, G_)                                                                         \
   if (g.D == D_ && g.G == G_) {                                                                 \
-    if (g.stat_dtype == ETA_DT_F16)                                                             \
-      hipLaunchKernelGGL((screen_kernel<D_, G_, BOUNDS_ONLY, _Float16>), grid,                  \
-                         dim3(kScreenThreads), 0, stream, sa);                                  \
-    else if (g.stat_dtype == ETA_DT_FP8)                                                        \
-      hipLaunchKernelGGL((screen_kernel<D_, G_, BOUNDS_ONLY, uint8_t>), grid,                   \
-                         dim3(kScreenThreads), 0, stream, sa);                                  \
-    else                                                                                        \
-      hipLaunchKernelGGL((screen_kernel<D_, G_, BOUNDS_ONLY, float>), grid,                     \
-                         dim3(kScreenThreads), 0, stream, sa);                                  \
+    if (g.stat_dtype == ETA_DT_F16) {                                                           \
+      ETA_SCR_T(D_, G_, _Float16)                                                               \
+    } else if (g.stat_dtype == ETA_DT_FP8) {                                                    \
+      ETA_SCR_T(D_, G_, uint8_t)                                                                \
+    } else {                                                                                    \
+      ETA_SCR_T(D_, G_, float)                                                                  \
+    }                                                                                           \
   }
   ETA_SCR(64, 1) ETA_SCR(64, 2) ETA_SCR(64, 4) ETA_SCR(64, 8)
   ETA_SCR(128, 1) ETA_SCR(128, 2) ETA_SCR(128, 4) ETA_SCR(128, 8)
 #undef ETA_SCR
+#undef ETA_SCR_T
 }
 
 template <bool DENSE>
@@ -2134,7 +2220,7 @@ hipError_t launch_decode(const Geom& g, const DecodeCfg& c, int q_dtype, const v
                          int32_t* counts, int32_t* union_counts, const DecodeWs& ws,
                          hipStream_t stream, LaunchHook hook) {
   const bool predict = tau == nullptr;
-  // The fused predictor reads its group's W columns in every screening
+  // The fused predictor reads its group's G rows of W in every screening
   // workgroup: B Hkv n_tiles Hq D G 4 bytes of L2 reads per step.  Past
   // kFusedPredictMaxBytes the thresholds are predicted once per step by
   // predict_kernel into the workspace (the same arithmetic in the same order,

@@ -246,7 +246,9 @@ def update_block_summaries(k: torch.Tensor, prev_lens: torch.Tensor, seq_lens: t
 
 def predict_threshold(q: torch.Tensor, W: Optional[torch.Tensor], bias: torch.Tensor, *,
                       out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """eta_predict_threshold: tau[B][Hq] = concat(q[b]) W + bias (W None: tau = bias)."""
+    """eta_predict_threshold: tau[b][h] = concat(q[b]) . W[h] + bias[h] (W None: tau = bias).
+    W is head-major, fp32 [Hq][Hq d]: row h holds the weights of head h's threshold
+    (the (Hq d) x Hq predictor matrix transposed)."""
     B, Hq, d = q.shape
     if out is None:
         out = torch.empty(B, Hq, device=q.device, dtype=torch.float32)
@@ -319,7 +321,8 @@ def decode_predicted(q, k, v, seq_lens, summ: Summaries, W, bias, *, block_size:
                      params: Optional[DecodeParams] = None, out=None, mask=None, counts=None,
                      union_counts=None, tau_out=None, want_counts: bool = True,
                      workspace: Optional[torch.Tensor] = None, stream=None) -> DecodeOut:
-    """eta_decode_predicted: predictor fused into the decode step (tau = concat(q) W + bias)."""
+    """eta_decode_predicted: predictor fused into the decode step (tau as in
+    predict_threshold, W head-major)."""
     B, Hq, d = q.shape
     p = params if params is not None else decode_params()
     desc = kv_desc(k, Hq, block_size)

@@ -61,6 +61,12 @@ class Workload:
     def n_blk_cap(self) -> int:
         return self.T_cap // self.block
 
+    @property
+    def W_heads(self) -> Optional[torch.Tensor]:
+        """W in the library's head-major layout [Hq][Hq d] (row h: the weights of
+        head h's threshold), i.e. W transposed."""
+        return None if self.W is None else self.W.t().contiguous()
+
     def to(self, device) -> "Workload":
         out = Workload(**{f: getattr(self, f) for f in self.__dataclass_fields__})
         for n in ("q", "k", "v", "W", "bias"):

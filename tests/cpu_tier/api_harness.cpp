@@ -213,6 +213,7 @@ static eta_summary_t summ(const eta_kv_desc_t& k, int st = ETA_DT_F32) {
   s.sigma = FAKE;
   s.max_norm = reinterpret_cast<float*>(FAKE);
   s.n_blk_cap = k.capacity_tokens / k.block_size;
+  if (s.n_blk_cap < 1) s.n_blk_cap = 1;
   s.stat_dtype = st;
   return s;
 }

@@ -82,7 +82,7 @@ def run_gpu(wl: Workload, *, num_splits: int = 0, screen_all: bool = False,
     summ = eta.build_block_summaries(k, sl, wl.block, num_q_heads=wl.Hq, sub_block=sub_block,
                                      stat_dtype=stat_dtype)
     if tau is None:
-        W = None if wl.W is None else wl.W.to(dev)
+        W = None if wl.W is None else wl.W_heads.to(dev)
         tau = eta.predict_threshold(q, W, wl.bias.to(dev))
     p = eta.decode_params(beta=wl.beta, z=wl.z, offset_a=wl.a,
                           rescue_window=wl.rescue_window if rescue_window is None else rescue_window,

@@ -36,7 +36,7 @@ def good_desc(**kw):
 
 def ws_size(lib, desc, params, n_blk_cap=None):
     if n_blk_cap is None:
-        n_blk_cap = max(desc.capacity_tokens, 0) // max(desc.block_size, 1)
+        n_blk_cap = max(max(desc.capacity_tokens, 0) // max(desc.block_size, 1), 1)
     n = ctypes.c_size_t()
     st = lib.eta_decode_workspace_size(ctypes.byref(desc), n_blk_cap, ctypes.byref(params),
                                        ctypes.byref(n))
@@ -55,8 +55,9 @@ def test_workspace_size_valid_and_monotone(lib):
     st, n4 = ws_size(lib, good_desc(), p, n_blk_cap=4096 // 64 + 64)
     assert st == eta.ETA_OK and n4 > n1
     st, n5 = ws_size(lib, good_desc(capacity_tokens=52), p, n_blk_cap=1)
-    st0, n6 = ws_size(lib, good_desc(capacity_tokens=52), p, n_blk_cap=0)
-    assert st == st0 == eta.ETA_OK and n5 > n6
+    assert st == eta.ETA_OK and n5 > 0
+    # a summary holds at least one block, also below one block of capacity
+    assert ws_size(lib, good_desc(capacity_tokens=52), p, n_blk_cap=0)[0] == eta.ETA_ERR_INVALID_ARG
     assert ws_size(lib, good_desc(), p, n_blk_cap=4096 // 64 - 1)[0] == eta.ETA_ERR_INVALID_ARG
     assert ws_size(lib, good_desc(), p, n_blk_cap=131073)[0] == eta.ETA_ERR_UNSUPPORTED
 

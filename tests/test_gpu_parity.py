@@ -73,7 +73,7 @@ def test_predict_threshold_matches_oracle(dt, Hq, d):
     W = torch.randn(Hq * d, Hq, generator=g) * 0.02
     bias = torch.randn(Hq, generator=g)
     dev = torch.device("cuda")
-    tau = eta.predict_threshold(q.to(dev), W.to(dev), bias.to(dev)).cpu().numpy()
+    tau = eta.predict_threshold(q.to(dev), W.t().contiguous().to(dev), bias.to(dev)).cpu().numpy()
     ref = oracle.predict(as_numpy(q), W.numpy(), bias.numpy())
     np.testing.assert_allclose(tau, ref, rtol=1e-5, atol=1e-5)
     tau0 = eta.predict_threshold(q.to(dev), None, bias.to(dev)).cpu().numpy()
@@ -194,7 +194,7 @@ def test_decode_predicted_equals_predict_then_decode(G, d, b, dt):
     q, k, v = wl.q.to(dev), wl.k.to(dev), wl.v.to(dev)
     sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
     summ = eta.build_block_summaries(k, sl, b, num_q_heads=wl.Hq)
-    W, bias = wl.W.to(dev), wl.bias.to(dev)
+    W, bias = wl.W_heads.to(dev), wl.bias.to(dev)
     p = eta.decode_params(beta=wl.beta, z=wl.z, rescue_window=wl.rescue_window)
     tau = eta.predict_threshold(q, W, bias)
     ref = eta.decode(q, k, v, sl, summ, tau, block_size=b, params=p)
@@ -341,7 +341,7 @@ def test_config4_benchmarked_step_all_heads():
     summ = eta.build_block_summaries(wl.k, sl, wl.block, num_q_heads=wl.Hq)
     bias_buf = torch.empty(wl.Hq, dtype=torch.float32, device=dev)
     params = eta.decode_params(beta=wl.beta, z=wl.z, offset_a=wl.a, rescue_window=wl.rescue_window)
-    step = eta.DecodeStep(wl.q, wl.k, wl.v, sl, summ, wl.W, bias_buf, block_size=wl.block,
+    step = eta.DecodeStep(wl.q, wl.k, wl.v, sl, summ, wl.W_heads, bias_buf, block_size=wl.block,
                           params=params)
     for surv in (0.01, 0.05, 0.20, 1.0):
         bias = place_bias(r0.bounds, nb, qW, surv, wl.a)
@@ -383,7 +383,7 @@ def test_decode_predicted_predicts_once_per_step_past_the_fused_limit():
         q, k, v = wl.q.to(dev), wl.k.to(dev), wl.v.to(dev)
         sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
         summ = eta.build_block_summaries(k, sl, wl.block, num_q_heads=wl.Hq)
-        W, bias = wl.W.to(dev), wl.bias.to(dev)
+        W, bias = wl.W_heads.to(dev), wl.bias.to(dev)
         p = eta.decode_params(beta=wl.beta, z=wl.z, rescue_window=wl.rescue_window)
         tau = eta.predict_threshold(q, W, bias)
         ref = eta.decode(q, k, v, sl, summ, tau, block_size=wl.block, params=p)
@@ -420,7 +420,7 @@ def test_decode_step_replays_in_a_hip_graph_like_eager(predictor):
     q, k, v = wl.q.to(dev), wl.k.to(dev), wl.v.to(dev)
     sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
     summ = eta.build_block_summaries(k, sl, wl.block, num_q_heads=wl.Hq)
-    W = wl.W.to(dev) if wl.W is not None else None
+    W = wl.W_heads.to(dev) if wl.W is not None else None
     bias = wl.bias.to(dev)
     p = eta.decode_params(beta=wl.beta, z=wl.z, rescue_window=wl.rescue_window)
     eager = eta.DecodeStep(q, k, v, sl, summ, W, bias, block_size=wl.block, params=p)

@@ -30,7 +30,7 @@ def _run_pair(kw):
     q, k, v = wl.q.to(dev), wl.k.to(dev), wl.v.to(dev)
     sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
     summ = eta.build_block_summaries(k, sl, wl.block, num_q_heads=wl.Hq)
-    W, bias = wl.W.to(dev), wl.bias.to(dev)
+    W, bias = wl.W_heads.to(dev), wl.bias.to(dev)
     p = eta.decode_params(beta=wl.beta, z=wl.z, offset_a=wl.a, rescue_window=wl.rescue_window)
     tau_ref = torch.full((wl.B, wl.Hq), float("nan"), device=dev)
     ref = eta.decode_predicted(q, k, v, sl, summ, W, bias, block_size=wl.block, params=p,
