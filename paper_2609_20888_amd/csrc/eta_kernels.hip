@@ -2029,15 +2029,15 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
   const int hh = h % g.G;
   // per-head selected blocks: wavefront 0 sums the head's tile counts; the
   // union blocks of the (sequence, kv head): wavefront 1 of the group's first
-  // head sums the union's tile counts (both issued first, with the rescue
-  // results and the group's split range)
-  int cnt = 0;
-  if (a.counts != nullptr && tid < 64)
-    for (int t = tid; t < g.n_tiles; t += 64) cnt += a.head_cnt[row * g.n_tiles + t];
+  // head sums the union's tile counts.  The first 64 of each are loaded here
+  // (every thread, from clamped indexes, so no load waits inside a branch or
+  // a loop) together with the rescue results and the group's split range, and
+  // summed at the end; tiles past 64 are read there.
+  const int lt = tid & 63, ti = lt < g.n_tiles ? lt : 0;
+  const bool do_cnt = a.counts != nullptr && tid < 64;
   const bool do_union = a.union_counts != nullptr && hh == 0 && tid >= 64 && tid < 128;
-  int ucnt = 0;
-  if (do_union)
-    for (int t = tid - 64; t < g.n_tiles; t += 64) ucnt += a.tile_cnt[bg * g.n_tiles + t];
+  int cnt = a.counts != nullptr ? a.head_cnt[row * g.n_tiles + ti] : 0;
+  int ucnt = a.union_counts != nullptr ? a.tile_cnt[bg * g.n_tiles + ti] : 0;
   const int rescued = (a.resc_out != nullptr && tid == 0) ? a.resc_out[row] : -1;
   const int extra = (a.extra_union != nullptr && tid == 64 && do_union) ? a.extra_union[bg] : 0;
   int first = (int)bg * a.S, S = a.S;
@@ -2094,7 +2094,9 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
     }
     store_out(a.out, a.q_dtype, row * D + tid, Lt > 0.f ? x / Lt : 0.f);
   }
-  if (a.counts != nullptr && tid < 64) {
+  if (do_cnt) {
+    cnt = lt < g.n_tiles ? cnt : 0;
+    for (int t = lt + 64; t < g.n_tiles; t += 64) cnt += a.head_cnt[row * g.n_tiles + t];
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
     if (tid == 0) {
@@ -2104,6 +2106,8 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
     }
   }
   if (do_union) {
+    ucnt = lt < g.n_tiles ? ucnt : 0;
+    for (int t = lt + 64; t < g.n_tiles; t += 64) ucnt += a.tile_cnt[bg * g.n_tiles + t];
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) ucnt += __shfl_xor(ucnt, o, 64);
     if (tid == 64) a.union_counts[bg] = ucnt + extra;
