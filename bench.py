@@ -33,6 +33,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -45,7 +46,7 @@ PRIMARY_SURVIVAL = 0.20
 SWEEP = (0.01, 0.05, 0.20, 1.00)
 # sources of the decode-path kernels: the counter file's traffic is valid only for these
 DECODE_SRCS = [os.path.join(ROOT, "paper_2609_20888_amd", "csrc", f)
-               for f in ("eta_kernels.hip", "eta_device.h")]
+               for f in ("eta_kernels.hip", "eta_device.h", "eta_index.h", "eta_internal.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "split_decode_512k_traffic.json")
 
 
@@ -54,10 +55,15 @@ def log(*a):
 
 
 def kernel_src_sha() -> str:
+    """Hash of the decode kernels' code (comments and whitespace removed, so a
+    comment edit does not orphan the committed counter summary)."""
     h = hashlib.sha256()
     for path in DECODE_SRCS:
-        with open(path, "rb") as f:
-            h.update(f.read())
+        with open(path, encoding="utf-8") as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

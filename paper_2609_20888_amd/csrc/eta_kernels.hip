@@ -649,22 +649,24 @@ __global__ __launch_bounds__(kPredThreads) void predict_kernel(const void* __res
 // ---------------------------------------------------------------- screening
 //
 // One workgroup of 256 threads per (tile of 64 blocks, kv head, sequence).
-// Lane l of wavefront w owns block 64 * tile + l and head-dimension quarter w:
-// with the dimension-major summaries, coordinate i of the tile's 64 blocks is
-// one coalesced 256-byte load, and each lane keeps its quarter's loads in
-// flight together.  These loads are issued first, before the query, length and
-// threshold loads they do not depend on.  The G query heads of the group are
-// evaluated from the same loads (q broadcast from LDS).  Wavefront 0 adds the
-// four quarter partials in a fixed order and owns everything per block after
-// that: selection, rescue, mask, and the ordered compaction of the tile's
-// union ids (one ballot).  A union id carries the block's head bits in its top
-// byte.
+// Wavefront w takes head-dimension quarter w; with the dimension-major
+// summaries, lane (cg, qd) (cg = lane / 16, qd = lane % 16) reads coordinate
+// 4 k + cg of the tile's blocks 4 qd .. 4 qd + 3 with one load per record array,
+// so a wavefront has 17 loads in flight for its quarter.  These loads are
+// issued right after the threshold and query loads, and every later step waits
+// only for its own.  The G query heads of the group are evaluated from the
+// same loads (q broadcast from LDS).  The partial sums reach wavefront 0 (lane
+// = block) through LDS; it adds them in a fixed order and owns everything per
+// block after that: selection, the rescue part, mask, and the ordered
+// compaction of the tile's union ids (one ballot).  A union id carries the
+// block's head bits in its top byte.
 //
 // Top-1 rescue needs the selection state of the whole window [0, min(c, N)),
-// which can span up to four tiles.  Every workgroup whose tile intersects the
-// window evaluates the window's bounds itself, with the same arithmetic as the
-// owning tiles (so the decisions agree bit for bit), and sets the rescued
-// block's bit only if that block is its own.
+// which can span up to four tiles.  Each tile that meets the window writes its
+// part: per head, whether one of its window blocks is selected, else the first
+// of its largest bounds and that block; and the union head bits of its window
+// blocks.  The split kernel, which runs after screening anyway, combines the
+// parts, so no workgroup waits for another.
 //
 // With a predictor (W, bias), every workgroup computes the thresholds of its
 // G heads itself, with the stand-alone predictor's summation order (so they
