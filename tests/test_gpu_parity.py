@@ -66,7 +66,8 @@ def test_block_summaries_match_oracle(case):
 
 
 @pytest.mark.parametrize("dt", [torch.bfloat16, torch.float32])
-@pytest.mark.parametrize("Hq,d", [(16, 128), (32, 128), (4, 64), (12, 64)])
+@pytest.mark.parametrize("Hq,d", [(16, 128), (32, 128), (4, 64), (12, 64),
+                                  (6, 37), (5, 3), (1, 1024)])   # Hq d not a multiple of 4; Hq % 4 != 0
 def test_predict_threshold_matches_oracle(dt, Hq, d):
     g = torch.Generator().manual_seed(Hq * d)
     q = torch.randn(5, Hq, d, generator=g).to(dt)
