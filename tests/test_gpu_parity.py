@@ -13,8 +13,8 @@ import pytest
 import torch
 
 import oracle
-from gpu_support import (GpuRun, calibrate_bias, compare, oracle_inputs, require_gpu, run_gpu,
-                         run_oracle, say)
+from gpu_support import (GpuRun, calibrate_bias, compare, f16_band, f16_record_ranges,
+                         oracle_inputs, oracle_summaries, require_gpu, run_gpu, run_oracle, say)
 from paper_2609_20888_amd import eta
 from synth import as_numpy, config1, config2, config3, config4, config5, make_workload, place_bias
 
@@ -358,6 +358,47 @@ def test_config4_benchmarked_step_all_heads():
         stats = compare(wl, g, orc, tau_o, np_inputs=np_in, union_counts=step.union_counts)
         assert stats["compared"] == wl.Hq and stats["union_counts_checked"] == wl.Hkv
         say(f"[gpu] 512K step at {surv:.0%} survival: {stats}")
+
+
+@pytest.mark.parametrize("rec", ["f16", "fp8"])
+def test_config4_benchmarked_step_compact_records(rec):
+    """The benchmark's fp16 / FP8 record arms at the benchmark's shape: the
+    prepared eta_decode_predicted step on the 512K workload's compact index at
+    20% survival (thresholds placed from that index's own bounds, as the
+    benchmark places them), every query head against the oracle screening the
+    same rounded records, the tie band widened by the rounding intervals."""
+    sd = torch.float16 if rec == "f16" else torch.float8_e4m3fn
+    rnd = oracle.round_f16 if rec == "f16" else oracle.round_e4m3
+    wl = config4(device="cuda")
+    np_in = oracle_inputs(wl)
+    q, k, v = np_in
+    mu, sg, mx = oracle_summaries(wl, k)
+    osumm = (rnd(mu), rnd(sg), mx)
+    r0 = oracle.decode(q, k, v, wl.seq_lens, None, block_size=wl.block, z=wl.z, bounds_only=True,
+                       summaries=osumm)
+    W = as_numpy(wl.W)
+    nb = [t // wl.block for t in wl.seq_lens]
+    bias = place_bias(r0.bounds, nb, oracle.predict(q, W, None), 0.20, wl.a)
+    dev = torch.device("cuda")
+    sl = torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev)
+    summ = eta.build_block_summaries(wl.k, sl, wl.block, num_q_heads=wl.Hq, stat_dtype=sd)
+    params = eta.decode_params(beta=wl.beta, z=wl.z, offset_a=wl.a, rescue_window=wl.rescue_window)
+    bias_t = torch.as_tensor(bias, dtype=torch.float32, device=dev)
+    step = eta.DecodeStep(wl.q, wl.k, wl.v, sl, summ, wl.W_heads, bias_t, block_size=wl.block,
+                          params=params)
+    step.run()
+    torch.cuda.synchronize()
+    wl.bias = torch.as_tensor(bias)
+    tau_o = oracle.predict(q, W, bias)
+    assert np.max(np.abs(step.tau.cpu().numpy() - tau_o)) <= 1e-5
+    orc, _ = run_oracle(wl, np_in, tau=tau_o, summaries=osumm)
+    extra = f16_band(wl, q, osumm[0], osumm[1], f16_record_ranges(wl, k, mu, sg, rnd=rnd))
+    g = GpuRun(out=step.out, mask=step.mask, counts=step.counts, tau=step.tau, summ=summ,
+               union_counts=step.union_counts)
+    stats = compare(wl, g, orc, tau_o, np_inputs=np_in, band_extra=extra,
+                    union_counts=step.union_counts)
+    assert stats["compared"] == wl.Hq and stats["union_counts_checked"] == wl.Hkv
+    say(f"[gpu] 512K step on {rec} records at 20% survival: {stats}")
 
 
 def test_config5_constant_thresholds_all_rows():
