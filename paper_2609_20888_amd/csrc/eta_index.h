@@ -85,4 +85,23 @@ ETA_HD int64_t union_slot(int64_t group_base, int tile, uint64_t bal, int lane) 
   return group_base + (int64_t)tile * 64 + __builtin_popcountll(below);
 }
 
+// Screening's record loads (dimension-major records, rows of n_blk_cap
+// entries): element offset of the four consecutive records of row `row` that
+// start at block j4 (a multiple of 4), for rows that are four-record aligned
+// (ncap a multiple of 4, ncap >= 4), clamped so that all four lie in the row;
+// and of one record at block j, clamped into the row (ncap >= 1).
+ETA_HD int64_t screen_rec4_offset(int64_t row, int64_t ncap, int64_t j4) {
+  return row * ncap + (j4 < ncap ? j4 : ncap - 4);
+}
+ETA_HD int64_t screen_rec1_offset(int64_t row, int64_t ncap, int64_t j) {
+  return row * ncap + (j < ncap ? j : ncap - 1);
+}
+
+// The predictor's rows for thread t in pass p: the first of its four rows
+// 1024 p + 4 t .. + 3 when they lie in [0, J) (J a multiple of 4), else 0.
+ETA_HD int pred_row4(int p, int t, int J) {
+  const int j = p * 1024 + 4 * t;
+  return j < J ? j : 0;
+}
+
 }  // namespace eta

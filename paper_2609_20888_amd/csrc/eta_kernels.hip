@@ -509,6 +509,7 @@ __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ 
 constexpr int kPredThreads = 256;
 constexpr int kPredCols = 4;                    // heads per stand-alone predictor workgroup
 constexpr int kPredStep = 4 * kPredThreads;     // rows per pass
+static_assert(kPredStep == 1024, "pred_row4 (eta_index.h) takes 1024 rows per pass");
 // The first kPredPass passes of each thread are loaded into registers by
 // pred_load (so a caller can issue them ahead of other loads) and consumed by
 // pred_sum, which then continues over any further rows in the same order.
@@ -538,7 +539,7 @@ __device__ __forceinline__ void pred_load(const void* __restrict__ q, int q_dtyp
   for (int p = 0; p < kPredPass; ++p) {
     const int j = (p0 + p) * kPredStep + 4 * (int)threadIdx.x;
     if constexpr (VEC) {
-      const int jc = j < J ? j : 0;
+      const int jc = pred_row4(p0 + p, (int)threadIdx.x, J);
       if (q_dtype == ETA_DT_F32) {
         const uint4 u = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint32_t*>(q) + qoff + jc);
         r.x[p][0] = u.x; r.x[p][1] = u.y; r.x[p][2] = u.z; r.x[p][3] = u.w;
@@ -744,11 +745,9 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
   auto issue = [&](int64_t jb, Rec4<ST> (&m)[NK], Rec4<ST> (&sd)[NK], float& M) {
     const int64_t row0 = bg * D + w * DQ + cg;
     if constexpr (VEC) {             // n_blk_cap >= 4, a multiple of 4
-      int64_t j4 = jb + 4 * qd;
-      j4 = j4 < g.ncap ? j4 : g.ncap - 4;
 #pragma unroll
       for (int k = 0; k < NK; ++k) {
-        const int64_t o = (row0 + 4 * k) * g.ncap + j4;
+        const int64_t o = screen_rec4_offset(row0 + 4 * k, g.ncap, jb + 4 * qd);
         m[k] = *reinterpret_cast<const Rec4<ST>*>(reinterpret_cast<const ST*>(a.mu) + o);
         sd[k] = *reinterpret_cast<const Rec4<ST>*>(reinterpret_cast<const ST*>(a.sigma) + o);
       }
@@ -757,9 +756,7 @@ __global__ __launch_bounds__(kScreenThreads) void screen_kernel(ScreenArgs a) {
       for (int k = 0; k < NK; ++k) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          int64_t jc = jb + 4 * qd + e;
-          jc = jc < g.ncap ? jc : g.ncap - 1;
-          const int64_t o = (row0 + 4 * k) * g.ncap + jc;
+          const int64_t o = screen_rec1_offset(row0 + 4 * k, g.ncap, jb + 4 * qd + e);
           m[k].v[e] = reinterpret_cast<const ST*>(a.mu)[o];
           sd[k].v[e] = reinterpret_cast<const ST*>(a.sigma)[o];
         }

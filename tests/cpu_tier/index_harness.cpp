@@ -117,6 +117,72 @@ static void check_compaction(uint64_t bal, int tile, int64_t base, int ncap) {
   for (int r = 0; r < 64; ++r) CHECK(used[r] <= 1, "slot %d used %d times", r, used[r]);
 }
 
+// Screening's record loads over heap arrays of exactly B Hkv d n_blk_cap records:
+// every lane (cg = lane / 16, qd = lane % 16) of every wavefront (head-dimension
+// quarter w) of every tile, on the four-record path (n_blk_cap a multiple of 4,
+// >= 4: the four records in the row, aligned) or the one-record path; and the
+// largest-norm load (lane = block).
+static void check_screen_loads(int BHkv, int D, int64_t ncap) {
+  const int64_t total = (int64_t)BHkv * D * ncap;
+  float* rec = new float[total];
+  float* mx = new float[(int64_t)BHkv * ncap];
+  for (int64_t i = 0; i < total; ++i) rec[i] = 0.f;
+  const int n_tiles = ncap < 64 ? 1 : (int)((ncap + 63) / 64);
+  const bool vec = ncap >= 4 && ncap % 4 == 0;
+  const int DQ = D / 4, NK = DQ / 4;
+  float sink = 0.f;
+  for (int bg = 0; bg < BHkv; ++bg)
+    for (int tile = 0; tile < n_tiles; ++tile)
+      for (int w = 0; w < 4; ++w)
+        for (int lane = 0; lane < 64; ++lane) {
+          const int cg = lane >> 4, qd = lane & 15;
+          const int64_t jb = (int64_t)tile * 64;
+          for (int k = 0; k < NK; ++k) {
+            const int64_t row = (int64_t)bg * D + w * DQ + cg + 4 * k;
+            CHECK(row < (int64_t)BHkv * D, "row %lld", (long long)row);
+            if (vec) {
+              const int64_t o = screen_rec4_offset(row, ncap, jb + 4 * qd);
+              CHECK(o >= row * ncap && o + 3 < (row + 1) * ncap && o % 4 == 0,
+                    "ncap %lld tile %d lane %d: records [%lld, %lld] outside row %lld",
+                    (long long)ncap, tile, lane, (long long)o, (long long)o + 3, (long long)row);
+              if (jb + 4 * qd < ncap) CHECK(o == row * ncap + jb + 4 * qd, "in-range quad moved");
+              for (int e = 0; e < 4; ++e) sink += rec[o + e];
+            } else {
+              for (int e = 0; e < 4; ++e) {
+                const int64_t o = screen_rec1_offset(row, ncap, jb + 4 * qd + e);
+                CHECK(o >= row * ncap && o < (row + 1) * ncap, "record %lld outside row", (long long)o);
+                if (jb + 4 * qd + e < ncap) CHECK(o == row * ncap + jb + 4 * qd + e, "in-range record moved");
+                sink += rec[o];
+              }
+            }
+          }
+          int64_t jm = jb + lane;
+          jm = jm < ncap ? jm : ncap - 1;
+          sink += mx[bg * ncap + jm] = 0.f;
+        }
+  (void)sink;
+  delete[] mx;
+  delete[] rec;
+}
+
+// The predictor's passes: every row of [0, J) taken by exactly one (pass,
+// thread, e), four consecutive rows per thread and pass (J a multiple of 4).
+static void check_pred_rows(int J) {
+  std::vector<int> seen(J, 0);
+  const int passes = (J + 1023) / 1024;
+  for (int p = 0; p < passes + 1; ++p)
+    for (int t = 0; t < 256; ++t) {
+      const int j = p * 1024 + 4 * t;
+      const int jc = pred_row4(p, t, J);
+      CHECK(jc >= 0 && jc + 3 < J, "J %d pass %d thread %d -> rows %d..%d", J, p, t, jc, jc + 3);
+      if (j < J) {
+        CHECK(jc == j, "in-range rows moved");
+        for (int e = 0; e < 4; ++e) ++seen[j + e];
+      }
+    }
+  for (int j = 0; j < J; ++j) CHECK(seen[j] == 1, "J %d row %d taken %d times", J, j, seen[j]);
+}
+
 int main() {
   std::mt19937_64 rng(12345);
   // plans: one group, the largest table, all work in one group, no work, ragged
@@ -163,6 +229,12 @@ int main() {
     if (k % 11 == 0) bal = ~0ull;
     check_compaction(bal, (int)(rng() % 2048), (int64_t)(rng() % 1000) * 131072, 2048 * 64);
   }
+  // screening record loads: one block, below a tile, a partial last tile, whole
+  // tiles, the largest table; both load paths; both head dimensions
+  for (int64_t ncap : {1, 3, 4, 5, 63, 64, 65, 68, 130, 2048, 2051})
+    for (int D : {64, 128}) check_screen_loads(2, D, ncap);
+  check_screen_loads(1, 128, 131072);
+  for (int J : {4, 64, 1020, 1024, 1028, 2048, 3072, 8192, 262144}) check_pred_rows(J);
   if (failures) {
     std::fprintf(stderr, "%d check(s) failed\n", failures);
     return 1;
