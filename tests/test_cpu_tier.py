@@ -1,11 +1,12 @@
 """CPU correctness tier: the library's host code and the kernels' index
 arithmetic built with g++ under the address and undefined-behaviour sanitizers.
 
-* tests/cpu_tier/index_harness.cpp runs the split-decode kernel's index
-  functions (paper_2609_20888_amd/csrc/eta_index.h: proportional split plan,
-  union-list tile prefix and item lookup, split shares, compaction slots) on
-  edge geometries -- ragged T, T below one block, 2048 screening tiles, 1024
-  splits -- over heap buffers of exactly the kernels' sizes.
+* tests/cpu_tier/index_harness.cpp runs the kernels' index functions
+  (paper_2609_20888_amd/csrc/eta_index.h: proportional split plan, union-list
+  tile prefix and item lookup, split shares, compaction slots, screening's
+  record offsets, the predictor's row groups) on edge geometries -- ragged T,
+  T below one block, capacities that are not a multiple of 4, 2048 screening
+  tiles, 1024 splits -- over heap buffers of exactly the kernels' sizes.
 * tests/cpu_tier/api_harness.cpp links eta_api.cpp (argument validation,
   split planning, workspace carve-up) against stub launchers that check every
   workspace region lies inside a workspace of exactly the requested size and
