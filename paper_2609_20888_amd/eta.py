@@ -244,12 +244,28 @@ def update_block_summaries(k: torch.Tensor, prev_lens: torch.Tensor, seq_lens: t
     return summ
 
 
+def _check_predictor(q: torch.Tensor, W: Optional[torch.Tensor], bias: torch.Tensor) -> None:
+    """The predictor's tensors as the C ABI reads them (it sees only pointers): q
+    contiguous [B][Hq][d]; W None or fp32 [Hq][Hq d] contiguous (head-major); bias
+    fp32 [Hq] contiguous."""
+    B, Hq, d = q.shape
+    if not q.is_contiguous():
+        raise ValueError("q must be contiguous [B][Hq][d]")
+    if W is not None and (W.dtype != torch.float32 or tuple(W.shape) != (Hq, Hq * d)
+                          or not W.is_contiguous()):
+        raise ValueError(f"W must be fp32 [{Hq}][{Hq * d}] contiguous (head-major: row h holds "
+                         f"head h's weights), got {W.dtype} {tuple(W.shape)}")
+    if bias.dtype != torch.float32 or tuple(bias.shape) != (Hq,) or not bias.is_contiguous():
+        raise ValueError(f"bias must be fp32 [{Hq}] contiguous, got {bias.dtype} {tuple(bias.shape)}")
+
+
 def predict_threshold(q: torch.Tensor, W: Optional[torch.Tensor], bias: torch.Tensor, *,
                       out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """eta_predict_threshold: tau[b][h] = concat(q[b]) . W[h] + bias[h] (W None: tau = bias).
     W is head-major, fp32 [Hq][Hq d]: row h holds the weights of head h's threshold
     (the (Hq d) x Hq predictor matrix transposed)."""
     B, Hq, d = q.shape
+    _check_predictor(q, W, bias)
     if out is None:
         out = torch.empty(B, Hq, device=q.device, dtype=torch.float32)
     _check(load_library().eta_predict_threshold(B, Hq, d, _dtype_code(q), _ptr(q), _ptr(W),
@@ -324,6 +340,7 @@ def decode_predicted(q, k, v, seq_lens, summ: Summaries, W, bias, *, block_size:
     """eta_decode_predicted: predictor fused into the decode step (tau as in
     predict_threshold, W head-major)."""
     B, Hq, d = q.shape
+    _check_predictor(q, W, bias)
     p = params if params is not None else decode_params()
     desc = kv_desc(k, Hq, block_size)
     if v.shape != k.shape or v.stride() != k.stride() or v.dtype != k.dtype:
@@ -353,6 +370,7 @@ def decode_predicted_noalloc(q, k, v, seq_lens, summ: Summaries, W, bias, *, blo
     as the workspace (the C call allocates nothing; output buffers not given are
     allocated here, before the call)."""
     B, Hq, d = q.shape
+    _check_predictor(q, W, bias)
     p = params if params is not None else decode_params()
     desc = kv_desc(k, Hq, block_size)
     if v.shape != k.shape or v.stride() != k.stride() or v.dtype != k.dtype:
@@ -377,6 +395,7 @@ class DecodeStep:
     def __init__(self, q, k, v, seq_lens, summ: Summaries, W, bias, *, block_size: int,
                  params: Optional[DecodeParams] = None, want_counts: bool = True, stream=None):
         B, Hq, d = q.shape
+        _check_predictor(q, W, bias)
         self.tensors = (q, k, v, seq_lens, summ.mu, summ.sigma, summ.max_norm, W, bias)
         self.params = params if params is not None else decode_params()
         self.desc = kv_desc(k, Hq, block_size)

@@ -5,6 +5,7 @@ import os
 import re
 
 import pytest
+import torch
 
 from paper_2609_20888_amd import eta
 
@@ -239,3 +240,18 @@ def test_prefill_rejects(lib):
     assert call(desc(), q=None) == eta.ETA_ERR_INVALID_ARG
     assert call(desc(), out=FAKE + 8) == eta.ETA_ERR_INVALID_ARG
     assert call(desc(), tau=FAKE + 2) == eta.ETA_ERR_INVALID_ARG
+
+
+def test_binding_checks_predictor_layout():
+    # the C ABI sees only pointers: the binding refuses a W that is not fp32
+    # [Hq][Hq d] contiguous (the head-major layout) before any call
+    q = torch.zeros(2, 4, 8, dtype=torch.bfloat16)
+    bias = torch.zeros(4)
+    for W in (torch.zeros(32, 4),                   # the [Hq d][Hq] layout
+              torch.zeros(4, 32, dtype=torch.float64),
+              torch.zeros(32, 4).t(),               # head-major shape, not contiguous
+              torch.zeros(4, 31)):
+        with pytest.raises(ValueError):
+            eta.predict_threshold(q, W, bias)
+    with pytest.raises(ValueError):
+        eta.predict_threshold(q, torch.zeros(4, 32), torch.zeros(5))
