@@ -41,16 +41,12 @@ ETA_HD int exclusive_prefix(int* v, int n) {
   return acc;
 }
 
-// The group of split workgroup `me`: the last g with first[g] <= me; -1 when me
-// is past the allocation (first[n] = the number of split workgroups used).
-ETA_HD int find_group(const int* first, int n, int me) {
-  if (me >= first[n]) return -1;
-  int lo = 0, hi = n;
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (first[mid] <= me) lo = mid; else hi = mid;
-  }
-  return lo;
+// Whether split workgroup `me` belongs to the group whose splits are
+// [first, first + splits): under the proportional plan each group has at least
+// one split and the groups' ranges follow each other, so exactly one group owns
+// each workgroup below the number used and none owns the rest.
+ETA_HD bool owns_split(int first, int splits, int me) {
+  return first <= me && me < first + splits;
 }
 
 // Union list item `it` (pref = exclusive prefix of the per-tile union counts,

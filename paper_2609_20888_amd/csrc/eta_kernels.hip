@@ -218,6 +218,23 @@ __device__ __forceinline__ float wave_sum(float x) {
   return wave_reduce(x, [](float a, float b) { return a + b; });
 }
 
+// Inclusive prefix sum of an integer over the wavefront's lanes, on the vector
+// ALUs: shifts by 1, 2, 4 and 8 lanes within each 16-lane row (a lane whose
+// source would lie in the previous row adds 0), then each row adds the totals
+// of the rows before it, read from lanes 15, 31 and 47.  Lane 63 ends with the
+// wavefront's total.  Full EXEC only.
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);   // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);   // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);   // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);   // row_shr:8
+  const int r0 = __builtin_amdgcn_readlane(x, 15);
+  const int r1 = r0 + __builtin_amdgcn_readlane(x, 31);
+  const int r2 = r1 + __builtin_amdgcn_readlane(x, 47);
+  const int row = (int)(threadIdx.x & 63) >> 4;
+  return x + (row == 0 ? 0 : (row == 1 ? r0 : (row == 2 ? r1 : r2)));
+}
+
 // ---------------------------------------------------------------- summaries
 //
 // One workgroup handles kSumBlocks consecutive full blocks of one (sequence,
@@ -1047,7 +1064,6 @@ struct SplitArgs {
   float beta, offset_a;
   int self_ungated;
   int c;                     // rescue window (blocks)
-  int S_uniform;             // > 0: S splits per group, grid (S, Hkv, B); 0: proportional, 1-D grid
 };
 
 
@@ -1349,7 +1365,7 @@ constexpr int kItemChunk = 256;
 // Wavefronts per split-decode workgroup.
 constexpr int kSplitWaves = 4;
 
-template <int D, int BS, int G, typename KVT, bool DENSE>
+template <int D, int BS, int G, typename KVT, bool DENSE, bool PROP>
 __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
   constexpr int NW = kSplitWaves, NT = 64 * NW;
   constexpr int DPL = D / 64;
@@ -1370,7 +1386,8 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
   __shared__ int32_t item_j[kItemChunk];
   __shared__ uint8_t item_bits[kItemChunk];
   __shared__ uint8_t item_sub[kItemChunk];
-  __shared__ int grp_s[DENSE ? 1 : kPropMaxGroups + 1];  // proportional: first split of each group
+  __shared__ int own_s[3];                               // proportional: (group, first split, splits)
+  __shared__ int wsum2_s[DENSE ? 1 : kPropMaxGroups / NT][NW];  // proportional: split scan's wavefront sums
   __shared__ int cnt_s[DENSE ? 1 : kPropMaxCounts + 1];  // proportional: prefix of every tile count
   __shared__ int wtail_s[NW];
   __shared__ float rbest_s[DENSE ? 1 : G][kRescueTiles];
@@ -1380,31 +1397,34 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
   __shared__ int rxw_s[G];                               // union bits at each head's rescued block
   __shared__ int nrx_s;
 
-  // ---- which (sequence, kv head) and split.  Uniform: S splits per group, grid
-  // (S, Hkv, B).  Proportional (several sequences): a 1-D grid whose workgroups are
-  // dealt to the groups in proportion to their union's 64-token tiles (at least
-  // one each), so short and long unions finish together in one round.
+  // ---- which (sequence, kv head) and split.  Uniform plan (PROP false): S splits
+  // per group, grid (S, Hkv, B).  Proportional plan (PROP, several sequences): a
+  // 1-D grid whose workgroups are dealt to the groups in proportion to their
+  // union's 64-token tiles (at least one each), so short and long unions finish
+  // together in one round.  The two plans are separate instantiations, so neither
+  // carries the other's code.
   constexpr int SPB = BF ? BS / 64 : 1;
-  const bool uniform = DENSE || a.S_uniform > 0;
+  constexpr bool uniform = !PROP;
+  static_assert(!(DENSE && PROP), "the dense baseline takes the uniform plan");
   int b, gh, s, S, first;
   const int32_t* tc = nullptr;     // uniform: the group's tile counts
   const int* pref = pref_s;        // exclusive prefix of the group's tile counts ...
   int pbase = 0;                   // ... offset by pbase
-  if (uniform) {
+  if constexpr (uniform) {
     s = blockIdx.x;
     gh = blockIdx.y;
     b = blockIdx.z;
     S = gridDim.x;
     first = (b * g.Hkv + gh) * S;
     tc = a.tile_cnt + ((int64_t)b * g.Hkv + gh) * g.n_tiles;
-  } else if constexpr (!DENSE) {
+  } else {
     // Every tile count and every length in one round trip.  One block scan of
     // the counts (groups in order, each group's tiles in order) gives each
     // group's union tiles and, offset by the group's start, its own tile prefix;
     // a second scan over the groups' split counts gives each group's first split.
     const int BG = g.B * g.Hkv, nct = g.n_tiles, nc = BG * nct, W = gridDim.x;
     constexpr int CPT = kPropMaxCounts / NT;   // counts per thread, contiguous
-    constexpr int GPT = kPropMaxGroups / NT;   // groups per thread, contiguous
+    constexpr int GPT = kPropMaxGroups / NT;   // groups per thread: r NT + tid, r < GPT
     static_assert(CPT * NT == kPropMaxCounts && GPT * NT == kPropMaxGroups, "whole shares");
     // (unconditional loads from clamped indexes, masked afterwards: a load under a
     // branch is waited for inside the branch, one round trip each)
@@ -1414,10 +1434,18 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
       const int i = tid * CPT + k;
       cv[k] = a.tile_cnt[i < nc ? i : 0];
     }
+    {
+      // group x = r NT + tid is (sequence q, kv head rm): one division per
+      // thread, then steps of NT groups
+      const unsigned hkv = (unsigned)g.Hkv, qn = (unsigned)NT / hkv, rn = (unsigned)NT % hkv;
+      unsigned q = (unsigned)tid / hkv, rm = (unsigned)tid % hkv;
 #pragma unroll
-    for (int r = 0; r < GPT; ++r) {
-      const int x = tid * GPT + r;
-      tails[r] = a.seq_lens[(x < BG ? x : 0) / g.Hkv];
+      for (int r = 0; r < GPT; ++r) {
+        tails[r] = a.seq_lens[r * NT + tid < BG ? q : 0u];
+        rm += rn;
+        q += qn + (rm >= hkv ? 1u : 0u);
+        rm -= rm >= hkv ? hkv : 0u;
+      }
     }
     // every value is needed here, so none of the loads is moved into a branch
 #pragma unroll
@@ -1428,7 +1456,7 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
     int ntl = 0;
 #pragma unroll
     for (int r = 0; r < GPT; ++r) {
-      const int x = tid * GPT + r;
+      const int x = r * NT + tid;
       const int64_t len = tails[r] < 0 ? 0 : (tails[r] > g.cap ? g.cap : tails[r]);
       // a group's work is its union's tiles plus one for a partial tail
       tails[r] = x < BG ? group_work(0, SPB, len, BS) : 0;
@@ -1441,16 +1469,11 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
       cv[k] = run;
       run += v;
     }
-    int incl = run;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(incl, o, 64);
-      if (lane >= o) incl += y;
-    }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) ntl += __shfl_xor(ntl, o, 64);
+    const int incl = wave_incl_scan(run);
+    ntl = __builtin_amdgcn_readlane(wave_incl_scan(ntl), 63);
     if (lane == 63) wsum_s[w] = incl;
     if (lane == 0) wtail_s[w] = ntl;
+    if (tid == 0) own_s[0] = -1;            // no group yet (set after two more barriers)
     __syncthreads();
     int woff = 0, tot = 0, ntails = 0;
 #pragma unroll
@@ -1466,40 +1489,52 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
     __syncthreads();
     // splits per group (integer work: the total does not depend on the order)
     const int64_t UT = (int64_t)tot * SPB + ntails;
-    int sp[GPT], run2 = 0;
+    int nsp[GPT], inc[GPT];
 #pragma unroll
     for (int r = 0; r < GPT; ++r) {
-      const int x = tid * GPT + r;
-      const int v = x < BG ? group_splits((cnt_s[(x + 1) * nct] - cnt_s[x * nct]) * SPB + tails[r],
-                                          UT, W, BG)
-                           : 0;
-      sp[r] = run2;
-      run2 += v;
+      const int x = r * NT + tid;
+      nsp[r] = x < BG ? group_splits((cnt_s[(x + 1) * nct] - cnt_s[x * nct]) * SPB + tails[r],
+                                     UT, W, BG)
+                      : 0;
     }
-    int incl2 = run2;
+    // one scan per round of NT groups in use
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(incl2, o, 64);
-      if (lane >= o) incl2 += y;
+    for (int r = 0; r < GPT; ++r) inc[r] = r * NT < BG ? wave_incl_scan(nsp[r]) : 0;
+    if (lane == 63) {
+#pragma unroll
+      for (int r = 0; r < GPT; ++r) wsum2_s[r][w] = inc[r];
     }
-    if (lane == 63) wsum_s[w] = incl2;     // every read of the first scan's sums is done
     __syncthreads();
-    int woff2 = 0;
+    // group r NT + tid starts after every group of the earlier rounds, of the
+    // earlier wavefronts of its round and of the earlier lanes; the workgroup's
+    // group is the one whose splits include it (at most one thread finds it,
+    // none for workgroups past the allocation)
+    const int me = (int)blockIdx.x;
+    int carry = 0;
 #pragma unroll
-    for (int k = 0; k < NW; ++k) woff2 += k < w ? wsum_s[k] : 0;
-    const int ex2 = woff2 + incl2 - run2;
+    for (int r = 0; r < GPT; ++r) {
+      int woff2 = 0, rt = 0;
 #pragma unroll
-    for (int r = 0; r < GPT; ++r) grp_s[tid * GPT + r] = ex2 + sp[r];
-    if (tid == NT - 1) grp_s[kPropMaxGroups] = ex2 + run2;
+      for (int k = 0; k < NW; ++k) {
+        woff2 += k < w ? wsum2_s[r][k] : 0;
+        rt += wsum2_s[r][k];
+      }
+      const int x = r * NT + tid, f = carry + woff2 + inc[r] - nsp[r];
+      if (x < BG && owns_split(f, nsp[r], me)) {
+        own_s[0] = x;
+        own_s[1] = f;
+        own_s[2] = nsp[r];
+      }
+      carry += rt;
+    }
     __syncthreads();
-    // this workgroup's group: the last one starting at or before it
-    const int me = (int)blockIdx.x, bgi = find_group(grp_s, BG, me);
+    const int bgi = own_s[0];
     if (bgi < 0) return;             // workgroups past the allocation (uniform exit)
     b = bgi / g.Hkv;
     gh = bgi % g.Hkv;
-    first = grp_s[bgi];
+    first = own_s[1];
     s = me - first;
-    S = grp_s[bgi + 1] - first;
+    S = own_s[2];
     pref = cnt_s + bgi * nct;
     pbase = pref[0];
   }
@@ -1581,7 +1616,7 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
   int64_t UI;                // items (blocks) in the list
   if constexpr (DENSE) {
     UI = N;
-  } else if (!uniform) {
+  } else if constexpr (!uniform) {
     UI = pref[g.n_tiles] - pbase;   // the plan's scan holds the group's prefix
   } else {
     // exclusive prefix sum of the per-tile union counts, NT tiles at a time
@@ -1589,12 +1624,7 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
     for (int base = 0; base < g.n_tiles; base += NT) {
       const int t = base + tid;
       const int x = base == 0 ? tc0 : (t < g.n_tiles ? tc[t] : 0);
-      int incl = x;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(incl, o, 64);
-        if (lane >= o) incl += y;
-      }
+      const int incl = wave_incl_scan(x);
       if (lane == 63) wsum_s[w] = incl;
       __syncthreads();
       int woff = 0, tot = 0;
@@ -1617,6 +1647,7 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
   // item of the list, after the union's, carrying the heads that rescued it (a
   // rescued head attends it only there, also when the block is in the union for
   // other heads, which then reads it once more).
+  int jr_h = -1;                  // tid < G: head tid's rescued block, or -1
   uint32_t wb_rescued = 1u;
   if constexpr (!DENSE) {
     if (tid < G) {
@@ -1637,10 +1668,11 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
         if (!any) jr = arg;
       }
       resc_s[tid] = jr;
-      // whether the rescued block is in the union: for the union count only (the
-      // last split writes it after streaming)
-      if (s == S - 1 && jr >= 0) wb_rescued = a.wbits[bg * kMaxRescueWindow + jr];
+      jr_h = jr;
     }
+    // whether the rescued block is in the union: for the union count only (the
+    // last split writes it after streaming)
+    if (tid < G && s == S - 1 && jr_h >= 0) wb_rescued = a.wbits[bg * kMaxRescueWindow + jr_h];
     if (s == 0 && tid == 0) a.plan[bg] = make_int2(first, S);
     __syncthreads();
     if (tid == 0) {
@@ -1745,7 +1777,7 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
     if (s == S - 1) {
       // the rescued blocks' mask bits, and (for the combine) each head's rescued
       // block and how many rescued blocks are outside the union
-      if (tid < G) rxw_s[tid] = (int)wb_rescued;        // union bits at the rescued block
+      if (tid < G) rxw_s[tid] = jr_h >= 0 ? (int)wb_rescued : 1;   // union bits at the rescued block
       __syncthreads();
       if (tid == 0) {
         int extra = 0;
@@ -2191,7 +2223,12 @@ void launch_split_impl(const Geom& g, const SplitPlan& pl, const SplitArgs& sp, 
   const dim3 grid = pl.S > 0 ? dim3(pl.S, g.Hkv, g.B) : dim3(pl.W);
 #define ETA_SPL(D_, BS_, G_, T_)                                                                \
   if (g.D == D_ && g.BS == BS_ && g.G == G_)                                                    \
-    hipLaunchKernelGGL((split_kernel<D_, BS_, G_, T_, DENSE>), grid, dim3(64 * kSplitWaves), 0, stream, sp);
+    if (DENSE || pl.S > 0)                                                                      \
+      hipLaunchKernelGGL((split_kernel<D_, BS_, G_, T_, DENSE, false>), grid, dim3(64 * kSplitWaves), 0, \
+                         stream, sp);                                                           \
+    else                                                                                        \
+      hipLaunchKernelGGL((split_kernel<D_, BS_, G_, T_, DENSE, !DENSE>), grid, dim3(64 * kSplitWaves), 0, \
+                         stream, sp);
 #define ETA_SPL_G(D_, BS_, T_) \
   ETA_SPL(D_, BS_, 1, T_) ETA_SPL(D_, BS_, 2, T_) ETA_SPL(D_, BS_, 4, T_) ETA_SPL(D_, BS_, 8, T_)
   if (g.kv_dtype == ETA_DT_F32) {
@@ -2244,7 +2281,7 @@ hipError_t launch_decode(const Geom& g, const DecodeCfg& c, int q_dtype, const v
   SplitArgs sp{q, k, v, seq_lens, predict ? ws.tau : tau, ws.ids, ws.tile_cnt, ws.part_ml,
                ws.part_acc, ws.resc_best, ws.resc_info, ws.wbits, mask, ws.resc_out,
                ws.extra_union, ws.plan, ws.head_cnt, out, counts, union_counts, g, q_dtype,
-               c.beta, c.offset_a, c.self_ungated, c.rescue_window, c.plan.S};
+               c.beta, c.offset_a, c.self_ungated, c.rescue_window};
   e = with_hook(hook, ETA_KERNEL_SPLIT_DECODE, stream,
                 [&] { launch_split_impl<false>(g, c.plan, sp, stream); });
   if (e != hipSuccess) return e;
@@ -2294,7 +2331,7 @@ hipError_t launch_dense(const Geom& g, int S, int q_dtype, const void* q, const 
                         hipStream_t stream, LaunchHook hook) {
   SplitArgs sp{q, k, v, seq_lens, nullptr, nullptr, nullptr, ws.part_ml, ws.part_acc,
                nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, out,
-               nullptr, nullptr, g, q_dtype, 0.f, 0.f, 0, 0, S};
+               nullptr, nullptr, g, q_dtype, 0.f, 0.f, 0, 0};
   hipError_t e = with_hook(hook, ETA_KERNEL_DENSE_SPLIT, stream,
                            [&] { launch_split_impl<true>(g, SplitPlan{S, S * g.B * g.Hkv}, sp, stream); });
   if (e != hipSuccess || S == 1) return e;     // one split per group wrote the output

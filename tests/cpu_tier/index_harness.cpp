@@ -5,7 +5,7 @@
 // is reported by the sanitizer; the checks add the invariants the kernels rely
 // on: each union item / 64-token tile is taken by exactly one split, the
 // proportional plan gives every group at least one split and no more than W in
-// all, and every workgroup finds its group.  Exit status 0 when all hold.
+// all, and each workgroup below the number used belongs to exactly one group.  Exit status 0 when all hold.
 #include <cstdio>
 #include <cstdlib>
 #include <cstdint>
@@ -34,20 +34,26 @@ static void check_plan(const std::vector<int>& work, int W) {
   const int BG = (int)work.size();
   int64_t total = 0;
   for (int x : work) total += x;
-  int* first = new int[BG + 1];            // the kernel's grp_s
+  int* first = new int[BG + 1];            // each group's first split, then the total
   for (int x = 0; x < BG; ++x) first[x] = group_splits(work[x], total, W, BG);
   for (int x = 0; x < BG; ++x) CHECK(first[x] >= 1, "group %d has %d splits", x, first[x]);
   first[BG] = exclusive_prefix(first, BG);
   CHECK(first[BG] <= W, "plan uses %d of %d workgroups", first[BG], W);
   std::vector<int> seen(BG, 0);
   for (int me = 0; me < W; ++me) {
-    const int gi = find_group(first, BG, me);
+    // the kernel's lookup: every group tests whether it owns the workgroup
+    int gi = -1, owners = 0;
+    for (int x = 0; x < BG; ++x)
+      if (owns_split(first[x], first[x + 1] - first[x], me)) {
+        gi = x;
+        ++owners;
+      }
     if (me >= first[BG]) {
-      CHECK(gi == -1, "workgroup %d past the plan got group %d", me, gi);
+      CHECK(owners == 0, "workgroup %d past the plan got group %d", me, gi);
       continue;
     }
-    CHECK(gi >= 0 && gi < BG, "workgroup %d: group %d", me, gi);
-    if (gi < 0 || gi >= BG) continue;
+    CHECK(owners == 1, "workgroup %d: %d owning groups", me, owners);
+    if (gi < 0) continue;
     CHECK(first[gi] <= me && me < first[gi + 1], "workgroup %d outside its group's range", me);
     ++seen[gi];
   }
