@@ -49,6 +49,20 @@ ETA_HD bool owns_split(int first, int splits, int me) {
   return first <= me && me < first + splits;
 }
 
+// Sequence of groups x0, x0 + step, x0 + 2 step, ... where group x is (sequence
+// x / hkv, kv head x % hkv): one division, then one step per group.  Holds
+// q = x / hkv and rm = x % hkv of the current group.
+struct GroupStepper {
+  unsigned q, rm, qn, rn, hkv;
+  ETA_HD GroupStepper(unsigned x0, unsigned step, unsigned hkv_)
+      : q(x0 / hkv_), rm(x0 % hkv_), qn(step / hkv_), rn(step % hkv_), hkv(hkv_) {}
+  ETA_HD void next() {
+    rm += rn;                      // < 2 hkv
+    q += qn + (rm >= hkv ? 1u : 0u);
+    rm -= rm >= hkv ? hkv : 0u;
+  }
+};
+
 // Union list item `it` (pref = exclusive prefix of the per-tile union counts,
 // pref[n_tiles] = their total, it < that total) -> the screening tile holding it
 // and its slot among that tile's compacted ids: pref[tile] <= it < pref[tile + 1].

@@ -1435,16 +1435,12 @@ __global__ __launch_bounds__(64 * kSplitWaves) void split_kernel(SplitArgs a) {
       cv[k] = a.tile_cnt[i < nc ? i : 0];
     }
     {
-      // group x = r NT + tid is (sequence q, kv head rm): one division per
-      // thread, then steps of NT groups
-      const unsigned hkv = (unsigned)g.Hkv, qn = (unsigned)NT / hkv, rn = (unsigned)NT % hkv;
-      unsigned q = (unsigned)tid / hkv, rm = (unsigned)tid % hkv;
+      // group x = r NT + tid is (sequence x / Hkv, kv head x % Hkv)
+      GroupStepper gs((unsigned)tid, (unsigned)NT, (unsigned)g.Hkv);
 #pragma unroll
       for (int r = 0; r < GPT; ++r) {
-        tails[r] = a.seq_lens[r * NT + tid < BG ? q : 0u];
-        rm += rn;
-        q += qn + (rm >= hkv ? 1u : 0u);
-        rm -= rm >= hkv ? hkv : 0u;
+        tails[r] = a.seq_lens[r * NT + tid < BG ? gs.q : 0u];
+        gs.next();
       }
     }
     // every value is needed here, so none of the loads is moved into a branch
@@ -2222,13 +2218,14 @@ template <bool DENSE>
 void launch_split_impl(const Geom& g, const SplitPlan& pl, const SplitArgs& sp, hipStream_t stream) {
   const dim3 grid = pl.S > 0 ? dim3(pl.S, g.Hkv, g.B) : dim3(pl.W);
 #define ETA_SPL(D_, BS_, G_, T_)                                                                \
-  if (g.D == D_ && g.BS == BS_ && g.G == G_)                                                    \
+  if (g.D == D_ && g.BS == BS_ && g.G == G_) {                                                  \
     if (DENSE || pl.S > 0)                                                                      \
       hipLaunchKernelGGL((split_kernel<D_, BS_, G_, T_, DENSE, false>), grid, dim3(64 * kSplitWaves), 0, \
                          stream, sp);                                                           \
     else                                                                                        \
       hipLaunchKernelGGL((split_kernel<D_, BS_, G_, T_, DENSE, !DENSE>), grid, dim3(64 * kSplitWaves), 0, \
-                         stream, sp);
+                         stream, sp);                                                           \
+  }
 #define ETA_SPL_G(D_, BS_, T_) \
   ETA_SPL(D_, BS_, 1, T_) ETA_SPL(D_, BS_, 2, T_) ETA_SPL(D_, BS_, 4, T_) ETA_SPL(D_, BS_, 8, T_)
   if (g.kv_dtype == ETA_DT_F32) {

@@ -189,8 +189,26 @@ static void check_pred_rows(int J) {
   for (int j = 0; j < J; ++j) CHECK(seen[j] == 1, "J %d row %d taken %d times", J, j, seen[j]);
 }
 
+// The plan's walk over groups x0, x0 + step, ... (x = sequence * hkv + kv head):
+// the stepper's (q, rm) equal x / hkv and x % hkv at every step.
+static void check_stepper(unsigned hkv, unsigned step, unsigned steps) {
+  for (unsigned x0 = 0; x0 < step; ++x0) {
+    GroupStepper gs(x0, step, hkv);
+    for (unsigned r = 0; r < steps; ++r) {
+      const unsigned x = x0 + r * step;
+      CHECK(gs.q == x / hkv && gs.rm == x % hkv, "hkv %u step %u group %u: (%u, %u)", hkv, step,
+            x, gs.q, gs.rm);
+      gs.next();
+    }
+  }
+}
+
 int main() {
   std::mt19937_64 rng(12345);
+  // the split kernel walks groups tid + 256 r, r < 4 (up to 1024 groups)
+  for (unsigned hkv = 1; hkv <= 40; ++hkv)
+    for (unsigned step : {1u, 7u, 64u, 256u}) check_stepper(hkv, step, 6);
+  check_stepper(1024, 256, 4);
   // plans: one group, the largest table, all work in one group, no work, ragged
   const int Ws[] = {1, 2, 63, 512, 1024, 4096};
   const int BGs[] = {1, 2, 32, 255, 256, 1024};

@@ -522,6 +522,38 @@ def _random_geometry(seed: int):
     return wkw, rkw
 
 
+# The proportional plan with more (sequence, kv head) groups than a split
+# workgroup has threads: thread t then takes groups t, t + 256, ... (all four
+# rounds at 1024 groups, the most the plan takes), and with 3 kv heads the
+# groups' sequence indexes step with carries.  One 64-block screening tile per
+# group keeps every tile count in the plan's table.
+MANY_GROUPS = {
+    "320_groups_predictor": dict(B=160, Hq=4, Hkv=2, d=64, block=64, T_cap=4096, predictor=True,
+                                 target_survival=0.1),
+    "300_groups_3_kv_heads": dict(B=100, Hq=6, Hkv=3, d=64, block=64, T_cap=2048, predictor=False,
+                                  tau_const=1.5),
+    "1024_groups_predictor": dict(B=512, Hq=4, Hkv=2, d=64, block=64, T_cap=1024, predictor=True,
+                                  target_survival=0.1),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MANY_GROUPS))
+def test_proportional_plan_many_groups(name):
+    kw = dict(MANY_GROUPS[name])
+    rng = np.random.default_rng(len(name))
+    lens = rng.integers(0, kw["T_cap"] + 1, size=kw["B"]).tolist()
+    groups, tiles = kw["B"] * kw["Hkv"], (kw["T_cap"] // kw["block"] + 63) // 64
+    assert 256 < groups <= 1024 and groups * tiles <= 4096      # the proportional plan's table
+    wl = make_workload(**kw, seq_lens=lens, planted={"frac": 0.05}, seed=4000 + len(name))
+    np_in = oracle_inputs(wl)
+    calibrate_bias(wl, np_in)
+    g = run_gpu(wl)
+    orc, tau_o = run_oracle(wl, np_in)
+    stats = compare(wl, g, orc, tau_o, np_inputs=np_in, union_counts=g.union_counts)
+    say(f"[gpu] {name}: {stats}")
+    assert stats["compared"] == wl.B * wl.Hq
+
+
 @pytest.mark.parametrize("seed", range(12))
 def test_decode_random_geometries(seed):
     wkw, rkw = _random_geometry(seed)
