@@ -2058,14 +2058,16 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
   // union blocks of the (sequence, kv head): wavefront 1 of the group's first
   // head sums the union's tile counts.  The first 64 of each are loaded here
   // (every thread, from clamped indexes, so no load waits inside a branch or
-  // a loop) together with the rescue results and the group's split range, and
-  // summed at the end; tiles past 64 are read there.
+  // a loop) together with the rescue results, the sequence length and the
+  // group's split range, and summed at the end (row shifts on the vector ALUs);
+  // tiles past 64 are read there.
   const int lt = tid & 63, ti = lt < g.n_tiles ? lt : 0;
   const bool do_cnt = a.counts != nullptr && tid < 64;
   const bool do_union = a.union_counts != nullptr && hh == 0 && tid >= 64 && tid < 128;
   int cnt = a.counts != nullptr ? a.head_cnt[row * g.n_tiles + ti] : 0;
   int ucnt = a.union_counts != nullptr ? a.tile_cnt[bg * g.n_tiles + ti] : 0;
   const int rescued = (a.resc_out != nullptr && tid == 0) ? a.resc_out[row] : -1;
+  const int32_t len_raw = a.seq_lens[b];      // for the attended-token count
   const int extra = (a.extra_union != nullptr && tid == 64 && do_union) ? a.extra_union[bg] : 0;
   int first = (int)bg * a.S, S = a.S;
   if (a.plan != nullptr) {
@@ -2124,10 +2126,9 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
   if (do_cnt) {
     cnt = lt < g.n_tiles ? cnt : 0;
     for (int t = lt + 64; t < g.n_tiles; t += 64) cnt += a.head_cnt[row * g.n_tiles + t];
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
+    cnt = __builtin_amdgcn_readlane(wave_incl_scan(cnt), 63);
     if (tid == 0) {
-      const int64_t T = clamp_len(a.seq_lens, b, g.cap);
+      const int64_t T = len_raw < 0 ? 0 : (len_raw > g.cap ? g.cap : (int64_t)len_raw);
       const int64_t N = T / g.BS;
       a.counts[row] = (int32_t)(((int64_t)cnt + (rescued >= 0 ? 1 : 0)) * g.BS + (T - N * g.BS));
     }
@@ -2135,8 +2136,7 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
   if (do_union) {
     ucnt = lt < g.n_tiles ? ucnt : 0;
     for (int t = lt + 64; t < g.n_tiles; t += 64) ucnt += a.tile_cnt[bg * g.n_tiles + t];
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) ucnt += __shfl_xor(ucnt, o, 64);
+    ucnt = __builtin_amdgcn_readlane(wave_incl_scan(ucnt), 63);
     if (tid == 64) a.union_counts[bg] = ucnt + extra;
   }
 }
