@@ -2,8 +2,9 @@
 
     python -m paper_2609_20888_amd.build [-v]
 
-hipcc compiles the kernel sources and the host API to objects (in parallel)
-and links them into one shared library beside this file.  Packed-fp32
+hipcc compiles the kernel sources and the host API to objects (in parallel;
+the decode kernels' source as three objects, selected by ETA_PART) and links
+them into one shared library beside this file.  Packed-fp32
 instruction selection is disabled for device code
 (`-target-feature -packed-fp32-ops`); the prefill source keeps MFMA
 accumulators in the ordinary vector registers (`-amdgpu-mfma-vgpr-form`).
@@ -20,6 +21,10 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libeta.so")
 SOURCES = [os.path.join(CSRC, f) for f in ("eta_kernels.hip", "eta_prefill.hip", "eta_api.cpp")]
+# (source, extra flags, object name): eta_kernels.hip holds split decode on bf16
+# caches in part 1, on fp32 caches in part 2, and everything else in part 0
+UNITS = [(SOURCES[0], [f"-DETA_PART={p}"], f"eta_kernels.{p}.o") for p in (0, 1, 2)] + \
+        [(src, [], os.path.basename(src) + ".o") for src in SOURCES[1:]]
 ARCH = "gfx950"
 
 
@@ -52,12 +57,12 @@ def _clean(stderr: str) -> str:
     return "\n".join(l for l in stderr.splitlines() if _NOISE not in l)
 
 
-def build(verbose: bool = False, jobs: int = 3) -> str:
+def build(verbose: bool = False, jobs: int = 5) -> str:
     """Compile every source to an object (in parallel), then link libeta.so."""
     objdir = tempfile.mkdtemp(prefix="eta_build_")
     try:
-        cmds = [[hipcc(), *_flags(src), "-c", src, "-o",
-                 os.path.join(objdir, os.path.basename(src) + ".o")] for src in SOURCES]
+        cmds = [[hipcc(), *_flags(src), *extra, "-c", src, "-o", os.path.join(objdir, obj)]
+                for src, extra, obj in UNITS]
         procs = []
         for cmd in cmds:
             if verbose:

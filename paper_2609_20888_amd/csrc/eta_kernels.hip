@@ -32,6 +32,13 @@
 #include "eta_index.h"
 #include "eta_internal.h"
 
+// The source compiles to three objects, in parallel (ETA_PART): 0 holds every
+// kernel but split decode, and the host launchers; 1 and 2 hold split decode
+// on bf16 and fp32 caches.
+#ifndef ETA_PART
+#define ETA_PART 0
+#endif
+
 namespace eta {
 namespace {
 
@@ -636,6 +643,7 @@ __device__ __forceinline__ void pred_reduce(const float (&acc)[NC], int ncols, f
   __syncthreads();
 }
 
+#if ETA_PART == 0
 __global__ __launch_bounds__(kPredThreads) void predict_kernel(const void* __restrict__ q,
                                                                int q_dtype,
                                                                const float* __restrict__ W,
@@ -663,6 +671,7 @@ __global__ __launch_bounds__(kPredThreads) void predict_kernel(const void* __res
   pred_reduce<kPredCols>(acc, ncols, red, &t);
   if ((int)threadIdx.x < ncols) tau[(int64_t)b * Hq + h0 + threadIdx.x] = t + bias[h0 + threadIdx.x];
 }
+#endif
 
 // ---------------------------------------------------------------- screening
 //
@@ -1036,6 +1045,8 @@ __device__ __forceinline__ uint16_t load_v_one(const uint16_t* p) {
 // MFMAs) so the scores keep ~16 mantissa bits; fp32 K uses the vector ALUs.
 
 
+}  // namespace
+
 struct SplitArgs {
   const void* q;
   const void* k;
@@ -1065,6 +1076,8 @@ struct SplitArgs {
   int self_ungated;
   int c;                     // rescue window (blocks)
 };
+
+namespace {
 
 
 // Gated score S~ = S sigmoid(beta (S - tau_eff)); -inf when the head does not
@@ -1970,6 +1983,7 @@ struct CalibSolveArgs {
   double beta, lo, hi;
 };
 
+#if ETA_PART == 0
 __global__ __launch_bounds__(256) void calib_solve_kernel(CalibSolveArgs a) {
   constexpr int PER = kCalibMaxBins / 256;
   __shared__ double red[4];
@@ -2001,6 +2015,7 @@ __global__ __launch_bounds__(256) void calib_solve_kernel(CalibSolveArgs a) {
     if (a.target_out != nullptr) a.target_out[h] = tot > 0.0 ? target : __builtin_nan("");
   }
 }
+#endif
 
 // ---------------------------------------------------------------- combine
 
@@ -2145,6 +2160,39 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(CombineArgs a) {
 
 // ---------------------------------------------------------------- launchers
 
+// Split decode on one cache type (defined in object 1 for bf16, 2 for fp32).
+template <bool DENSE, typename KVT>
+void launch_split_kv(const Geom& g, const SplitPlan& pl, const SplitArgs& sp, hipStream_t stream);
+
+#if ETA_PART == 1 || ETA_PART == 2
+template <bool DENSE, typename KVT>
+void launch_split_kv(const Geom& g, const SplitPlan& pl, const SplitArgs& sp, hipStream_t stream) {
+  const dim3 grid = pl.S > 0 ? dim3(pl.S, g.Hkv, g.B) : dim3(pl.W);
+#define ETA_SPL(D_, BS_, G_)                                                                    \
+  if (g.D == D_ && g.BS == BS_ && g.G == G_) {                                                  \
+    if (DENSE || pl.S > 0)                                                                      \
+      hipLaunchKernelGGL((split_kernel<D_, BS_, G_, KVT, DENSE, false>), grid, dim3(64 * kSplitWaves), 0, \
+                         stream, sp);                                                           \
+    else                                                                                        \
+      hipLaunchKernelGGL((split_kernel<D_, BS_, G_, KVT, DENSE, !DENSE>), grid, dim3(64 * kSplitWaves), 0, \
+                         stream, sp);                                                           \
+  }
+#define ETA_SPL_G(D_, BS_) ETA_SPL(D_, BS_, 1) ETA_SPL(D_, BS_, 2) ETA_SPL(D_, BS_, 4) ETA_SPL(D_, BS_, 8)
+  ETA_SPL_G(64, 64) ETA_SPL_G(64, 128) ETA_SPL_G(128, 64) ETA_SPL_G(128, 128)
+#undef ETA_SPL_G
+#undef ETA_SPL
+}
+#if ETA_PART == 1
+template void launch_split_kv<false, uint16_t>(const Geom&, const SplitPlan&, const SplitArgs&, hipStream_t);
+template void launch_split_kv<true, uint16_t>(const Geom&, const SplitPlan&, const SplitArgs&, hipStream_t);
+#else
+template void launch_split_kv<false, float>(const Geom&, const SplitPlan&, const SplitArgs&, hipStream_t);
+template void launch_split_kv<true, float>(const Geom&, const SplitPlan&, const SplitArgs&, hipStream_t);
+#endif
+#endif
+
+#if ETA_PART == 0
+
 hipError_t launch_summaries(const Geom& g, const void* k, const int32_t* seq_lens,
                             const int32_t* prev_lens, int max_new_blocks, int sub_block,
                             const eta_summary_t& s, hipStream_t stream, LaunchHook hook) {
@@ -2216,27 +2264,10 @@ void launch_screen_impl(const Geom& g, const ScreenArgs& sa, hipStream_t stream)
 
 template <bool DENSE>
 void launch_split_impl(const Geom& g, const SplitPlan& pl, const SplitArgs& sp, hipStream_t stream) {
-  const dim3 grid = pl.S > 0 ? dim3(pl.S, g.Hkv, g.B) : dim3(pl.W);
-#define ETA_SPL(D_, BS_, G_, T_)                                                                \
-  if (g.D == D_ && g.BS == BS_ && g.G == G_) {                                                  \
-    if (DENSE || pl.S > 0)                                                                      \
-      hipLaunchKernelGGL((split_kernel<D_, BS_, G_, T_, DENSE, false>), grid, dim3(64 * kSplitWaves), 0, \
-                         stream, sp);                                                           \
-    else                                                                                        \
-      hipLaunchKernelGGL((split_kernel<D_, BS_, G_, T_, DENSE, !DENSE>), grid, dim3(64 * kSplitWaves), 0, \
-                         stream, sp);                                                           \
-  }
-#define ETA_SPL_G(D_, BS_, T_) \
-  ETA_SPL(D_, BS_, 1, T_) ETA_SPL(D_, BS_, 2, T_) ETA_SPL(D_, BS_, 4, T_) ETA_SPL(D_, BS_, 8, T_)
-  if (g.kv_dtype == ETA_DT_F32) {
-    ETA_SPL_G(64, 64, float) ETA_SPL_G(64, 128, float) ETA_SPL_G(128, 64, float)
-    ETA_SPL_G(128, 128, float)
-  } else {
-    ETA_SPL_G(64, 64, uint16_t) ETA_SPL_G(64, 128, uint16_t) ETA_SPL_G(128, 64, uint16_t)
-    ETA_SPL_G(128, 128, uint16_t)
-  }
-#undef ETA_SPL_G
-#undef ETA_SPL
+  if (g.kv_dtype == ETA_DT_F32)
+    launch_split_kv<DENSE, float>(g, pl, sp, stream);
+  else
+    launch_split_kv<DENSE, uint16_t>(g, pl, sp, stream);
 }
 
 void launch_combine_impl(const Geom& g, const CombineArgs& ca, hipStream_t stream) {
@@ -2374,5 +2405,7 @@ hipError_t scratch_address(hipStream_t stream, void** out) {
   *out = addr[dev];
   return hipSuccess;
 }
+
+#endif  // ETA_PART == 0
 
 }  // namespace eta
