@@ -531,7 +531,9 @@ __global__ __launch_bounds__(256) void summaries_kernel(const KVT* __restrict__ 
 // added in order; the bias is added last.
 
 constexpr int kPredThreads = 256;
+#if ETA_PART == 0
 constexpr int kPredCols = 4;                    // heads per stand-alone predictor workgroup
+#endif
 constexpr int kPredStep = 4 * kPredThreads;     // rows per pass
 static_assert(kPredStep == 1024, "pred_row4 (eta_index.h) takes 1024 rows per pass");
 // The first kPredPass passes of each thread are loaded into registers by
