@@ -554,6 +554,25 @@ def test_proportional_plan_many_groups(name):
     assert stats["compared"] == wl.B * wl.Hq
 
 
+@pytest.mark.parametrize("num_splits", [0, 3])
+def test_uniform_plan_many_sequences(num_splits):
+    # More (sequence, kv head) groups than the proportional plan's table holds
+    # (1040 > 1024): the uniform plan on a (S, Hkv, B) grid with B = 520, by
+    # default one split per group (the split workgroup writes the output, no
+    # combine), else three splits per group and the combine.
+    rng = np.random.default_rng(77)
+    lens = rng.integers(0, 1025, size=520).tolist()
+    wl = make_workload(B=520, Hq=4, Hkv=2, d=64, block=64, seq_lens=lens, T_cap=1024,
+                       planted={"frac": 0.05}, predictor=True, target_survival=0.2, seed=78)
+    np_in = oracle_inputs(wl)
+    calibrate_bias(wl, np_in)
+    g = run_gpu(wl, num_splits=num_splits)
+    orc, tau_o = run_oracle(wl, np_in)
+    stats = compare(wl, g, orc, tau_o, np_inputs=np_in, union_counts=g.union_counts)
+    say(f"[gpu] uniform plan, 520 sequences, splits {num_splits}: {stats}")
+    assert stats["compared"] == wl.B * wl.Hq
+
+
 @pytest.mark.parametrize("seed", range(12))
 def test_decode_random_geometries(seed):
     wkw, rkw = _random_geometry(seed)
